@@ -1,0 +1,262 @@
+"""Plain CPU reference for InfLLM's block-memory attention step (arXiv 2402.04617, Section 3).
+
+TEST INFRASTRUCTURE ONLY.  This module is the oracle that the device library is
+checked against.  Only the tests, the package smoke check and the benchmark's
+CPU-baseline leg may import it; the product path never does.  It shares no code
+with the HIP library and computes everything in float64 from the exact input
+values (bf16/fp32 inputs widen to float64 without rounding).
+
+Notation follows the paper: past length l_P, initial tokens l_I, local window
+l_L, unit (block) size l_bs, representative tokens per unit r_k, units loaded per
+step k_m, current tokens l_X.  For grouped-query attention the paper is silent;
+the readings used here are listed with each function.
+
+Every function has a pin in tests/test_oracle_pins.py (brute force, closed
+forms, special cases reducing to library attention, invariants).
+"""
+from __future__ import annotations
+
+import dataclasses
+from typing import Dict, List, Optional, Sequence, Tuple
+
+import numpy as np
+
+
+@dataclasses.dataclass(frozen=True)
+class Params:
+    n_q_heads: int
+    n_kv_heads: int
+    head_dim: int
+    n_init: int       # l_I
+    n_local: int      # l_L
+    block_size: int   # l_bs
+    n_repr: int       # r_k
+    topk: int         # k_m
+    sm_scale: float = 1.0
+
+    @property
+    def group(self) -> int:
+        return self.n_q_heads // self.n_kv_heads
+
+
+@dataclasses.dataclass(frozen=True)
+class Partition:
+    n_init: int       # |I| (fewer than l_I while the past is short)
+    n_units: int      # whole units formed from the evicted tokens E
+    local_begin: int  # first position of L; L = [local_begin, l_P)
+
+
+def partition(past_len: int, p: Params) -> Partition:
+    """Split of the past key-values P (Section 3.1, "Overall Framework").
+
+    I = the first l_I tokens, L = the last l_L tokens, E = the tokens between.
+    E is cut into consecutive units of l_bs tokens (Section 3.2).  Reading where
+    the paper is silent: only whole units are formed; a trailing remainder of
+    fewer than l_bs evicted tokens stays attended as part of L, so L holds
+    between l_L and l_L + l_bs - 1 tokens once eviction has begun.
+    """
+    n_init = min(p.n_init, past_len)
+    evicted = past_len - p.n_init - p.n_local
+    n_units = evicted // p.block_size if evicted > 0 else 0
+    return Partition(n_init, n_units, n_init + n_units * p.block_size)
+
+
+def unit_start(unit: int, p: Params) -> int:
+    """First position of memory unit `unit`; units tile E starting right after I (Section 3.2)."""
+    return p.n_init + unit * p.block_size
+
+
+def representative_scores(q_group: np.ndarray, k_head: np.ndarray, unit: int, p: Params) -> np.ndarray:
+    """Representative score r_m of every token m of one unit (Section 3.2, "Block-Level Memory Units").
+
+    r_m = (1/l_L) * sum_{j=1..l_L} q_{m+j} . k_m : the mean dot product of token m's
+    key with the queries of the l_L tokens that follow it.  GQA reading: the
+    query side is also averaged over the G query heads that share the kv head, so
+    r_m = 1/(l_L*G) * sum_h sum_j q^h_{m+j} . k_m.
+
+    q_group: [G][S][D] queries of the group's heads (positions up to m + l_L must
+    exist); k_head: [S][D] keys of the kv head.  Returns float64 [l_bs].
+    """
+    G = q_group.shape[0]
+    m0 = unit_start(unit, p)
+    lbs, lL = p.block_size, p.n_local
+    # Window queries of all tokens of the unit: positions m0+1 .. m0+l_bs-1+l_L,
+    # summed over the group's heads (sum_h q^h . k = (sum_h q^h) . k).
+    qw = np.asarray(q_group[:, m0 + 1: m0 + lbs + lL, :], dtype=np.float64).sum(axis=0)
+    ku = np.asarray(k_head[m0: m0 + lbs, :], dtype=np.float64)
+    dots = qw @ ku.T  # dots[a, t] = q~_{m0+1+a} . k_{m0+t}
+    r = np.empty(lbs)
+    for t in range(lbs):
+        # j = 1..l_L  <->  window row a = t + j - 1 = t .. t + l_L - 1
+        r[t] = dots[t: t + lL, t].sum()
+    return r / (lL * G)
+
+
+def top_indices(values: np.ndarray, count: int) -> np.ndarray:
+    """The `count` largest entries of `values`, returned as ascending indices.
+
+    Ties go to the lower index (reading: the paper does not say).  Done as
+    repeated arg-max, which returns the first (lowest) index among equal maxima.
+    """
+    vals = np.array(values, dtype=np.float64, copy=True)
+    count = min(count, vals.shape[0])
+    chosen = []
+    for _ in range(count):
+        i = int(np.argmax(vals))
+        chosen.append(i)
+        vals[i] = -np.inf
+    return np.array(sorted(chosen), dtype=np.int64)
+
+
+def representatives(r: np.ndarray, p: Params) -> np.ndarray:
+    """R(B): the r_k tokens of a unit with the highest r_m (Section 3.2), as ascending offsets in the unit."""
+    return top_indices(r, p.n_repr)
+
+
+def unit_relevance(q_chunk_group: np.ndarray, k_head: np.ndarray, rep_pos: np.ndarray) -> np.ndarray:
+    """sim(X, B) = sum_{i=1..l_X} sum_{j=1..r_k} q_{i+l_P} . k^B_{b_j} for every unit B (Section 3.2).
+
+    No normalisation (the formula has none).  GQA reading: one score per kv head,
+    summed over the query heads of its group as well.
+    q_chunk_group: [G][l_X][D]; rep_pos: [n_units][r_k] absolute key positions.
+    Returns float64 [n_units].
+    """
+    if rep_pos.shape[0] == 0:
+        return np.zeros(0)
+    D = k_head.shape[1]
+    qx = np.asarray(q_chunk_group, dtype=np.float64).reshape(-1, D)        # every (head, i)
+    keys = np.asarray(k_head[rep_pos.reshape(-1)], dtype=np.float64)        # every (unit, j)
+    dots = qx @ keys.T                                                        # all q_i . k_{b_j}
+    return dots.reshape(qx.shape[0], rep_pos.shape[0], rep_pos.shape[1]).sum(axis=(0, 2))
+
+
+def select_units(sim: np.ndarray, p: Params, k: Optional[int] = None) -> np.ndarray:
+    """Memory lookup f(X, E): the k_m units with the highest sim (Section 3.2, "memory lookup").
+
+    Returns k_m entries: the min(k_m, n_units) chosen unit ids ascending, then -1.
+    """
+    k = p.topk if k is None else k
+    out = np.full(k, -1, dtype=np.int64)
+    chosen = top_indices(sim, k) if k > 0 else np.zeros(0, dtype=np.int64)
+    out[: chosen.shape[0]] = chosen
+    return out
+
+
+def context_positions(past_len: int, sel: np.ndarray, p: Params) -> np.ndarray:
+    """Positions of the current key-value cache C = Concat(I, f(X, E), L) (Section 3.1)."""
+    part = partition(past_len, p)
+    pos = [np.arange(part.n_init)]
+    for b in sel:
+        if b >= 0:
+            s = unit_start(int(b), p)
+            pos.append(np.arange(s, s + p.block_size))
+    pos.append(np.arange(part.local_begin, past_len))
+    return np.concatenate(pos).astype(np.int64)
+
+
+def attend(q_chunk: np.ndarray, k: np.ndarray, v: np.ndarray, past_len: int,
+           sel: np.ndarray, p: Params) -> Tuple[np.ndarray, np.ndarray]:
+    """O = Attn[Q X, Concat(C_k, K X), Concat(C_v, V X)] (Section 3.1).
+
+    One softmax per query over the union of C and the current tokens X, causal
+    inside X (query i sees X positions up to its own).  Logits are
+    sm_scale * q . k; sm_scale = 1 when the inputs come pre-scaled.
+    q_chunk: [Hq][l_X][D]; k, v: [Hkv][S][D]; sel: [Hkv][k] unit ids (-1 = none).
+    Returns O float64 [Hq][l_X][D] and natural-log lse [Hq][l_X].
+    """
+    Hq, nq, D = q_chunk.shape
+    G = p.group
+    O = np.empty((Hq, nq, D))
+    lse = np.empty((Hq, nq))
+    causal = np.tril(np.ones((nq, nq), dtype=bool))
+    for g in range(p.n_kv_heads):
+        pos = context_positions(past_len, sel[g], p)
+        kc = np.asarray(k[g, pos], dtype=np.float64)
+        vc = np.asarray(v[g, pos], dtype=np.float64)
+        kx = np.asarray(k[g, past_len: past_len + nq], dtype=np.float64)
+        vx = np.asarray(v[g, past_len: past_len + nq], dtype=np.float64)
+        for h in range(g * G, (g + 1) * G):
+            qh = np.asarray(q_chunk[h], dtype=np.float64)
+            z = np.concatenate([p.sm_scale * (qh @ kc.T),
+                                np.where(causal, p.sm_scale * (qh @ kx.T), -np.inf)], axis=1)
+            zmax = z.max(axis=1, keepdims=True)
+            w = np.exp(z - zmax)
+            s = w.sum(axis=1, keepdims=True)
+            O[h] = (w / s) @ np.concatenate([vc, vx], axis=0)
+            lse[h] = (zmax + np.log(s))[:, 0]
+    return O, lse
+
+
+def lse_merge(outs: Sequence[np.ndarray], lses: Sequence[np.ndarray]) -> Tuple[np.ndarray, np.ndarray]:
+    """Combine softmax-normalised partial attentions over disjoint key sets into the single softmax.
+
+    LSE = log sum_s exp(lse_s);  O = sum_s exp(lse_s - LSE) O_s.  A part with no
+    keys has lse_s = -inf and weight 0.  This is what the single Attn of
+    Section 3.1 equals when its key set is split.
+    """
+    L = np.stack([np.asarray(x, dtype=np.float64) for x in lses])
+    M = L.max(axis=0)
+    Ms = np.where(np.isfinite(M), M, 0.0)
+    w = np.exp(L - Ms)
+    tot = w.sum(axis=0)
+    lse = Ms + np.log(tot)
+    O = sum(w[s][..., None] * np.asarray(outs[s], dtype=np.float64) for s in range(len(outs)))
+    return O / tot[..., None], lse
+
+
+class StreamOracle:
+    """Runs the per-step lookup + attention of one layer over a stream of steps.
+
+    q: [B][Hq][S][D], k, v: [B][Hkv][S][D] (float32 or float64 arrays holding the
+    exact input values).  Units are a pure function of Q and K, so each unit's
+    representatives are computed once on first use and cached; any step can be
+    evaluated alone.
+    """
+
+    def __init__(self, q: np.ndarray, k: np.ndarray, v: np.ndarray, p: Params):
+        self.q, self.k, self.v, self.p = q, k, v, p
+        self._rep: Dict[Tuple[int, int, int], np.ndarray] = {}
+        self._rscore: Dict[Tuple[int, int, int], np.ndarray] = {}
+
+    def repr_scores(self, b: int, g: int, unit: int) -> np.ndarray:
+        key = (b, g, unit)
+        if key not in self._rscore:
+            G = self.p.group
+            self._rscore[key] = representative_scores(self.q[b, g * G:(g + 1) * G], self.k[b, g], unit, self.p)
+        return self._rscore[key]
+
+    def repr_offsets(self, b: int, g: int, unit: int) -> np.ndarray:
+        key = (b, g, unit)
+        if key not in self._rep:
+            self._rep[key] = representatives(self.repr_scores(b, g, unit), self.p)
+        return self._rep[key]
+
+    def rep_positions(self, b: int, g: int, n_units: int) -> np.ndarray:
+        if n_units == 0:
+            return np.zeros((0, self.p.n_repr), dtype=np.int64)
+        return np.stack([unit_start(u, self.p) + self.repr_offsets(b, g, u) for u in range(n_units)])
+
+    def scores(self, b: int, past_len: int, n_q: int) -> np.ndarray:
+        """sim for every (kv head, unit) at this step: float64 [Hkv][n_units]."""
+        p = self.p
+        G = p.group
+        nu = partition(past_len, p).n_units
+        out = np.zeros((p.n_kv_heads, nu))
+        for g in range(p.n_kv_heads):
+            qx = self.q[b, g * G:(g + 1) * G, past_len:past_len + n_q]
+            out[g] = unit_relevance(qx, self.k[b, g], self.rep_positions(b, g, nu))
+        return out
+
+    def step(self, b: int, past_len: int, n_q: int, sel: Optional[np.ndarray] = None) -> dict:
+        """One step of sequence b: scores, selection, output and lse.
+
+        `sel` overrides the lookup (used by tests that fix the selection).
+        """
+        p = self.p
+        sim = self.scores(b, past_len, n_q)
+        if sel is None:
+            sel = np.stack([select_units(sim[g], p) for g in range(p.n_kv_heads)])
+        qx = self.q[b, :, past_len:past_len + n_q]
+        O, lse = attend(qx, self.k[b], self.v[b], past_len, sel, p)
+        return {"scores": sim, "idx": sel, "out": O, "lse": lse,
+                "n_units": partition(past_len, p).n_units}

@@ -1,0 +1,158 @@
+"""The CPU oracle against its pins, plus planted-mistake checks showing the pins bite.
+
+CPU only.  Each mutant below is a plausible slip in writing the oracle from the
+paper (a window off by one, a dropped 1/G, ties broken the other way, causal
+mask dropped, ...).  The mutant replaces the oracle function for the duration
+of one test, and at least one pin must then fail.
+"""
+import numpy as np
+import pytest
+
+from oracle import infllm_oracle as O
+from tests import oracle_pins as P
+
+
+@pytest.mark.parametrize("check", P.ALL_CHECKS, ids=lambda c: c.__name__)
+def test_pin(check):
+    check()
+
+
+# ------------------------------------------------------------------ mutants
+_orig = {name: getattr(O, name) for name in
+         ("partition", "representative_scores", "top_indices", "unit_relevance", "attend",
+          "lse_merge", "context_positions", "select_units", "unit_start")}
+
+
+def _mut_partition_drop_remainder(past_len, p):
+    # remainder of E discarded instead of kept in L
+    part = _orig["partition"](past_len, p)
+    if part.n_units:
+        return O.Partition(part.n_init, part.n_units, max(part.local_begin, past_len - p.n_local))
+    return part
+
+
+def _mut_partition_ceil_units(past_len, p):
+    ev = past_len - p.n_init - p.n_local
+    n = -(-ev // p.block_size) if ev > 0 else 0
+    n_init = min(p.n_init, past_len)
+    return O.Partition(n_init, n, min(past_len, n_init + n * p.block_size))
+
+
+def _mut_repr_window_shift(q_group, k_head, unit, p):
+    # j = 0 .. l_L-1 instead of 1 .. l_L
+    G = q_group.shape[0]
+    m0 = O.unit_start(unit, p)
+    qw = np.asarray(q_group[:, m0: m0 + p.block_size + p.n_local - 1, :], float).sum(axis=0)
+    dots = qw @ np.asarray(k_head[m0:m0 + p.block_size], float).T
+    return np.array([dots[t:t + p.n_local, t].sum() for t in range(p.block_size)]) / (p.n_local * G)
+
+
+def _mut_repr_no_group_mean(q_group, k_head, unit, p):
+    return _orig["representative_scores"](q_group, k_head, unit, p) * q_group.shape[0]
+
+
+def _mut_repr_first_head_only(q_group, k_head, unit, p):
+    return _orig["representative_scores"](q_group[:1], k_head, unit, p)
+
+
+def _mut_topk_high_index_ties(values, count):
+    vals = np.array(values, float)
+    order = sorted(range(len(vals)), key=lambda i: (-vals[i], -i))
+    return np.array(sorted(order[:min(count, len(vals))]), dtype=np.int64)
+
+
+def _mut_topk_smallest(values, count):
+    return _orig["top_indices"](-np.asarray(values, float), count)
+
+
+def _mut_relevance_sign(q, k, rep):
+    return -_orig["unit_relevance"](q, k, rep)
+
+
+def _mut_relevance_one_rep(q, k, rep):
+    return _orig["unit_relevance"](q, k, rep[:, :1])
+
+
+def _mut_attend_no_causal(q_chunk, k, v, past_len, sel, p):
+    # current tokens fully visible to each other
+    Hq, nq, D = q_chunk.shape
+    G = p.group
+    out, lse = np.empty((Hq, nq, D)), np.empty((Hq, nq))
+    for g in range(p.n_kv_heads):
+        pos = np.concatenate([O.context_positions(past_len, sel[g], p),
+                              np.arange(past_len, past_len + nq)])
+        for h in range(g * G, (g + 1) * G):
+            z = p.sm_scale * q_chunk[h] @ k[g, pos].T
+            m = z.max(axis=1, keepdims=True)
+            w = np.exp(z - m)
+            out[h] = (w / w.sum(1, keepdims=True)) @ v[g, pos]
+            lse[h] = (m + np.log(w.sum(1, keepdims=True)))[:, 0]
+    return out, lse
+
+
+def _mut_attend_no_scale(q_chunk, k, v, past_len, sel, p):
+    import dataclasses
+    return _orig["attend"](q_chunk, k, v, past_len, sel, dataclasses.replace(p, sm_scale=1.0))
+
+
+def _mut_attend_log2_lse(q_chunk, k, v, past_len, sel, p):
+    o, l = _orig["attend"](q_chunk, k, v, past_len, sel, p)
+    return o, l / np.log(2.0)
+
+
+def _mut_merge_unnormalised(outs, lses):
+    # weights exp(lse_s - max) applied but never divided by their sum
+    L = np.stack(lses)
+    M = L.max(axis=0)
+    w = np.exp(L - M)
+    return sum(w[s][..., None] * outs[s] for s in range(len(outs))), M + np.log(w.sum(axis=0))
+
+
+def _mut_unit_start_off_by_one(unit, p):
+    return p.n_init + unit * p.block_size + 1
+
+
+def _mut_context_drop_init(past_len, sel, p):
+    pos = _orig["context_positions"](past_len, sel, p)
+    return pos[O.partition(past_len, p).n_init:]
+
+
+def _mut_select_top_km_minus_1(sim, p, k=None):
+    k = p.topk if k is None else k
+    out = _orig["select_units"](sim, p, k)
+    c = (out >= 0).sum()
+    if c:
+        out[c - 1] = -1
+    return out
+
+
+MUTANTS = [
+    ("partition", _mut_partition_drop_remainder),
+    ("partition", _mut_partition_ceil_units),
+    ("representative_scores", _mut_repr_window_shift),
+    ("representative_scores", _mut_repr_no_group_mean),
+    ("representative_scores", _mut_repr_first_head_only),
+    ("top_indices", _mut_topk_high_index_ties),
+    ("top_indices", _mut_topk_smallest),
+    ("unit_relevance", _mut_relevance_sign),
+    ("unit_relevance", _mut_relevance_one_rep),
+    ("attend", _mut_attend_no_causal),
+    ("attend", _mut_attend_no_scale),
+    ("attend", _mut_attend_log2_lse),
+    ("lse_merge", _mut_merge_unnormalised),
+    ("unit_start", _mut_unit_start_off_by_one),
+    ("context_positions", _mut_context_drop_init),
+    ("select_units", _mut_select_top_km_minus_1),
+]
+
+
+@pytest.mark.parametrize("name,mutant", MUTANTS, ids=[m.__name__ for _, m in MUTANTS])
+def test_pins_catch_planted_mistake(monkeypatch, name, mutant):
+    monkeypatch.setattr(O, name, mutant)
+    failed = []
+    for check in P.ALL_CHECKS:
+        try:
+            check()
+        except (AssertionError, IndexError, ValueError):
+            failed.append(check.__name__)
+    assert failed, f"no pin caught mutant {mutant.__name__} of {name}"
