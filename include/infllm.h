@@ -1,0 +1,199 @@
+/*
+ * infllm.h - C ABI of the block-memory attention step of InfLLM
+ * (arXiv 2402.04617, "InfLLM: Training-Free Long-Context Extrapolation for LLMs
+ * with an Efficient Context Memory"), for AMD Instinct MI355X (gfx950).
+ *
+ * One attention layer processes a stream in steps (Section 3.1).  A step has
+ * past key-values P (length l_P) and current tokens X (length l_X: the chunk size
+ * while encoding, 1 while decoding).  P splits into initial tokens I (the first
+ * l_I), local tokens L (the last l_L) and evicted tokens E between them.  E is cut
+ * into memory units of l_bs tokens; each unit is represented by its r_k tokens of
+ * highest representative score r_m (Section 3.2).  Each step scores every unit
+ * against X, loads the k_m best, and attends over Concat(I, units, L, X) with one
+ * softmax, causal inside X.
+ *
+ * Conventions for every call
+ *  - Every pointer argument except the params/memory structs and the partition
+ *    outputs is DEVICE memory owned by the caller.  The library never allocates,
+ *    frees or retains memory, and keeps no state between calls.
+ *  - Tensors are dense row-major, innermost dimension contiguous, 16-byte aligned.
+ *    "dtype" tensors are bfloat16 (INFLLM_BF16) or float32 (INFLLM_F32).
+ *  - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL = the
+ *    default stream).  Device faults surface at the caller's next synchronize.
+ *  - Arguments are validated on the host before anything is enqueued; on any
+ *    error status nothing is enqueued and no output is touched.  A failed launch
+ *    returns INFLLM_E_LAUNCH.  No C++ exception crosses this interface.
+ *  - Calls on different streams that write the same buffers race; calls are
+ *    otherwise re-entrant.
+ *  - All sequences of a batch share one past length.
+ */
+#ifndef INFLLM_H
+#define INFLLM_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  INFLLM_OK = 0,
+  INFLLM_E_NULL = 1,        /* a required pointer is NULL */
+  INFLLM_E_SHAPE = 2,       /* inconsistent sizes or parameters */
+  INFLLM_E_RANGE = 3,       /* positions, units or ring slots outside what the memory holds */
+  INFLLM_E_UNSUPPORTED = 4, /* valid request this build does not implement (e.g. head_dim) */
+  INFLLM_E_WORKSPACE = 5,   /* workspace smaller than required */
+  INFLLM_E_LAUNCH = 6,      /* a kernel launch failed */
+  INFLLM_E_DEVICE = 7       /* the current device is not a usable gfx950 GPU */
+} infllm_status;
+
+typedef enum { INFLLM_F32 = 0, INFLLM_BF16 = 1 } infllm_dtype;
+
+/* Method parameters (Sections 3.1-3.2; the paper's symbols in comments). */
+typedef struct {
+  int32_t n_q_heads;  /* Hq: query heads; Hq % Hkv == 0.  Query head h reads kv head h / (Hq/Hkv). */
+  int32_t n_kv_heads; /* Hkv */
+  int32_t head_dim;   /* D: 64 or 128 */
+  int32_t n_init;     /* l_I >= 0: initial tokens always attended */
+  int32_t n_local;    /* l_L >= 1: local window */
+  int32_t block_size; /* l_bs in [1, 256]: tokens per memory unit */
+  int32_t n_repr;     /* r_k in [1, l_bs]: representative tokens per unit */
+  int32_t topk;       /* k_m >= 0: units loaded per step */
+  int32_t dtype;      /* infllm_dtype of q, k, v and the attention output */
+  float sm_scale;     /* softmax logit scale (1 when q or k arrive pre-scaled) */
+} infllm_params;
+
+/*
+ * The layer's context memory, all device memory owned by the caller.
+ *   k, v       [batch][Hkv][capacity][D] dtype.  Token-ordered store of P (and of X
+ *              once appended): I, the units and L are views of it, so eviction
+ *              moves no data.
+ *   repr_idx   [batch][Hkv][max_units][r_k] int32: offsets inside the unit of its
+ *              representative tokens R(B), ascending.  Written by infllm_build_units.
+ *   unit_ksum  [batch][Hkv][D/4][max_units][4] float32: per unit, the sum of its
+ *              representative keys, sum_{j in R(B)} k_j, stored four dimensions per
+ *              16-byte cell, unit-contiguous (the layout unit scoring streams).
+ *   qprefix    [batch][Hkv][ring][D] float64 ring: slot (t mod ring) holds
+ *              sum_{p <= t} sum_{h in group} q^h_p, the running sum of the group's
+ *              queries.  Written by infllm_append, read by infllm_build_units.
+ * Unit b of E covers positions [l_I + b*l_bs, l_I + (b+1)*l_bs).
+ */
+typedef struct {
+  int32_t batch;
+  int64_t capacity;
+  void* k;
+  void* v;
+  int32_t max_units;
+  int32_t* repr_idx;
+  float* unit_ksum;
+  double* qprefix;
+  int32_t ring;
+} infllm_memory;
+
+/* Partition of P at past length l_P (Section 3.1): |I| = min(l_I, l_P);
+ * n_units = floor((l_P - l_I - l_L) / l_bs) whole units (0 if negative);
+ * L = [local_begin, l_P) with local_begin = |I| + n_units*l_bs.  Evicted tokens
+ * that do not fill a whole unit stay in L.  Host only; outputs are host pointers. */
+infllm_status infllm_partition(const infllm_params* p, int64_t past_len, int64_t* n_init,
+                               int32_t* n_units, int64_t* local_begin);
+
+/* Bytes of device workspace that infllm_score_units and infllm_chunk_attend need
+ * for `batch` sequences and n_q current tokens (split-key partial results and
+ * query sums).  Depends only on these arguments. */
+size_t infllm_workspace_bytes(const infllm_params* p, int32_t batch, int32_t n_q);
+
+/* Append the current tokens X at positions [past_len, past_len + n_q).
+ *  q: [batch][Hq] heads of n_q x D dtype rows; head h of sequence b starts at
+ *     q + (b*Hq + h)*q_head_stride elements (q_head_stride >= n_q*D).
+ *  k, v: chunk keys/values laid out the same way with kv_head_stride; both NULL
+ *     when the caller has already written them into the store.
+ * Copies k, v into the store and extends the qprefix ring (the window query sums
+ * that the representative score r_m of Section 3.2 needs once tokens are
+ * evicted).  Positions must be appended in order: slot (past_len - 1) must hold
+ * the running sum through past_len - 1.  E_RANGE if past_len + n_q > capacity. */
+infllm_status infllm_append(const infllm_params* p, const infllm_memory* m, const void* q,
+                            int64_t q_head_stride, const void* k, const void* v,
+                            int64_t kv_head_stride, int32_t n_q, int64_t past_len, void* stream);
+
+/* Memory-unit construction (Section 3.2, "Block-Level Memory Units").
+ * For units [first_unit, first_unit + n_new) of every (sequence, kv head):
+ * r_m = 1/(l_L*G) * sum_{h in group} sum_{j=1..l_L} q^h_{m+j} . k_m for each of its
+ * l_bs tokens (G = Hq/Hkv), then R(B) = the r_k tokens of largest r_m (ties: lower
+ * position).  Writes repr_idx and unit_ksum.  `past_len` is the number of
+ * positions appended so far; every window m+1..m+l_L must lie below it and the
+ * ring must still hold slots first_pos .. last_pos + l_L (E_RANGE otherwise).
+ * repr_score: optional [batch][Hkv][n_new][l_bs] float64 output of r_m. */
+infllm_status infllm_build_units(const infllm_params* p, const infllm_memory* m, int32_t first_unit,
+                                 int32_t n_new, int64_t past_len, double* repr_score, void* stream);
+
+/* Unit relevance (Section 3.2, "memory lookup"):
+ * sim(X, B) = sum_{i=1..l_X} sum_{j=1..r_k} q_{i+l_P} . k_{b_j}, one score per
+ * (sequence, kv head, unit) with the query side summed over the kv head's query
+ * group.  q as in infllm_append.  scores: [batch][Hkv][n_units] float32.
+ * n_units must not exceed max_units.  Needs the workspace. */
+infllm_status infllm_score_units(const infllm_params* p, const infllm_memory* m, const void* q,
+                                 int64_t q_head_stride, int32_t n_q, int32_t n_units, float* scores,
+                                 void* workspace, size_t workspace_bytes, void* stream);
+
+/* Top-k lookup f(X, E) (Section 3.2): for each of `rows` rows of `scores`
+ * ([rows][n_units] float32), the min(k, n_units) largest, ties to the lower index,
+ * written ascending to idx [rows][k] int32 followed by -1 padding.  NaN scores
+ * rank below every number; -0 equals +0. */
+infllm_status infllm_select_topk(int32_t rows, const float* scores, int32_t n_units, int32_t k,
+                                 int32_t* idx, void* stream);
+
+/* Attention of the current tokens over the current key-value cache (Section 3.1):
+ * O = Attn[Q X, Concat(C_k, K X), Concat(C_v, V X)] with C = Concat(I, f(X,E), L).
+ * For query i of head h (kv head g = h / G), one softmax of sm_scale * q . k over
+ * I, the units idx[b][g][0 .. min(k, n_units)) (entries that are negative or
+ * >= n_units are skipped), L, and X positions past_len .. past_len + i.
+ * The chunk's K/V must already be in the store.
+ *  out: [batch][Hq] heads of n_q x D dtype rows, head stride out_head_stride.
+ *  lse: optional [batch][Hq][n_q] float32 natural-log sum of exp of the logits.
+ * The keys are split into parts processed in parallel whose partial softmaxes are
+ * merged by their log-sum-exp; the workspace holds the partials. */
+infllm_status infllm_chunk_attend(const infllm_params* p, const infllm_memory* m, const void* q,
+                                  int64_t q_head_stride, int32_t n_q, int64_t past_len,
+                                  const int32_t* idx, int32_t k, void* out, int64_t out_head_stride,
+                                  float* lse, void* workspace, size_t workspace_bytes, void* stream);
+
+/* The two halves of infllm_chunk_attend, for callers that time or schedule them
+ * apart.  infllm_attend_partial writes per-part normalised outputs and lse into the
+ * workspace and reports the part count; infllm_lse_merge combines them
+ * (LSE = log sum_s exp(lse_s), O = sum_s exp(lse_s - LSE) O_s) into out / lse.
+ * With one part, infllm_attend_partial writes out and lse directly and
+ * infllm_lse_merge must not be called.  Arguments as in infllm_chunk_attend. */
+infllm_status infllm_attend_partial(const infllm_params* p, const infllm_memory* m, const void* q,
+                                    int64_t q_head_stride, int32_t n_q, int64_t past_len,
+                                    const int32_t* idx, int32_t k, void* out, int64_t out_head_stride,
+                                    float* lse, void* workspace, size_t workspace_bytes,
+                                    int32_t* n_parts, void* stream);
+infllm_status infllm_lse_merge(const infllm_params* p, int32_t batch, int32_t n_q, int32_t n_parts,
+                               const void* workspace, size_t workspace_bytes, void* out,
+                               int64_t out_head_stride, float* lse, void* stream);
+
+/* One whole step of the layer (Sections 3.1-3.2) for the current tokens X at
+ * positions [past_len, past_len + n_q), in this order on `stream`:
+ *   1. unit construction for units [units_built, n_units(past_len)), the units
+ *      evicted since the caller's previous step (as infllm_build_units);
+ *   2. append of X (as infllm_append; k, v may be NULL when already stored);
+ *   3. relevance of every unit: scores [batch][Hkv][n_units(past_len)] float32;
+ *   4. lookup of the k_m best: idx [batch][Hkv][k_m] int32 (as infllm_select_topk);
+ *   5. attention (as infllm_chunk_attend) into out / lse.
+ * units_built is the number of units built by earlier steps (0 for the first
+ * step); afterwards n_units(past_len) units are built.  Every stage is validated
+ * before the first is enqueued. */
+infllm_status infllm_step(const infllm_params* p, const infllm_memory* m, const void* q, int64_t q_head_stride,
+                          const void* k, const void* v, int64_t kv_head_stride, int32_t n_q, int64_t past_len,
+                          int32_t units_built, float* scores, int32_t* idx, void* out, int64_t out_head_stride,
+                          float* lse, void* workspace, size_t workspace_bytes, void* stream);
+
+/* Static description of a status code. */
+const char* infllm_status_string(infllm_status s);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* INFLLM_H */

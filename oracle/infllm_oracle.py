@@ -66,7 +66,8 @@ def unit_start(unit: int, p: Params) -> int:
     return p.n_init + unit * p.block_size
 
 
-def representative_scores(q_group: np.ndarray, k_head: np.ndarray, unit: int, p: Params) -> np.ndarray:
+def representative_scores(q_group: np.ndarray, k_head: np.ndarray, unit: int, p: Params,
+                          q_summed: Optional[np.ndarray] = None) -> np.ndarray:
     """Representative score r_m of every token m of one unit (Section 3.2, "Block-Level Memory Units").
 
     r_m = (1/l_L) * sum_{j=1..l_L} q_{m+j} . k_m : the mean dot product of token m's
@@ -75,20 +76,25 @@ def representative_scores(q_group: np.ndarray, k_head: np.ndarray, unit: int, p:
     r_m = 1/(l_L*G) * sum_h sum_j q^h_{m+j} . k_m.
 
     q_group: [G][S][D] queries of the group's heads (positions up to m + l_L must
-    exist); k_head: [S][D] keys of the kv head.  Returns float64 [l_bs].
+    exist); k_head: [S][D] keys of the kv head.  q_summed, if given, is the same
+    group's query sum sum_h q^h as float64 [S][D], precomputed once per sequence
+    (q_group then only supplies G).  Returns float64 [l_bs].
     """
     G = q_group.shape[0]
     m0 = unit_start(unit, p)
     lbs, lL = p.block_size, p.n_local
     # Window queries of all tokens of the unit: positions m0+1 .. m0+l_bs-1+l_L,
     # summed over the group's heads (sum_h q^h . k = (sum_h q^h) . k).
-    qw = np.asarray(q_group[:, m0 + 1: m0 + lbs + lL, :], dtype=np.float64).sum(axis=0)
+    if q_summed is None:
+        qw = np.asarray(q_group[:, m0 + 1: m0 + lbs + lL, :], dtype=np.float64).sum(axis=0)
+    else:
+        qw = q_summed[m0 + 1: m0 + lbs + lL]
     ku = np.asarray(k_head[m0: m0 + lbs, :], dtype=np.float64)
-    dots = qw @ ku.T  # dots[a, t] = q~_{m0+1+a} . k_{m0+t}
+    dots = ku @ qw.T  # dots[t, a] = k_{m0+t} . q~_{m0+1+a}
     r = np.empty(lbs)
     for t in range(lbs):
-        # j = 1..l_L  <->  window row a = t + j - 1 = t .. t + l_L - 1
-        r[t] = dots[t: t + lL, t].sum()
+        # j = 1..l_L  <->  window index a = t + j - 1 = t .. t + l_L - 1
+        r[t] = dots[t, t: t + lL].sum()
     return r / (lL * G)
 
 
@@ -217,12 +223,23 @@ class StreamOracle:
         self.q, self.k, self.v, self.p = q, k, v, p
         self._rep: Dict[Tuple[int, int, int], np.ndarray] = {}
         self._rscore: Dict[Tuple[int, int, int], np.ndarray] = {}
+        self._qsum: Dict[Tuple[int, int], np.ndarray] = {}
+
+    def group_query_sum(self, b: int, g: int) -> Optional[np.ndarray]:
+        """sum_h q^h over kv head g's query group, float64 [S][D] (cached; None for very long inputs)."""
+        if self.q.shape[2] > (1 << 18):
+            return None
+        if (b, g) not in self._qsum:
+            G = self.p.group
+            self._qsum[(b, g)] = np.asarray(self.q[b, g * G:(g + 1) * G], dtype=np.float64).sum(axis=0)
+        return self._qsum[(b, g)]
 
     def repr_scores(self, b: int, g: int, unit: int) -> np.ndarray:
         key = (b, g, unit)
         if key not in self._rscore:
             G = self.p.group
-            self._rscore[key] = representative_scores(self.q[b, g * G:(g + 1) * G], self.k[b, g], unit, self.p)
+            self._rscore[key] = representative_scores(self.q[b, g * G:(g + 1) * G], self.k[b, g], unit, self.p,
+                                                      self.group_query_sum(b, g))
         return self._rscore[key]
 
     def repr_offsets(self, b: int, g: int, unit: int) -> np.ndarray:

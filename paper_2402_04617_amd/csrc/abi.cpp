@@ -1,0 +1,472 @@
+// C ABI of the InfLLM step (declared in include/infllm.h): argument validation on
+// the host, partition arithmetic, workspace sizing and kernel dispatch on the
+// caller's stream.  Every check runs before the first HIP call, so invalid
+// arguments are rejected without touching the device.
+#include <hip/hip_runtime.h>
+
+#include <atomic>
+#include <cmath>
+#include <cstring>
+
+#include "../../include/infllm.h"
+#include "launch.h"
+
+using namespace infllm;
+
+namespace infllm {
+int attend_max_parts(bool bf16, int G, int n_q, int64_t max_virtual);
+}
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::atomic<int> g_device_ok[kMaxDevices];  // 0 unknown, 1 gfx950, 2 unusable
+
+infllm_status check_device() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return INFLLM_E_DEVICE;
+  }
+  int st = g_device_ok[dev].load(std::memory_order_relaxed);
+  if (st == 0) {
+    hipDeviceProp_t prop;
+    st = 2;
+    if (hipGetDeviceProperties(&prop, dev) == hipSuccess && std::strncmp(prop.gcnArchName, "gfx950", 6) == 0)
+      st = 1;
+    (void)hipGetLastError();
+    g_device_ok[dev].store(st, std::memory_order_relaxed);
+  }
+  return st == 1 ? INFLLM_OK : INFLLM_E_DEVICE;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+int esize(const infllm_params* p) { return p->dtype == INFLLM_BF16 ? 2 : 4; }
+
+infllm_status check_params(const infllm_params* p) {
+  if (p == nullptr) return INFLLM_E_NULL;
+  if (p->n_q_heads <= 0 || p->n_kv_heads <= 0 || p->n_q_heads % p->n_kv_heads != 0) return INFLLM_E_SHAPE;
+  if (p->dtype != INFLLM_F32 && p->dtype != INFLLM_BF16) return INFLLM_E_SHAPE;
+  if (p->head_dim <= 0) return INFLLM_E_SHAPE;
+  if (p->head_dim != 64 && p->head_dim != 128) return INFLLM_E_UNSUPPORTED;
+  if (p->n_init < 0 || p->n_local < 1 || p->block_size < 1 || p->topk < 0) return INFLLM_E_SHAPE;
+  if (p->block_size > 256) return INFLLM_E_UNSUPPORTED;
+  if (p->n_repr < 1 || p->n_repr > p->block_size) return INFLLM_E_SHAPE;
+  if (!std::isfinite(p->sm_scale)) return INFLLM_E_SHAPE;
+  return INFLLM_OK;
+}
+
+infllm_status check_store(const infllm_params* p, const infllm_memory* m) {
+  if (m == nullptr || m->k == nullptr || m->v == nullptr) return INFLLM_E_NULL;
+  if (m->batch < 1 || m->capacity < 1) return INFLLM_E_SHAPE;
+  if (!aligned16(m->k) || !aligned16(m->v)) return INFLLM_E_SHAPE;
+  (void)p;
+  return INFLLM_OK;
+}
+
+infllm_status check_units(const infllm_memory* m) {
+  if (m->repr_idx == nullptr || m->unit_ksum == nullptr) return INFLLM_E_NULL;
+  if (m->max_units < 0) return INFLLM_E_SHAPE;
+  if (!aligned16(m->unit_ksum)) return INFLLM_E_SHAPE;
+  return INFLLM_OK;
+}
+
+// Rows of `n_q` tokens per head with stride `head_stride` elements, read as 16-byte vectors.
+infllm_status check_rows(const infllm_params* p, const void* ptr, int64_t head_stride, int32_t n_q) {
+  if (ptr == nullptr) return INFLLM_E_NULL;
+  if (head_stride < (int64_t)n_q * p->head_dim) return INFLLM_E_SHAPE;
+  if (((head_stride * esize(p)) & 15) != 0 || !aligned16(ptr)) return INFLLM_E_SHAPE;
+  return INFLLM_OK;
+}
+
+struct Part {
+  int64_t n_init, local_begin;
+  int32_t n_units;
+};
+Part partition(const infllm_params* p, int64_t past_len) {
+  Part r;
+  r.n_init = past_len < p->n_init ? past_len : p->n_init;
+  const int64_t evicted = past_len - p->n_init - p->n_local;
+  const int64_t nu = evicted > 0 ? evicted / p->block_size : 0;
+  r.n_units = (int32_t)(nu > INT32_MAX ? INT32_MAX : nu);
+  r.local_begin = r.n_init + nu * p->block_size;
+  return r;
+}
+
+int64_t max_virtual_keys(const infllm_params* p, int32_t n_q) {
+  return (int64_t)p->n_init + (int64_t)p->topk * p->block_size + p->n_local + p->block_size - 1 + n_q;
+}
+
+size_t attend_ws_bytes(const infllm_params* p, int32_t batch, int32_t n_q, int parts) {
+  const int64_t rows = (int64_t)batch * p->n_q_heads * n_q;
+  return (size_t)parts * (size_t)rows * (size_t)(p->head_dim + 1) * 4u;
+}
+
+size_t qbar_ws_bytes(const infllm_params* p, int32_t batch, int32_t n_q) {
+  const int G = p->n_q_heads / p->n_kv_heads;
+  return (size_t)batch * p->n_kv_heads * score_qbar_parts(G, n_q) * p->head_dim * 4u;
+}
+
+infllm_status launch_status(hipError_t e) {
+  if (e != hipSuccess) {
+    (void)hipGetLastError();
+    return INFLLM_E_LAUNCH;
+  }
+  return INFLLM_OK;
+}
+
+// Shared preparation of infllm_chunk_attend / infllm_attend_partial.
+infllm_status prepare_attend(const infllm_params* p, const infllm_memory* m, const void* q,
+                             int64_t q_head_stride, int32_t n_q, int64_t past_len, const int32_t* idx,
+                             int32_t k, void* out, int64_t out_head_stride, float* lse, void* workspace,
+                             size_t workspace_bytes, AttendArgs* a) {
+  infllm_status st;
+  if ((st = check_params(p)) != INFLLM_OK) return st;
+  if ((st = check_store(p, m)) != INFLLM_OK) return st;
+  if (n_q < 0 || past_len < 0 || k < 0) return INFLLM_E_SHAPE;
+  if (past_len + n_q > m->capacity) return INFLLM_E_RANGE;
+  if ((st = check_rows(p, q, q_head_stride, n_q)) != INFLLM_OK) return st;
+  if ((st = check_rows(p, out, out_head_stride, n_q)) != INFLLM_OK) return st;
+  const Part part = partition(p, past_len);
+  const int32_t n_sel = k < part.n_units ? k : part.n_units;
+  if (n_sel > 0 && idx == nullptr) return INFLLM_E_NULL;
+  const int64_t n_virtual = part.n_init + (int64_t)n_sel * p->block_size + (past_len - part.local_begin) + n_q;
+  if (n_virtual > INT32_MAX) return INFLLM_E_UNSUPPORTED;
+  const bool bf16 = p->dtype == INFLLM_BF16;
+  const int64_t rows = (int64_t)m->batch * p->n_q_heads * n_q;
+  const size_t per_part = rows > 0 ? (size_t)rows * (size_t)(p->head_dim + 1) * 4u : 1;
+  const int max_parts = (workspace == nullptr) ? 0 : (int)(workspace_bytes / per_part > 4096 ? 4096 : workspace_bytes / per_part);
+  const int parts = attend_choose_parts(bf16, m->batch, p->n_q_heads, p->n_kv_heads, n_q, (int)n_virtual, max_parts);
+  if (parts < 1) return INFLLM_E_WORKSPACE;
+  if (parts > 1 && !aligned16(workspace)) return INFLLM_E_SHAPE;
+
+  std::memset(a, 0, sizeof(*a));
+  a->batch = m->batch;
+  a->n_q_heads = p->n_q_heads;
+  a->n_kv_heads = p->n_kv_heads;
+  a->head_dim = p->head_dim;
+  a->capacity = m->capacity;
+  a->q_head_stride = q_head_stride;
+  a->out_head_stride = out_head_stride;
+  a->sm_scale = p->sm_scale;
+  a->geom.n_init = (int32_t)part.n_init;
+  a->geom.n_units = part.n_units;
+  a->geom.n_sel = n_sel;
+  a->geom.block_size = p->block_size;
+  a->geom.unit_base = p->n_init;
+  a->geom.idx_stride = k;
+  a->geom.local_begin = part.local_begin;
+  a->geom.past_len = past_len;
+  a->geom.n_q = n_q;
+  a->geom.n_virtual = (int32_t)n_virtual;
+  a->q = q;
+  a->k_store = m->k;
+  a->v_store = m->v;
+  a->idx = idx;
+  a->out = out;
+  a->lse = lse;
+  a->parts = parts;
+  a->part_o = (float*)workspace;
+  a->part_lse = workspace ? (float*)((char*)workspace + (size_t)parts * rows * p->head_dim * 4u) : nullptr;
+  a->bf16 = bf16;
+  return INFLLM_OK;
+}
+
+MergeArgs merge_args(const infllm_params* p, int32_t batch, int32_t n_q, int32_t n_parts, const void* workspace,
+                     void* out, int64_t out_head_stride, float* lse) {
+  MergeArgs ma;
+  const int64_t rows = (int64_t)batch * p->n_q_heads * n_q;
+  ma.rows = (int)rows;
+  ma.head_dim = p->head_dim;
+  ma.parts = n_parts;
+  ma.n_q = n_q;
+  ma.n_q_heads = p->n_q_heads;
+  ma.out_head_stride = out_head_stride;
+  ma.part_o = (const float*)workspace;
+  ma.part_lse = (const float*)((const char*)workspace + (size_t)n_parts * rows * p->head_dim * 4u);
+  ma.out = out;
+  ma.lse = lse;
+  ma.bf16 = p->dtype == INFLLM_BF16;
+  return ma;
+}
+
+
+infllm_status prep_append(const infllm_params* p, const infllm_memory* m, const void* q, int64_t q_head_stride,
+                          const void* k, const void* v, int64_t kv_head_stride, int32_t n_q, int64_t past_len,
+                          AppendArgs* a) {
+  infllm_status st;
+  if ((st = check_params(p)) != INFLLM_OK) return st;
+  if ((st = check_store(p, m)) != INFLLM_OK) return st;
+  if (m->qprefix == nullptr) return INFLLM_E_NULL;
+  if (n_q < 0 || past_len < 0) return INFLLM_E_SHAPE;
+  if ((k == nullptr) != (v == nullptr)) return INFLLM_E_NULL;
+  if (q == nullptr) return INFLLM_E_NULL;
+  if (q_head_stride < (int64_t)n_q * p->head_dim) return INFLLM_E_SHAPE;
+  if (k != nullptr && ((st = check_rows(p, k, kv_head_stride, n_q)) != INFLLM_OK ||
+                       (st = check_rows(p, v, kv_head_stride, n_q)) != INFLLM_OK))
+    return st;
+  if (m->ring < 1 || m->ring <= n_q) return INFLLM_E_SHAPE;
+  if (past_len + n_q > m->capacity) return INFLLM_E_RANGE;
+  a->batch = m->batch;
+  a->n_q_heads = p->n_q_heads;
+  a->n_kv_heads = p->n_kv_heads;
+  a->head_dim = p->head_dim;
+  a->n_q = n_q;
+  a->ring = m->ring;
+  a->past_len = past_len;
+  a->capacity = m->capacity;
+  a->q_head_stride = q_head_stride;
+  a->kv_head_stride = kv_head_stride;
+  a->q = q;
+  a->k_src = k;
+  a->v_src = v;
+  a->k_store = m->k;
+  a->v_store = m->v;
+  a->qprefix = m->qprefix;
+  a->bf16 = p->dtype == INFLLM_BF16;
+  return INFLLM_OK;
+}
+
+infllm_status prep_build(const infllm_params* p, const infllm_memory* m, int32_t first_unit, int32_t n_new,
+                         int64_t past_len, double* repr_score, BuildArgs* a) {
+  infllm_status st;
+  if ((st = check_params(p)) != INFLLM_OK) return st;
+  if ((st = check_store(p, m)) != INFLLM_OK) return st;
+  if ((st = check_units(m)) != INFLLM_OK) return st;
+  if (m->qprefix == nullptr) return INFLLM_E_NULL;
+  if (first_unit < 0 || n_new < 0 || past_len < 0 || m->ring < 1) return INFLLM_E_SHAPE;
+  if ((int64_t)first_unit + n_new > m->max_units) return INFLLM_E_RANGE;
+  if (past_len > m->capacity) return INFLLM_E_RANGE;
+  if (n_new > 0) {
+    const int64_t m0 = (int64_t)p->n_init + (int64_t)first_unit * p->block_size;
+    const int64_t m_last = (int64_t)p->n_init + ((int64_t)first_unit + n_new) * p->block_size - 1;
+    if (m_last + p->n_local > past_len - 1) return INFLLM_E_RANGE;  // windows not appended yet: not evicted
+    if (m0 < past_len - m->ring) return INFLLM_E_RANGE;              // ring no longer holds the oldest slot
+  }
+  a->batch = m->batch;
+  a->n_q_heads = p->n_q_heads;
+  a->n_kv_heads = p->n_kv_heads;
+  a->head_dim = p->head_dim;
+  a->n_init = p->n_init;
+  a->n_local = p->n_local;
+  a->block_size = p->block_size;
+  a->n_repr = p->n_repr;
+  a->first_unit = first_unit;
+  a->n_new = n_new;
+  a->max_units = m->max_units;
+  a->ring = m->ring;
+  a->capacity = m->capacity;
+  a->k_store = m->k;
+  a->qprefix = m->qprefix;
+  a->repr_idx = m->repr_idx;
+  a->unit_ksum = m->unit_ksum;
+  a->repr_score = repr_score;
+  a->bf16 = p->dtype == INFLLM_BF16;
+  return INFLLM_OK;
+}
+
+infllm_status prep_score(const infllm_params* p, const infllm_memory* m, const void* q, int64_t q_head_stride,
+                         int32_t n_q, int32_t n_units, float* scores, void* workspace, size_t workspace_bytes,
+                         ScoreArgs* a) {
+  infllm_status st;
+  if ((st = check_params(p)) != INFLLM_OK) return st;
+  if (m == nullptr) return INFLLM_E_NULL;
+  if (m->batch < 1) return INFLLM_E_SHAPE;
+  if ((st = check_units(m)) != INFLLM_OK) return st;
+  if (n_q < 0 || n_units < 0) return INFLLM_E_SHAPE;
+  if (n_units > m->max_units) return INFLLM_E_RANGE;
+  a->n_units = n_units;
+  if (n_units == 0) return INFLLM_OK;
+  if (scores == nullptr) return INFLLM_E_NULL;
+  if ((st = check_rows(p, q, q_head_stride, n_q)) != INFLLM_OK) return st;
+  if (workspace == nullptr) return INFLLM_E_NULL;
+  if (workspace_bytes < qbar_ws_bytes(p, m->batch, n_q)) return INFLLM_E_WORKSPACE;
+  if (!aligned16(workspace)) return INFLLM_E_SHAPE;
+  a->batch = m->batch;
+  a->n_q_heads = p->n_q_heads;
+  a->n_kv_heads = p->n_kv_heads;
+  a->head_dim = p->head_dim;
+  a->n_q = n_q;
+  a->max_units = m->max_units;
+  a->q_head_stride = q_head_stride;
+  a->q = q;
+  a->unit_ksum = m->unit_ksum;
+  a->scores = scores;
+  a->qbar_parts = (float*)workspace;
+  a->bf16 = p->dtype == INFLLM_BF16;
+  return INFLLM_OK;
+}
+
+infllm_status prep_topk(int32_t rows, const float* scores, int32_t n_units, int32_t k, int32_t* idx) {
+  if (rows < 0 || n_units < 0 || k < 0) return INFLLM_E_SHAPE;
+  if (rows == 0 || k == 0) return INFLLM_OK;
+  if (idx == nullptr) return INFLLM_E_NULL;
+  if (n_units > 0 && scores == nullptr) return INFLLM_E_NULL;
+  return INFLLM_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* infllm_status_string(infllm_status s) {
+  switch (s) {
+    case INFLLM_OK: return "ok";
+    case INFLLM_E_NULL: return "a required pointer is NULL";
+    case INFLLM_E_SHAPE: return "inconsistent sizes or parameters";
+    case INFLLM_E_RANGE: return "positions, units or ring slots outside the memory";
+    case INFLLM_E_UNSUPPORTED: return "unsupported configuration";
+    case INFLLM_E_WORKSPACE: return "workspace too small";
+    case INFLLM_E_LAUNCH: return "kernel launch failed";
+    case INFLLM_E_DEVICE: return "no usable gfx950 device";
+  }
+  return "unknown status";
+}
+
+infllm_status infllm_partition(const infllm_params* p, int64_t past_len, int64_t* n_init, int32_t* n_units,
+                               int64_t* local_begin) {
+  infllm_status st = check_params(p);
+  if (st != INFLLM_OK) return st;
+  if (n_init == nullptr || n_units == nullptr || local_begin == nullptr) return INFLLM_E_NULL;
+  if (past_len < 0) return INFLLM_E_SHAPE;
+  const Part r = partition(p, past_len);
+  *n_init = r.n_init;
+  *n_units = r.n_units;
+  *local_begin = r.local_begin;
+  return INFLLM_OK;
+}
+
+size_t infllm_workspace_bytes(const infllm_params* p, int32_t batch, int32_t n_q) {
+  if (check_params(p) != INFLLM_OK || batch < 1 || n_q < 0) return 0;
+  const int G = p->n_q_heads / p->n_kv_heads;
+  const int parts = attend_max_parts(p->dtype == INFLLM_BF16, G, n_q, max_virtual_keys(p, n_q));
+  size_t a = attend_ws_bytes(p, batch, n_q, parts);
+  size_t b = qbar_ws_bytes(p, batch, n_q);
+  size_t r = a > b ? a : b;
+  return (r + 255) & ~(size_t)255;
+}
+
+infllm_status infllm_append(const infllm_params* p, const infllm_memory* m, const void* q, int64_t q_head_stride,
+                            const void* k, const void* v, int64_t kv_head_stride, int32_t n_q, int64_t past_len,
+                            void* stream) {
+  AppendArgs a;
+  infllm_status st = prep_append(p, m, q, q_head_stride, k, v, kv_head_stride, n_q, past_len, &a);
+  if (st != INFLLM_OK) return st;
+  if ((st = check_device()) != INFLLM_OK) return st;
+  return launch_status(launch_append(a, (hipStream_t)stream));
+}
+
+infllm_status infllm_build_units(const infllm_params* p, const infllm_memory* m, int32_t first_unit, int32_t n_new,
+                                 int64_t past_len, double* repr_score, void* stream) {
+  BuildArgs a;
+  infllm_status st = prep_build(p, m, first_unit, n_new, past_len, repr_score, &a);
+  if (st != INFLLM_OK || n_new == 0) return st;
+  if ((st = check_device()) != INFLLM_OK) return st;
+  return launch_status(launch_build_units(a, (hipStream_t)stream));
+}
+
+infllm_status infllm_score_units(const infllm_params* p, const infllm_memory* m, const void* q, int64_t q_head_stride,
+                                 int32_t n_q, int32_t n_units, float* scores, void* workspace, size_t workspace_bytes,
+                                 void* stream) {
+  ScoreArgs a;
+  infllm_status st = prep_score(p, m, q, q_head_stride, n_q, n_units, scores, workspace, workspace_bytes, &a);
+  if (st != INFLLM_OK || n_units == 0) return st;
+  if ((st = check_device()) != INFLLM_OK) return st;
+  return launch_status(launch_score(a, (hipStream_t)stream));
+}
+
+infllm_status infllm_select_topk(int32_t rows, const float* scores, int32_t n_units, int32_t k, int32_t* idx,
+                                 void* stream) {
+  infllm_status st = prep_topk(rows, scores, n_units, k, idx);
+  if (st != INFLLM_OK || rows == 0 || k == 0) return st;
+  if ((st = check_device()) != INFLLM_OK) return st;
+  return launch_status(launch_select_topk(rows, scores, n_units, k, idx, (hipStream_t)stream));
+}
+
+infllm_status infllm_attend_partial(const infllm_params* p, const infllm_memory* m, const void* q,
+                                    int64_t q_head_stride, int32_t n_q, int64_t past_len, const int32_t* idx,
+                                    int32_t k, void* out, int64_t out_head_stride, float* lse, void* workspace,
+                                    size_t workspace_bytes, int32_t* n_parts, void* stream) {
+  if (n_parts == nullptr) return INFLLM_E_NULL;
+  AttendArgs a;
+  infllm_status st = prepare_attend(p, m, q, q_head_stride, n_q, past_len, idx, k, out, out_head_stride, lse,
+                                    workspace, workspace_bytes, &a);
+  if (st != INFLLM_OK) return st;
+  *n_parts = a.parts;
+  if (n_q == 0) return INFLLM_OK;
+  if ((st = check_device()) != INFLLM_OK) return st;
+  return launch_status(launch_attend(a, (hipStream_t)stream));
+}
+
+infllm_status infllm_lse_merge(const infllm_params* p, int32_t batch, int32_t n_q, int32_t n_parts,
+                               const void* workspace, size_t workspace_bytes, void* out, int64_t out_head_stride,
+                               float* lse, void* stream) {
+  infllm_status st;
+  if ((st = check_params(p)) != INFLLM_OK) return st;
+  if (batch < 1 || n_q < 0 || n_parts < 2) return INFLLM_E_SHAPE;
+  if (workspace == nullptr) return INFLLM_E_NULL;
+  if (workspace_bytes < attend_ws_bytes(p, batch, n_q, n_parts)) return INFLLM_E_WORKSPACE;
+  if ((st = check_rows(p, out, out_head_stride, n_q)) != INFLLM_OK) return st;
+  if (n_q == 0) return INFLLM_OK;
+  if ((st = check_device()) != INFLLM_OK) return st;
+  MergeArgs ma = merge_args(p, batch, n_q, n_parts, workspace, out, out_head_stride, lse);
+  return launch_status(launch_merge(ma, (hipStream_t)stream));
+}
+
+infllm_status infllm_chunk_attend(const infllm_params* p, const infllm_memory* m, const void* q, int64_t q_head_stride,
+                                  int32_t n_q, int64_t past_len, const int32_t* idx, int32_t k, void* out,
+                                  int64_t out_head_stride, float* lse, void* workspace, size_t workspace_bytes,
+                                  void* stream) {
+  AttendArgs a;
+  infllm_status st = prepare_attend(p, m, q, q_head_stride, n_q, past_len, idx, k, out, out_head_stride, lse,
+                                    workspace, workspace_bytes, &a);
+  if (st != INFLLM_OK) return st;
+  if (n_q == 0) return INFLLM_OK;
+  if ((st = check_device()) != INFLLM_OK) return st;
+  if ((st = launch_status(launch_attend(a, (hipStream_t)stream))) != INFLLM_OK) return st;
+  if (a.parts == 1) return INFLLM_OK;
+  MergeArgs ma = merge_args(p, m->batch, n_q, a.parts, workspace, out, out_head_stride, lse);
+  return launch_status(launch_merge(ma, (hipStream_t)stream));
+}
+
+infllm_status infllm_step(const infllm_params* p, const infllm_memory* m, const void* q, int64_t q_head_stride,
+                          const void* k, const void* v, int64_t kv_head_stride, int32_t n_q, int64_t past_len,
+                          int32_t units_built, float* scores, int32_t* idx, void* out, int64_t out_head_stride,
+                          float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+  infllm_status st;
+  if ((st = check_params(p)) != INFLLM_OK) return st;
+  if (m == nullptr) return INFLLM_E_NULL;
+  if (past_len < 0 || units_built < 0) return INFLLM_E_SHAPE;
+  const Part part = partition(p, past_len);
+  if (units_built > part.n_units) return INFLLM_E_SHAPE;
+  BuildArgs ba;
+  AppendArgs aa;
+  ScoreArgs sa;
+  AttendArgs at;
+  if ((st = prep_build(p, m, units_built, part.n_units - units_built, past_len, nullptr, &ba)) != INFLLM_OK) return st;
+  if ((st = prep_append(p, m, q, q_head_stride, k, v, kv_head_stride, n_q, past_len, &aa)) != INFLLM_OK) return st;
+  if ((st = prep_score(p, m, q, q_head_stride, n_q, part.n_units, scores, workspace, workspace_bytes, &sa)) !=
+      INFLLM_OK)
+    return st;
+  const int32_t rows = m->batch * p->n_kv_heads;
+  if ((st = prep_topk(part.n_units > 0 ? rows : 0, scores, part.n_units, p->topk, idx)) != INFLLM_OK) return st;
+  if ((st = prepare_attend(p, m, q, q_head_stride, n_q, past_len, idx, p->topk, out, out_head_stride, lse, workspace,
+                           workspace_bytes, &at)) != INFLLM_OK)
+    return st;
+  if ((st = check_device()) != INFLLM_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  if (ba.n_new > 0 && (st = launch_status(launch_build_units(ba, s))) != INFLLM_OK) return st;
+  if ((st = launch_status(launch_append(aa, s))) != INFLLM_OK) return st;
+  if (part.n_units > 0) {
+    if ((st = launch_status(launch_score(sa, s))) != INFLLM_OK) return st;
+    if (p->topk > 0 && (st = launch_status(launch_select_topk(rows, scores, part.n_units, p->topk, idx, s))) != INFLLM_OK)
+      return st;
+  }
+  if (n_q == 0) return INFLLM_OK;
+  if ((st = launch_status(launch_attend(at, s))) != INFLLM_OK) return st;
+  if (at.parts == 1) return INFLLM_OK;
+  MergeArgs ma = merge_args(p, m->batch, n_q, at.parts, workspace, out, out_head_stride, lse);
+  return launch_status(launch_merge(ma, s));
+}
+
+}  // extern "C"

@@ -1,0 +1,87 @@
+// Host-side launchers of the gfx950 kernels (internal to the library).  The C ABI
+// in abi.cpp validates every argument, then calls these; each returns the
+// hipError_t of its launch(es).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "common.h"
+
+namespace infllm {
+
+struct AppendArgs {
+  int batch, n_q_heads, n_kv_heads, head_dim, n_q, ring;
+  int64_t past_len, capacity, q_head_stride, kv_head_stride;
+  const void* q;
+  const void* k_src;
+  const void* v_src;
+  void* k_store;
+  void* v_store;
+  double* qprefix;
+  bool bf16;
+};
+hipError_t launch_append(const AppendArgs& a, hipStream_t s);
+
+struct BuildArgs {
+  int batch, n_q_heads, n_kv_heads, head_dim, n_init, n_local, block_size, n_repr;
+  int first_unit, n_new, max_units, ring;
+  int64_t capacity;
+  const void* k_store;
+  const double* qprefix;
+  int32_t* repr_idx;
+  float* unit_ksum;
+  double* repr_score;  // nullable
+  bool bf16;
+};
+hipError_t launch_build_units(const BuildArgs& a, hipStream_t s);
+
+struct ScoreArgs {
+  int batch, n_q_heads, n_kv_heads, head_dim, n_q, n_units, max_units;
+  int64_t q_head_stride;
+  const void* q;
+  const float* unit_ksum;
+  float* scores;
+  float* qbar_parts;  // workspace
+  bool bf16;
+};
+int score_qbar_parts(int G, int n_q);
+hipError_t launch_score(const ScoreArgs& a, hipStream_t s);
+
+hipError_t launch_select_topk(int rows, const float* scores, int n_units, int k, int32_t* idx,
+                              hipStream_t s);
+
+struct AttendArgs {
+  int batch, n_q_heads, n_kv_heads, head_dim;
+  int64_t capacity, q_head_stride, out_head_stride;
+  float sm_scale;
+  StepGeom geom;
+  const void* q;
+  const void* k_store;
+  const void* v_store;
+  const int32_t* idx;
+  void* out;     // final output (one part)
+  float* lse;    // nullable
+  float* part_o;    // [parts][rows][D] fp32
+  float* part_lse;  // [parts][rows]
+  int parts;
+  bool bf16;
+};
+// Number of key parts the attention uses for this shape, limited by max_parts.
+int attend_choose_parts(bool bf16, int batch, int n_q_heads, int n_kv_heads, int n_q, int n_virtual,
+                        int max_parts);
+hipError_t launch_attend(const AttendArgs& a, hipStream_t s);
+
+struct MergeArgs {
+  int rows, head_dim, parts, n_q, n_q_heads;
+  int64_t out_head_stride;
+  const float* part_o;
+  const float* part_lse;
+  void* out;
+  float* lse;
+  bool bf16;
+};
+hipError_t launch_merge(const MergeArgs& a, hipStream_t s);
+
+}  // namespace infllm

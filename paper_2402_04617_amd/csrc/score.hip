@@ -1,0 +1,106 @@
+// Unit relevance (Section 3.2, "memory lookup").
+//
+// sim(X, B) = sum_i sum_j q_{i+l_P} . k_{b_j} is bilinear, so per kv head it is
+// Qbar . Kbar_B with Qbar the sum of the group's current queries and Kbar_B the
+// sum of the unit's representative keys (kept by unit construction).  Two
+// kernels: a reduction of the chunk's queries into per-part partial sums
+// (deterministic order), then one streaming pass over the Kbar table (fp32,
+// unit-contiguous 16-byte cells) at HBM rate.
+#include "launch.h"
+
+namespace infllm {
+namespace {
+
+constexpr int kMaxQbarParts = 16;
+
+// grid (parts, batch*Hkv); rows of the group are (head, i) pairs, head-major.
+template <typename T>
+__global__ void __launch_bounds__(256) qbar_kernel(const T* __restrict__ q, int64_t q_head_stride,
+                                                   int n_q_heads, int n_kv_heads, int head_dim,
+                                                   int n_q, int parts, float* __restrict__ qbar_parts) {
+  constexpr int kVec = 16 / sizeof(T);
+  const int part = blockIdx.x;
+  const int bg = blockIdx.y;
+  const int b = bg / n_kv_heads, g = bg - b * n_kv_heads;
+  const int G = n_q_heads / n_kv_heads;
+  const int rows = G * n_q;
+  const int per = (rows + parts - 1) / parts;
+  const int r0 = min(rows, part * per), r1 = min(rows, r0 + per);
+  const int lanes_per_row = head_dim / kVec;
+  const int rgroups = 256 / lanes_per_row;
+  const int c = threadIdx.x % lanes_per_row;
+  const int rg = threadIdx.x / lanes_per_row;
+
+  float acc[kVec];
+#pragma unroll
+  for (int e = 0; e < kVec; ++e) acc[e] = 0.f;
+  for (int r = r0 + rg; r < r1; r += rgroups) {
+    const int hl = r / n_q, i = r - hl * n_q;
+    const T* row = q + (int64_t)(b * n_q_heads + g * G + hl) * q_head_stride + (int64_t)i * head_dim;
+    uint4 raw = *(const uint4*)(row + c * kVec);
+    const T* vals = (const T*)&raw;
+#pragma unroll
+    for (int e = 0; e < kVec; ++e) acc[e] += Elem<T>::load(vals + e);
+  }
+  __shared__ float red[256 * kVec];
+#pragma unroll
+  for (int e = 0; e < kVec; ++e) red[rg * head_dim + c * kVec + e] = acc[e];
+  __syncthreads();
+  for (int d = threadIdx.x; d < head_dim; d += 256) {
+    float s = 0.f;
+    for (int j = 0; j < rgroups; ++j) s += red[j * head_dim + d];
+    qbar_parts[((int64_t)bg * parts + part) * head_dim + d] = s;
+  }
+}
+
+// grid (ceil(n_units/256), batch*Hkv); one unit per thread.
+__global__ void __launch_bounds__(256) score_kernel(const float* __restrict__ qbar_parts, int parts,
+                                                    const float4* __restrict__ unit_ksum, int head_dim,
+                                                    int n_units, int max_units, float* __restrict__ scores) {
+  const int bg = blockIdx.y;
+  __shared__ float qbar[256];
+  for (int d = threadIdx.x; d < head_dim; d += 256) {
+    float s = 0.f;
+    for (int p = 0; p < parts; ++p) s += qbar_parts[((int64_t)bg * parts + p) * head_dim + d];
+    qbar[d] = s;
+  }
+  __syncthreads();
+  const int u = blockIdx.x * 256 + threadIdx.x;
+  if (u >= n_units) return;
+  const int nc = head_dim / 4;
+  const float4* ks = unit_ksum + (int64_t)bg * nc * max_units + u;
+  float acc = 0.f;
+#pragma unroll 8
+  for (int c = 0; c < nc; ++c) {
+    const float4 k4 = ks[(int64_t)c * max_units];
+    acc += qbar[4 * c] * k4.x + qbar[4 * c + 1] * k4.y + qbar[4 * c + 2] * k4.z + qbar[4 * c + 3] * k4.w;
+  }
+  scores[(int64_t)bg * n_units + u] = acc;
+}
+
+}  // namespace
+
+int score_qbar_parts(int G, int n_q) {
+  int rows = G * n_q;
+  int parts = (rows + 255) / 256;
+  return parts < 1 ? 1 : (parts > kMaxQbarParts ? kMaxQbarParts : parts);
+}
+
+hipError_t launch_score(const ScoreArgs& a, hipStream_t s) {
+  if (a.n_units == 0) return hipSuccess;
+  const int G = a.n_q_heads / a.n_kv_heads;
+  const int parts = score_qbar_parts(G, a.n_q);
+  dim3 g1(parts, a.batch * a.n_kv_heads);
+  if (a.bf16)
+    hipLaunchKernelGGL(qbar_kernel<bf16_t>, g1, dim3(256), 0, s, (const bf16_t*)a.q, a.q_head_stride,
+                       a.n_q_heads, a.n_kv_heads, a.head_dim, a.n_q, parts, a.qbar_parts);
+  else
+    hipLaunchKernelGGL(qbar_kernel<float>, g1, dim3(256), 0, s, (const float*)a.q, a.q_head_stride,
+                       a.n_q_heads, a.n_kv_heads, a.head_dim, a.n_q, parts, a.qbar_parts);
+  dim3 g2((a.n_units + 255) / 256, a.batch * a.n_kv_heads);
+  hipLaunchKernelGGL(score_kernel, g2, dim3(256), 0, s, (const float*)a.qbar_parts, parts,
+                     (const float4*)a.unit_ksum, a.head_dim, a.n_units, a.max_units, a.scores);
+  return hipGetLastError();
+}
+
+}  // namespace infllm

@@ -125,6 +125,19 @@ def check_repr_scores_prefix_identity():
             assert np.allclose(got, ref, rtol=1e-12, atol=1e-12)
 
 
+def check_repr_scores_presummed_queries():
+    """Passing the group's query sum precomputed gives the same r_m as summing per call."""
+    rng = np.random.default_rng(23)
+    p = _params(n_q_heads=6, n_kv_heads=2, head_dim=5, n_init=2, n_local=7, block_size=4)
+    q, k, _ = _rand_qkv(rng, p, S=2 + 5 * 4 + 8)
+    for g in range(2):
+        qs = q[0, 3 * g:3 * g + 3].sum(axis=0)
+        for unit in range(5):
+            a = O.representative_scores(q[0, 3 * g:3 * g + 3], k[0, g], unit, p)
+            b = O.representative_scores(q[0, 3 * g:3 * g + 3], k[0, g], unit, p, qs)
+            assert np.allclose(a, b, rtol=1e-13, atol=1e-13)
+
+
 def check_repr_scores_window_one():
     """l_L = 1: r_m is the group-mean of q_{m+1} . k_m."""
     rng = np.random.default_rng(13)
@@ -392,6 +405,7 @@ ALL_CHECKS = [
     check_partition,
     check_repr_scores_bruteforce,
     check_repr_scores_prefix_identity,
+    check_repr_scores_presummed_queries,
     check_repr_scores_window_one,
     check_repr_scores_window_support,
     check_top_indices,

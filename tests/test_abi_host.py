@@ -1,0 +1,198 @@
+"""C ABI on the host: symbols, partition arithmetic, workspace sizing, argument validation.
+
+No GPU is used.  Every call below either is host-only (partition, workspace
+size, status strings) or carries an argument error that the library must
+reject before its first HIP call; the fake device pointers are never
+dereferenced.  (A call with valid arguments is made only in the E_DEVICE test,
+which is skipped wherever a GPU is visible.)
+"""
+import ctypes
+import os
+import re
+
+import pytest
+
+from oracle import infllm_oracle as O
+from paper_2402_04617_amd import infllm as F
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+FAKE = 0x7F0000001000  # 16-byte aligned, never dereferenced
+
+
+@pytest.fixture(scope="module")
+def L():
+    if not os.path.exists(F._LIB_PATH):
+        from paper_2402_04617_amd.build import build
+        build()
+    return F.lib()
+
+
+def header_functions():
+    txt = open(os.path.join(ROOT, "include", "infllm.h")).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(infllm_\w+)\s*\(", txt)))
+
+
+def test_exports_every_declared_symbol(L):
+    names = header_functions()
+    assert len(names) >= 11
+    for n in names:
+        assert hasattr(L, n), n
+    assert sorted(F.EXPORTS) == names
+
+
+def test_status_strings(L):
+    for c in range(8):
+        assert L.infllm_status_string(c)
+    assert b"unknown" in L.infllm_status_string(99)
+
+
+def P(**kw):
+    base = dict(n_q_heads=32, n_kv_heads=8, head_dim=128, n_init=128, n_local=4096, block_size=128,
+                n_repr=4, topk=32, dtype="bf16", sm_scale=1.0)
+    base.update(kw)
+    return F.params(**base)
+
+
+def test_partition_matches_oracle(L):
+    for l_I, l_L, l_bs in ((128, 4096, 128), (16, 256, 32), (0, 5, 3), (7, 1, 1)):
+        p = P(n_init=l_I, n_local=l_L, block_size=l_bs, n_repr=1)
+        op = O.Params(32, 8, 128, l_I, l_L, l_bs, 1, 32)
+        for past in list(range(0, l_I + l_L + 5 * l_bs + 3)) + [131072, 1 << 20]:
+            got = F.infllm_partition(p, past)
+            exp = O.partition(past, op)
+            assert got == (exp.n_init, exp.n_units, exp.local_begin), (past, got, exp)
+
+
+def test_partition_errors(L):
+    n0, n1, n2 = ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int64()
+    assert L.infllm_partition(None, 5, ctypes.byref(n0), ctypes.byref(n1), ctypes.byref(n2)) == 1
+    assert L.infllm_partition(ctypes.byref(P()), -1, ctypes.byref(n0), ctypes.byref(n1), ctypes.byref(n2)) == 2
+    assert L.infllm_partition(ctypes.byref(P()), 5, None, ctypes.byref(n1), ctypes.byref(n2)) == 1
+
+
+@pytest.mark.parametrize("kw,code", [
+    (dict(n_kv_heads=7), 2), (dict(n_q_heads=0), 2), (dict(head_dim=96), 4), (dict(head_dim=0), 2),
+    (dict(n_local=0), 2), (dict(block_size=0), 2), (dict(block_size=512, n_repr=4), 4),
+    (dict(n_repr=0), 2), (dict(n_repr=129), 2), (dict(topk=-1), 2), (dict(n_init=-1), 2),
+    (dict(sm_scale=float("inf")), 2),
+])
+def test_param_validation(L, kw, code):
+    p = P(**kw)
+    n0, n1, n2 = ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int64()
+    assert L.infllm_partition(ctypes.byref(p), 100, ctypes.byref(n0), ctypes.byref(n1), ctypes.byref(n2)) == code
+    assert L.infllm_workspace_bytes(ctypes.byref(p), 1, 512) == 0
+
+
+def test_workspace_bytes(L):
+    p = P()
+    ws = L.infllm_workspace_bytes(ctypes.byref(p), 1, 512)
+    rows = 32 * 512
+    assert ws >= 2 * rows * 129 * 4 and ws % 256 == 0
+    # decode: parts fixed by the bounded key count l_I + k_m*l_bs + l_L + l_bs - 1 + 1
+    wsd = L.infllm_workspace_bytes(ctypes.byref(p), 16, 1)
+    nv = 128 + 32 * 128 + 4096 + 127 + 1
+    assert wsd >= ((nv + 255) // 256) * 16 * 32 * 129 * 4
+
+
+def mem(**kw):
+    base = dict(batch=1, capacity=1 << 17, k=FAKE, v=FAKE, max_units=2048, repr_idx=FAKE,
+                unit_ksum=FAKE, qprefix=FAKE, ring=4096 + 128 + 512 + 1)
+    base.update(kw)
+    return F.Memory(**base)
+
+
+def test_append_validation(L):
+    p, m = P(), mem()
+    f = L.infllm_append
+    bp, bm = ctypes.byref(p), ctypes.byref(m)
+    assert f(None, bm, FAKE, 512 * 128, None, None, 0, 512, 0, None) == 1
+    assert f(bp, None, FAKE, 512 * 128, None, None, 0, 512, 0, None) == 1
+    assert f(bp, bm, None, 512 * 128, None, None, 0, 512, 0, None) == 1
+    assert f(bp, bm, FAKE, 100, None, None, 0, 512, 0, None) == 2               # head stride < n_q*D
+    assert f(bp, bm, FAKE, 512 * 128, FAKE, None, 512 * 128, 512, 0, None) == 1  # k without v
+    assert f(bp, bm, FAKE, 512 * 128, FAKE, FAKE, 512 * 128 + 1, 512, 0, None) == 2  # misaligned stride
+    assert f(bp, bm, FAKE, 512 * 128, FAKE + 2, FAKE, 512 * 128, 512, 0, None) == 2  # misaligned ptr
+    assert f(bp, bm, FAKE, 512 * 128, None, None, 0, 512, (1 << 17) - 100, None) == 3  # past capacity
+    small = mem(ring=512)
+    assert f(bp, ctypes.byref(small), FAKE, 512 * 128, None, None, 0, 512, 0, None) == 2  # ring <= n_q
+    noq = mem(qprefix=None)
+    assert f(bp, ctypes.byref(noq), FAKE, 512 * 128, None, None, 0, 512, 0, None) == 1
+    assert f(bp, bm, FAKE, 512 * 128, None, None, 0, -1, 0, None) == 2
+
+
+def test_build_validation(L):
+    p, m = P(), mem()
+    f = L.infllm_build_units
+    bp, bm = ctypes.byref(p), ctypes.byref(m)
+    # unit 0 covers [128, 256): its last window ends at 255 + 4096, so it needs past_len >= 4352
+    assert f(bp, bm, 0, 1, 4351, None, None) == 3
+    assert f(bp, bm, 0, 2, 4479, None, None) == 3
+    assert f(bp, bm, 2040, 16, 1 << 17, None, None) == 3     # beyond max_units
+    assert f(bp, bm, -1, 1, 10000, None, None) == 2
+    # ring too short for the oldest slot: unit 0 starts at 128, ring holds [past-ring, past)
+    assert f(bp, bm, 0, 1, 128 + 4833, None, None) == 3
+    nou = mem(unit_ksum=None)
+    assert f(bp, ctypes.byref(nou), 0, 1, 4352, None, None) == 1
+    assert f(bp, bm, 0, 0, 0, None, None) == 0  # nothing to build: no device needed
+
+
+def test_score_validation(L):
+    p, m = P(), mem()
+    f = L.infllm_score_units
+    bp, bm = ctypes.byref(p), ctypes.byref(m)
+    assert f(bp, bm, FAKE, 512 * 128, 512, 4096, FAKE, FAKE, 1 << 20, None) == 3   # n_units > max_units
+    assert f(bp, bm, FAKE, 512 * 128, 512, 100, None, FAKE, 1 << 20, None) == 1
+    assert f(bp, bm, FAKE, 512 * 128, 512, 100, FAKE, None, 1 << 20, None) == 1
+    assert f(bp, bm, FAKE, 512 * 128, 512, 100, FAKE, FAKE, 16, None) == 5          # workspace
+    assert f(bp, bm, FAKE, 512 * 128, 512, 0, None, None, 0, None) == 0             # no units: no-op
+
+
+def test_topk_validation(L):
+    f = L.infllm_select_topk
+    assert f(-1, FAKE, 10, 4, FAKE, None) == 2
+    assert f(8, FAKE, 10, 4, None, None) == 1
+    assert f(8, None, 10, 4, FAKE, None) == 1
+    assert f(0, None, 10, 4, None, None) == 0
+    assert f(8, None, 10, 0, None, None) == 0
+
+
+def test_attend_validation(L):
+    p, m = P(), mem()
+    f = L.infllm_chunk_attend
+    bp, bm = ctypes.byref(p), ctypes.byref(m)
+    S = 512 * 128
+    assert f(bp, bm, FAKE, S, 512, 1 << 17, FAKE, 32, FAKE, S, None, FAKE, 1 << 30, None) == 3  # past+n_q > cap
+    assert f(bp, bm, None, S, 512, 8192, FAKE, 32, FAKE, S, None, FAKE, 1 << 30, None) == 1
+    assert f(bp, bm, FAKE, S, 512, 8192, None, 32, FAKE, S, None, FAKE, 1 << 30, None) == 1     # idx needed
+    assert f(bp, bm, FAKE, S, 512, 8192, FAKE, 32, None, S, None, FAKE, 1 << 30, None) == 1
+    assert f(bp, bm, FAKE, S - 8, 512, 8192, FAKE, 32, FAKE, S, None, FAKE, 1 << 30, None) == 2
+    assert f(bp, bm, FAKE, S, 512, 8192, FAKE, -1, FAKE, S, None, FAKE, 1 << 30, None) == 2
+    # decode needs a fixed number of parts: a tiny workspace is rejected
+    pd = P()
+    assert f(ctypes.byref(pd), ctypes.byref(mem(batch=16)), FAKE, 128, 1, 131000, FAKE, 32, FAKE, 128, None,
+             FAKE, 64, None) == 5
+    parts = ctypes.c_int32()
+    assert L.infllm_attend_partial(bp, bm, FAKE, S, 512, 8192, FAKE, 32, FAKE, S, None, FAKE, 1 << 30,
+                                   None, None) == 1
+    assert L.infllm_lse_merge(bp, 1, 512, 1, FAKE, 1 << 30, FAKE, S, None, None) == 2  # one part: nothing to merge
+    assert L.infllm_lse_merge(bp, 1, 512, 4, FAKE, 100, FAKE, S, None, None) == 5
+    del parts
+
+
+def test_step_validation(L):
+    p, m = P(), mem()
+    f = L.infllm_step
+    bp, bm = ctypes.byref(p), ctypes.byref(m)
+    S = 512 * 128
+    # units_built beyond what the partition allows
+    assert f(bp, bm, FAKE, S, None, None, 0, 512, 8192, 100, FAKE, FAKE, FAKE, S, None, FAKE, 1 << 30, None) == 2
+    # scores missing while units exist
+    assert f(bp, bm, FAKE, S, None, None, 0, 512, 8192, 31, None, FAKE, FAKE, S, None, FAKE, 1 << 30, None) == 1
+
+
+@pytest.mark.skipif(os.path.exists("/dev/kfd") and os.access("/dev/kfd", os.R_OK),
+                    reason="a GPU may be present; valid arguments would launch on fake pointers")
+def test_valid_arguments_without_gpu_report_device_error(L):
+    p, m = P(), mem()
+    assert L.infllm_select_topk(8, FAKE, 10, 4, FAKE, None) == 7

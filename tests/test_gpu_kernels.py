@@ -1,0 +1,274 @@
+"""Per-entry-point parity of the HIP library against the CPU oracle (GPU).
+
+Every case is seeded and synthetic; expected values come from oracle/ on the
+same inputs.  Bars: integer outputs bit-exact (top-k on given scores, unit
+offsets away from near-ties); bf16 outputs within 2e-2 max-abs and fp32 within
+1e-4 of the float64 oracle.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import infllm_oracle as O
+from paper_2402_04617_amd import infllm as F
+from tests.gpu_util import Layer, check_selection, dev, host, log, oparams
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"bf16": 2e-2, "f32": 1e-4}
+
+
+def rand_inputs(rng, Hq, Hkv, S, D, dtype, qk_std=None, B=1):
+    s = qk_std if qk_std is not None else D ** -0.5
+    q = (rng.standard_normal((B, Hq, S, D)) * s).astype(np.float32)
+    k = (rng.standard_normal((B, Hkv, S, D)) * s).astype(np.float32)
+    v = rng.standard_normal((B, Hkv, S, D)).astype(np.float32)
+    if dtype == "bf16":
+        q, k, v = (torch.from_numpy(x).to(torch.bfloat16).float().numpy() for x in (q, k, v))
+    return q, k, v
+
+
+# ------------------------------------------------------------------ a5: top-k
+@pytest.mark.parametrize("n,k", [(0, 4), (1, 4), (5, 5), (7, 3), (100, 32), (987, 32), (8155, 32),
+                                 (9000, 64), (300, 1), (50, 0), (4096, 100)])
+def test_select_topk_bit_exact(n, k):
+    rng = np.random.default_rng(n * 131 + k)
+    rows = 8
+    s = rng.standard_normal((rows, n)).astype(np.float32) * 50
+    if n > 4:
+        s[1] = rng.integers(0, 5, n).astype(np.float32)       # massive ties
+        s[2] = 0.0
+        s[2, ::3] = -0.0                                      # -0 == +0
+        s[3, : n // 2] = s[3, n // 2: 2 * (n // 2)]             # duplicated halves
+        s[4] = np.float32(1e-30) * rng.standard_normal(n).astype(np.float32)
+    log(f"[topk] n={n} k={k}")
+    sd = torch.from_numpy(s).cuda()
+    idx = torch.full((rows, max(k, 1)), 7, dtype=torch.int32, device="cuda")
+    F.infllm_select_topk(rows, sd, n, k, idx)
+    got = host(idx)
+    op = O.Params(1, 1, 64, 0, 1, 1, 1, k)
+    for r in range(rows):
+        exp = O.select_units(s[r].astype(np.float64), op)
+        if k > 0:
+            assert np.array_equal(got[r, :k], exp), (r, got[r, :k], exp)
+
+
+def test_select_topk_nan_ranks_lowest():
+    s = np.array([[np.nan, 1.0, np.nan, -5.0, 3.0, np.nan]], dtype=np.float32)
+    idx = torch.zeros((1, 4), dtype=torch.int32, device="cuda")
+    F.infllm_select_topk(1, torch.from_numpy(s).cuda(), 6, 4, idx)
+    assert host(idx)[0].tolist() == [0, 1, 3, 4]  # three numbers, then the lowest-index NaN
+
+
+# ------------------------------------------------------------------ a2 + a8: append
+@pytest.mark.parametrize("dtype,G,D", [("bf16", 4, 128), ("f32", 2, 64), ("bf16", 1, 64)])
+def test_append_store_and_ring(dtype, G, D):
+    rng = np.random.default_rng(1)
+    Hkv, B, S = 2, 2, 300
+    p = F.params(G * Hkv, Hkv, D, 4, 16, 8, 2, 2, dtype)
+    q, k, v = rand_inputs(rng, G * Hkv, Hkv, S, D, dtype, B=B)
+    L = Layer(p, B, S, chunk=40, ring=97)
+    qd, kd, vd = dev(q, dtype), dev(k, dtype), dev(v, dtype)
+    es = L.esize
+    past = 0
+    for n in (40, 1, 33, 17, 40, 3):
+        log(f"[append] {dtype} G={G} D={D} past={past} n={n}")
+        F.infllm_append(p, L.mem.struct, qd.data_ptr() + past * D * es, S * D, kd.data_ptr() + past * D * es,
+                        vd.data_ptr() + past * D * es, S * D, n, past)
+        past += n
+    torch.cuda.synchronize()
+    assert np.array_equal(host(L.mem.k)[:, :, :past], k[:, :, :past])
+    assert np.array_equal(host(L.mem.v)[:, :, :past], v[:, :, :past])
+    ring = host(L.mem.qprefix)
+    qt = q.astype(np.float64).reshape(B, Hkv, G, S, D).sum(axis=2)
+    pref = np.cumsum(qt[:, :, :past], axis=2)
+    for t in range(max(0, past - 97), past):
+        assert np.allclose(ring[:, :, t % 97], pref[:, :, t], rtol=1e-12, atol=1e-12), t
+
+
+# ------------------------------------------------------------------ a3: unit construction
+@pytest.mark.parametrize("dtype,G,D,lI,lL,lbs,rk", [
+    ("bf16", 4, 128, 128, 4096, 128, 4),
+    ("f32", 2, 64, 16, 256, 32, 4),
+    ("bf16", 2, 64, 3, 37, 16, 16),   # every token representative
+    ("f32", 1, 128, 0, 5, 1, 1),      # one-token units
+    ("bf16", 8, 128, 7, 100, 200, 3), # unit size not a power of two
+])
+def test_build_units(dtype, G, D, lI, lL, lbs, rk):
+    rng = np.random.default_rng(2)
+    Hkv, B = 2, 1
+    n_units = 6
+    S = lI + n_units * lbs + lL + 3
+    p = F.params(G * Hkv, Hkv, D, lI, lL, lbs, rk, 4, dtype)
+    op = oparams(p)
+    q, k, v = rand_inputs(rng, G * Hkv, Hkv, S, D, dtype, B=B)
+    k[0, 1, lI + 2 * lbs: lI + 3 * lbs] = 0.0  # a unit of zero keys: all r_m tie at 0
+    L = Layer(p, B, S, chunk=S, ring=S + 1)
+    qd, kd, vd = dev(q, dtype), dev(k, dtype), dev(v, dtype)
+    log(f"[build] append {dtype} G={G} D={D} S={S}")
+    F.infllm_append(p, L.mem.struct, qd, S * D, kd, vd, S * D, S, 0)
+    nu = O.partition(S, op).n_units
+    assert nu >= n_units
+    rs = torch.zeros((B, Hkv, nu, lbs), dtype=torch.float64, device="cuda")
+    log(f"[build] units 0..{nu}")
+    F.infllm_build_units(p, L.mem.struct, 0, nu, S, rs)
+    torch.cuda.synchronize()
+    got_r = host(rs)
+    got_idx = host(L.mem.repr_idx)
+    got_ks = host(L.mem.unit_ksum)
+    so = O.StreamOracle(q, k, v, op)
+    for g in range(Hkv):
+        for u in range(nu):
+            r = so.repr_scores(0, g, u)
+            assert np.allclose(got_r[0, g, u], r, rtol=1e-9, atol=1e-12 * max(1.0, np.abs(r).max()))
+            exp = so.repr_offsets(0, g, u)
+            gi = got_idx[0, g, u]
+            if not np.array_equal(gi, exp):
+                # only allowed inside a near-tie at the r_k-th value
+                s = np.sort(r)[::-1]
+                assert rk < lbs and (s[rk - 1] - s[rk]) <= 1e-9 * max(1.0, abs(s[rk - 1])), (g, u, gi, exp)
+            ks = np.zeros(D)
+            for o in gi:
+                ks += k[0, g, lI + u * lbs + o].astype(np.float64)
+            cell = got_ks[0, g, :, u, :].reshape(D)
+            assert np.allclose(cell, ks, rtol=1e-6, atol=1e-6)
+    # the zero-key unit ties everywhere: the lowest offsets win
+    assert got_idx[0, 1, 2].tolist() == list(range(rk))
+
+
+# ------------------------------------------------------------------ a4: unit scoring
+@pytest.mark.parametrize("dtype,G,D,n_q,n_units", [("bf16", 4, 128, 512, 987), ("f32", 2, 64, 64, 53),
+                                                   ("bf16", 4, 128, 1, 991), ("bf16", 8, 64, 33, 300),
+                                                   ("f32", 1, 128, 5, 8155)])
+def test_score_units(dtype, G, D, n_q, n_units):
+    """Scoring alone: the unit table is filled from the oracle's representatives, so this checks
+    sim(X, B) = sum_i sum_j q_i . k_{b_j} independently of unit construction."""
+    rng = np.random.default_rng(3)
+    Hkv, B = 2, 2
+    lbs, rk, lI = 4, 2, 1
+    S = lI + n_units * lbs + 8
+    p = F.params(G * Hkv, Hkv, D, lI, 4, lbs, rk, 8, dtype)
+    q, k, _ = rand_inputs(rng, G * Hkv, Hkv, max(S, n_q), D, dtype, B=B)
+    rep_off = np.stack([np.sort(rng.choice(lbs, rk, replace=False)) for _ in range(B * Hkv * n_units)])
+    rep_off = rep_off.reshape(B, Hkv, n_units, rk)
+    rep_pos = lI + np.arange(n_units)[None, None, :, None] * lbs + rep_off
+    ksum = np.zeros((B, Hkv, n_units, D), dtype=np.float64)
+    for b in range(B):
+        for g in range(Hkv):
+            ksum[b, g] = k[b, g][rep_pos[b, g]].astype(np.float64).sum(axis=1)
+    L = Layer(p, B, S, chunk=n_q, ring=n_q + 1)
+    tab = np.zeros((B, Hkv, D // 4, L.max_units, 4), dtype=np.float32)
+    tab[:, :, :, :n_units, :] = ksum.astype(np.float32).reshape(B, Hkv, n_units, D // 4, 4).transpose(0, 1, 3, 2, 4)
+    L.mem.unit_ksum.copy_(torch.from_numpy(tab))
+    qd = dev(q[:, :, :n_q], dtype)
+    scores = torch.zeros((B, Hkv, n_units), dtype=torch.float32, device="cuda")
+    log(f"[score] {dtype} G={G} D={D} n_q={n_q} n_units={n_units}")
+    F.infllm_score_units(p, L.mem.struct, qd, n_q * D, n_q, n_units, scores, L.ws)
+    got = host(scores).astype(np.float64)
+    tol = 1e-5 if dtype == "f32" else 1e-5  # bf16 inputs are exact; both sum in fp32
+    for b in range(B):
+        for g in range(Hkv):
+            exp = O.unit_relevance(q[b, g * G:(g + 1) * G, :n_q], k[b, g], rep_pos[b, g])
+            scale = max(np.abs(exp).max(), np.sqrt(np.mean(exp ** 2)))
+            assert np.abs(got[b, g] - exp).max() <= tol * scale + 1e-6, (b, g)
+
+
+# ------------------------------------------------------------------ a6 + a7: attention
+ATTEND_CASES = [
+    # dtype, G, Hkv, D, lI, lL, lbs, k_m, past, n_q, B
+    ("bf16", 4, 2, 128, 128, 512, 128, 4, 3000, 512, 1),
+    ("bf16", 4, 2, 128, 128, 512, 128, 4, 3000, 77, 1),     # ragged rows
+    ("bf16", 4, 8, 128, 128, 4096, 128, 32, 20000, 512, 1),  # real shape, several key parts
+    ("bf16", 1, 2, 128, 16, 256, 32, 4, 1500, 64, 2),
+    ("bf16", 8, 1, 64, 5, 100, 16, 7, 900, 100, 1),
+    ("bf16", 2, 2, 64, 0, 50, 20, 3, 400, 130, 1),          # no initial tokens, l_bs not a power of 2
+    ("bf16", 4, 2, 128, 128, 4096, 128, 32, 100, 512, 1),   # past shorter than l_I: no memory yet
+    ("bf16", 4, 2, 128, 128, 4096, 128, 32, 0, 512, 1),     # first chunk
+    ("bf16", 4, 2, 128, 128, 4096, 128, 32, 13000, 1, 3),   # decode
+    ("bf16", 8, 2, 64, 16, 300, 32, 5, 1000, 1, 2),         # decode, G=8, D=64
+    ("bf16", 3, 1, 128, 16, 300, 32, 5, 1000, 1, 1),        # decode shape with G=3 (MFMA path)
+    ("f32", 2, 1, 64, 16, 256, 32, 4, 1000, 64, 1),
+    ("f32", 2, 1, 64, 16, 256, 32, 4, 1000, 1, 1),
+    ("f32", 4, 2, 128, 128, 512, 128, 4, 3000, 37, 2),
+    ("f32", 3, 2, 64, 0, 20, 8, 50, 500, 20, 1),            # k_m larger than n_units
+]
+
+
+def _attend_case(case, seed=4, workspace=True, invalid_entry=False):
+    dtype, G, Hkv, D, lI, lL, lbs, km, past, n_q, B = case
+    rng = np.random.default_rng(seed)
+    S = past + n_q
+    p = F.params(G * Hkv, Hkv, D, lI, lL, lbs, 2, km, dtype, sm_scale=0.9)
+    op = oparams(p)
+    q, k, v = rand_inputs(rng, G * Hkv, Hkv, S, D, dtype, B=B)
+    nu = O.partition(past, op).n_units
+    sel = np.full((B, Hkv, km), -1, dtype=np.int64)
+    for b in range(B):
+        for g in range(Hkv):
+            c = np.sort(rng.choice(nu, min(km, nu), replace=False)) if nu else np.zeros(0, np.int64)
+            sel[b, g, :c.size] = c
+    sel_gpu = sel.copy()
+    if invalid_entry and nu > 0 and km > 1:
+        sel_gpu[:, :, 0] = nu + 5       # out of range: must be skipped
+        sel[:, :, 0] = -1
+    L = Layer(p, B, S, chunk=n_q, ring=n_q + 1)
+    L.mem.k.copy_(dev(k, dtype))
+    L.mem.v.copy_(dev(v, dtype))
+    qd = dev(q[:, :, past:past + n_q], dtype)
+    idx = torch.from_numpy(sel_gpu.astype(np.int32)).cuda()
+    out = torch.zeros((B, G * Hkv, n_q, D), dtype=L.dt, device="cuda")
+    lse = torch.zeros((B, G * Hkv, n_q), dtype=torch.float32, device="cuda")
+    ws = L.ws if workspace else None
+    log(f"[attend] {case} ws={workspace} invalid={invalid_entry}")
+    F.infllm_chunk_attend(p, L.mem.struct, qd, n_q * D, n_q, past, idx, km, out, n_q * D, lse, ws)
+    torch.cuda.synchronize()
+    got_o, got_l = host(out).astype(np.float64), host(lse).astype(np.float64)
+    for b in range(B):
+        eo, el = O.attend(q[b, :, past:past + n_q], k[b], v[b], past, sel[b], op)
+        err = np.abs(got_o[b] - eo).max()
+        assert err <= TOL[dtype], (case, b, err)
+        assert np.abs(got_l[b] - el).max() <= (1e-3 if dtype == "bf16" else 1e-4), case
+    return got_o, got_l
+
+
+@pytest.mark.parametrize("case", ATTEND_CASES, ids=[str(c) for c in ATTEND_CASES])
+def test_chunk_attend(case):
+    _attend_case(case)
+
+
+@pytest.mark.parametrize("case", [ATTEND_CASES[0], ATTEND_CASES[3], ATTEND_CASES[11]],
+                         ids=["bf16", "bf16-batch", "f32"])
+def test_chunk_attend_single_part_and_invalid_entries(case):
+    _attend_case(case, workspace=False)
+    _attend_case(case, invalid_entry=True)
+
+
+def test_attend_partial_plus_merge_equals_chunk_attend():
+    dtype, G, Hkv, D, lI, lL, lbs, km, past, n_q, B = ATTEND_CASES[2]
+    rng = np.random.default_rng(5)
+    S = past + n_q
+    p = F.params(G * Hkv, Hkv, D, lI, lL, lbs, 2, km, dtype)
+    q, k, v = rand_inputs(rng, G * Hkv, Hkv, S, D, dtype, B=B)
+    nu = O.partition(past, oparams(p)).n_units
+    sel = np.sort(rng.choice(nu, km, replace=False))
+    L = Layer(p, B, S, chunk=n_q, ring=n_q + 1)
+    L.mem.k.copy_(dev(k, dtype))
+    L.mem.v.copy_(dev(v, dtype))
+    qd = dev(q[:, :, past:], dtype)
+    idx = torch.from_numpy(np.tile(sel, (B, Hkv, 1)).astype(np.int32)).cuda()
+    o1 = torch.zeros((B, G * Hkv, n_q, D), dtype=L.dt, device="cuda")
+    o2, l1, l2 = torch.zeros_like(o1), torch.zeros((B, G * Hkv, n_q), device="cuda"), torch.zeros(
+        (B, G * Hkv, n_q), device="cuda")
+    log("[attend] partial + merge vs chunk_attend")
+    F.infllm_chunk_attend(p, L.mem.struct, qd, n_q * D, n_q, past, idx, km, o1, n_q * D, l1, L.ws)
+    parts = F.infllm_attend_partial(p, L.mem.struct, qd, n_q * D, n_q, past, idx, km, o2, n_q * D, l2, L.ws)
+    assert parts > 1
+    F.infllm_lse_merge(p, B, n_q, parts, L.ws, o2, n_q * D, l2)
+    torch.cuda.synchronize()
+    assert torch.equal(o1, o2) and torch.equal(l1, l2)
+
+
+def test_attend_deterministic():
+    a = _attend_case(ATTEND_CASES[2], seed=9)
+    b = _attend_case(ATTEND_CASES[2], seed=9)
+    assert np.array_equal(a[0], b[0]) and np.array_equal(a[1], b[1])

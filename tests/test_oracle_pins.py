@@ -38,7 +38,7 @@ def _mut_partition_ceil_units(past_len, p):
     return O.Partition(n_init, n, min(past_len, n_init + n * p.block_size))
 
 
-def _mut_repr_window_shift(q_group, k_head, unit, p):
+def _mut_repr_window_shift(q_group, k_head, unit, p, q_summed=None):
     # j = 0 .. l_L-1 instead of 1 .. l_L
     G = q_group.shape[0]
     m0 = O.unit_start(unit, p)
@@ -47,11 +47,11 @@ def _mut_repr_window_shift(q_group, k_head, unit, p):
     return np.array([dots[t:t + p.n_local, t].sum() for t in range(p.block_size)]) / (p.n_local * G)
 
 
-def _mut_repr_no_group_mean(q_group, k_head, unit, p):
+def _mut_repr_no_group_mean(q_group, k_head, unit, p, q_summed=None):
     return _orig["representative_scores"](q_group, k_head, unit, p) * q_group.shape[0]
 
 
-def _mut_repr_first_head_only(q_group, k_head, unit, p):
+def _mut_repr_first_head_only(q_group, k_head, unit, p, q_summed=None):
     return _orig["representative_scores"](q_group[:1], k_head, unit, p)
 
 
