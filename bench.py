@@ -1,0 +1,311 @@
+#!/usr/bin/env python3
+"""Throughput of the InfLLM block-memory attention step on one MI355X.
+
+A benchmark step is one pass of the whole per-layer path over one synthetic
+sequence: for every chunk, unit construction for newly evicted blocks, append,
+unit scoring, top-k lookup, and chunk attention with its log-sum-exp merge
+(one infllm_step call per chunk).  Inputs are seeded synthetic Q/K/V resident
+in HBM before timing starts.
+
+Prints ONE JSON line.  The headline value is chunk-encode context tokens/s on
+the 128K-token Llama-3-8B-shaped layer (32 query / 8 kv heads, head_dim 128,
+bf16, 128 initial tokens, 4K local window, 128-token units, r_k 4, k_m 32,
+512-token chunks).  Extra legs (1M-token streaming encode; 16 x 128K batched
+decode) are reported in the same line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+from concurrent.futures import ThreadPoolExecutor
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def log(msg):
+    print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+
+def upload_inputs(synth, torch, threads=16):
+    """Q [B][Hq][S][D], K, V [B][Hkv][S][D] bf16 on the GPU, drawn span by span."""
+    wl = synth.wl
+    S, D = wl.seq_len, wl.head_dim
+    dt = torch.bfloat16 if wl.dtype == "bf16" else torch.float32
+    out = {}
+    for name, H in (("q", wl.n_q_heads), ("k", wl.n_kv_heads), ("v", wl.n_kv_heads)):
+        t = torch.empty((wl.batch, H, S, D), dtype=dt, device="cuda")
+        fn = getattr(synth, name)
+        jobs = [(b, h) for b in range(wl.batch) for h in range(H)]
+        with ThreadPoolExecutor(threads) as ex:
+            for (b, h), x in zip(jobs, ex.map(lambda bh: fn(bh[0], bh[1], 0, S), jobs)):
+                t[b, h].copy_(torch.from_numpy(x).to(dt))
+        out[name] = t
+    torch.cuda.synchronize()
+    return out
+
+
+def attention_flops(wl, steps):
+    """Algorithmic attention flops of a pass: 4*D*Hq per (query, visible key) pair."""
+    from paper_2402_04617_amd import infllm as F
+    p = params_of(wl)
+    total = 0
+    for past, n in steps:
+        n_init, n_units, local_begin = F.infllm_partition(p, past)
+        ctx = n_init + min(wl.topk, n_units) * wl.block_size + (past - local_begin)
+        total += 4 * wl.head_dim * wl.n_q_heads * wl.batch * (n * ctx + n * (n + 1) // 2)
+    return total
+
+
+def params_of(wl):
+    from paper_2402_04617_amd import infllm as F
+    return F.params(wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.n_init, wl.n_local, wl.block_size,
+                    wl.n_repr, wl.topk, wl.dtype)
+
+
+class Stream:
+    """Device state of one layer over a sequence, stepped through infllm_step."""
+
+    def __init__(self, wl, inputs, torch):
+        from paper_2402_04617_amd import infllm as F
+        self.F, self.torch, self.wl = F, torch, wl
+        self.p = params_of(wl)
+        self.inp = inputs
+        S, D = wl.seq_len, wl.head_dim
+        self.max_units = max(1, F.infllm_partition(self.p, S)[1])
+        self.mem = F.alloc_memory(self.p, wl.batch, S, self.max_units, F.recommended_ring(self.p, wl.chunk))
+        ws = max(F.infllm_workspace_bytes(self.p, wl.batch, wl.chunk), F.infllm_workspace_bytes(self.p, wl.batch, 1))
+        self.ws = torch.zeros(ws, dtype=torch.uint8, device="cuda")
+        dt = inputs["q"].dtype
+        self.out = torch.zeros((wl.batch, wl.n_q_heads, wl.chunk, D), dtype=dt, device="cuda")
+        self.lse = torch.zeros((wl.batch, wl.n_q_heads, wl.chunk), dtype=torch.float32, device="cuda")
+        self.scores = torch.zeros(wl.batch * wl.n_kv_heads * self.max_units, dtype=torch.float32, device="cuda")
+        self.idx = torch.zeros((wl.batch, wl.n_kv_heads, max(1, wl.topk)), dtype=torch.int32, device="cuda")
+        self.esize = 2 if dt == torch.bfloat16 else 4
+
+    def ptr(self, name, past):
+        return self.inp[name].data_ptr() + past * self.wl.head_dim * self.esize
+
+    def step(self, past, n, units_built):
+        wl, S, D = self.wl, self.wl.seq_len, self.wl.head_dim
+        self.F.infllm_step(self.p, self.mem.struct, self.ptr("q", past), S * D, self.ptr("k", past),
+                           self.ptr("v", past), S * D, n, past, units_built, self.scores, self.idx, self.out,
+                           wl.chunk * D, self.lse, self.ws)
+        return self.F.infllm_partition(self.p, past)[1]
+
+    def run(self, steps, built=0, on_step=None):
+        for i, (past, n) in enumerate(steps):
+            built = self.step(past, n, built)
+            if on_step is not None:
+                on_step(i)
+        return built
+
+    def prefill_memory(self, upto):
+        """Untimed set-up for decode: append positions [0, upto) chunk by chunk and build every unit."""
+        F, wl, S, D = self.F, self.wl, self.wl.seq_len, self.wl.head_dim
+        built = 0
+        for past in range(0, upto, wl.chunk):
+            n = min(wl.chunk, upto - past)
+            nu = F.infllm_partition(self.p, past)[1]
+            if nu > built:
+                F.infllm_build_units(self.p, self.mem.struct, built, nu - built, past)
+                built = nu
+            F.infllm_append(self.p, self.mem.struct, self.ptr("q", past), S * D, self.ptr("k", past),
+                            self.ptr("v", past), S * D, n, past)
+        nu = F.infllm_partition(self.p, upto)[1]
+        if nu > built:
+            F.infllm_build_units(self.p, self.mem.struct, built, nu - built, upto)
+            built = nu
+        return built
+
+    def attention_replay(self, steps, idx_hist):
+        """Attention kernels alone, same launches as in the step, each bracketed by HIP events on the
+        launching stream; returns per-launch durations (ms) of the attention kernel."""
+        F, torch, wl, S, D = self.F, self.torch, self.wl, self.wl.seq_len, self.wl.head_dim
+        evs = []
+        for i, (past, n) in enumerate(steps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            parts = F.infllm_attend_partial(self.p, self.mem.struct, self.ptr("q", past), S * D, n, past,
+                                            idx_hist[i], wl.topk, self.out, wl.chunk * D, self.lse, self.ws)
+            b.record()
+            if parts > 1:
+                F.infllm_lse_merge(self.p, wl.batch, n, parts, self.ws, self.out, wl.chunk * D, self.lse)
+            evs.append((a, b))
+        torch.cuda.synchronize()
+        return [a.elapsed_time(b) for a, b in evs]
+
+
+def time_steps(torch, fn, steps, warmup):
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    t0, t1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    t0.record()
+    for _ in range(steps):
+        fn()
+    t1.record()
+    torch.cuda.synchronize()
+    return t0.elapsed_time(t1) / steps
+
+
+def encode_leg(name, seed, steps, warmup, torch, want_roofline=True):
+    from workload import WORKLOADS, Synth
+    wl = WORKLOADS[name]
+    t = time.time()
+    synth = Synth(wl, seed)
+    inputs = upload_inputs(synth, torch)
+    log(f"{name}: inputs resident in HBM ({time.time() - t:.1f}s)")
+    st = Stream(wl, inputs, torch)
+    plan = wl.step_starts()
+    ms = time_steps(torch, lambda: st.run(plan), steps, warmup)
+    res = {"workload": name, "seq_len": wl.seq_len, "ms_per_step": ms,
+           "ctx_tok_per_s": wl.seq_len * wl.batch / (ms / 1e3)}
+    if want_roofline:
+        # one more (untimed) pass recording the lookup of every chunk, then the attention replay
+        idx_hist = torch.zeros((len(plan),) + tuple(st.idx.shape), dtype=torch.int32, device="cuda")
+        st.run(plan, on_step=lambda i: idx_hist[i].copy_(st.idx))
+        durs = st.attention_replay(plan, idx_hist)
+        flops = attention_flops(wl, plan)
+        tot_ms = float(np.sum(durs))
+        res["attention"] = {"launches": len(durs), "avg_ms": tot_ms / len(durs), "total_ms": tot_ms,
+                            "algorithmic_flops": flops, "tflops": flops / (tot_ms / 1e3) / 1e12}
+    return res, synth, st
+
+
+def decode_leg(seed, steps, warmup, torch):
+    from workload import WORKLOADS, Synth
+    wl = WORKLOADS["llama3-8b-decode-16x128k"]
+    t = time.time()
+    synth = Synth(wl, seed)
+    inputs = upload_inputs(synth, torch)
+    log(f"decode: inputs resident ({time.time() - t:.1f}s)")
+    st = Stream(wl, inputs, torch)
+    t = time.time()
+    built = st.prefill_memory(wl.prefill_len)
+    torch.cuda.synchronize()
+    log(f"decode: memory of {wl.prefill_len} tokens x {wl.batch} built ({time.time() - t:.1f}s)")
+    plan = wl.step_starts()[-wl.decode_steps:]
+    ms = time_steps(torch, lambda: st.run(plan, built=built), steps, warmup)
+    us_tok = ms * 1e3 / len(plan)
+    return {"workload": wl.name, "decode_steps": len(plan), "batch": wl.batch, "us_per_step": us_tok,
+            "tok_per_s": wl.batch * len(plan) / (ms / 1e3)}
+
+
+def cpu_baseline(synth, n_chunk_samples=16):
+    """The oracle on a bounded sample of the 128K encode: kv head 0 (of 8) with its 4 query heads;
+    all of that head's units are built, and every 16th chunk is scored, looked up and attended.
+    Extrapolated linearly to all chunks and all kv heads."""
+    from oracle import infllm_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # pragma: no cover
+        threads = len(os.sched_getaffinity(0))
+    wl = synth.wl
+    G, S = wl.group, wl.seq_len
+    q = np.stack([synth.q(0, h, 0, S) for h in range(G)])[None]
+    k = synth.k(0, 0, 0, S)[None, None]
+    v = synth.v(0, 0, 0, S)[None, None]
+    op = O.Params(G, 1, wl.head_dim, wl.n_init, wl.n_local, wl.block_size, wl.n_repr, wl.topk)
+    so = O.StreamOracle(q, k, v, op)
+    plan = wl.step_starts()
+    last_units = O.partition(plan[-1][0], op).n_units
+    t0 = time.time()
+    so.group_query_sum(0, 0)
+    for u in range(last_units):
+        so.repr_offsets(0, 0, u)
+    t_units = time.time() - t0
+    stride = max(1, len(plan) // n_chunk_samples)
+    sample = plan[stride - 1::stride]
+    t0 = time.time()
+    for past, n in sample:
+        so.step(0, past, n)
+    t_chunks = time.time() - t0
+    t_full = wl.n_kv_heads * (t_units + t_chunks * len(plan) / len(sample))
+    return {"value": S / t_full, "unit": "ctx tok/s", "cores": threads, "kind": "oracle",
+            "sample": f"kv head 0 of {wl.n_kv_heads}: all {last_units} units built, {len(sample)} of {len(plan)} "
+                      f"chunks (every {stride}th) scored/selected/attended; extrapolated x{len(plan) / len(sample):g} "
+                      f"over chunks and x{wl.n_kv_heads} over kv heads",
+            "sample_seconds": t_units + t_chunks}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--legs", default="1m,decode", help="extra legs: comma list of 1m, decode (or 'none')")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this path runs on one GPU: the whole context memory lives in one "
+                                   "MI355X's HBM and no step exchanges data between GPUs; run with --gpus 1",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+
+    import torch
+    from paper_2402_04617_amd import infllm as F
+    F.lib()
+    torch.cuda.set_device(0)
+
+    main_res, synth, st = encode_leg("llama3-8b-128k", args.seed, args.steps, args.warmup, torch)
+    log(f"128K: {main_res['ms_per_step']:.2f} ms/step, {main_res['ctx_tok_per_s'] / 1e6:.2f}M ctx tok/s; "
+        f"attention {main_res['attention']['tflops']:.0f} TFLOP/s")
+    del st
+    extra = {}
+    legs = [] if args.legs == "none" else [x.strip() for x in args.legs.split(",") if x.strip()]
+    if "1m" in legs:
+        r1, _, st1 = encode_leg("llama3-8b-1m", args.seed, max(1, min(args.steps, 2)), 1, torch)
+        del st1
+        torch.cuda.empty_cache()
+        extra["encode_1m"] = r1
+        log(f"1M: {r1['ms_per_step']:.1f} ms/step, {r1['ctx_tok_per_s'] / 1e6:.2f}M ctx tok/s")
+    if "decode" in legs:
+        rd = decode_leg(args.seed, max(1, min(args.steps, 3)), 1, torch)
+        torch.cuda.empty_cache()
+        extra["decode_16x128k"] = rd
+        log(f"decode: {rd['us_per_step']:.1f} us/step (16 seqs)")
+
+    att = main_res["attention"]
+    achieved = att["tflops"]
+    line = {
+        "metric": "chunk-encode context tok/s at 128K (1M and decode legs in extra)",
+        "value": main_res["ctx_tok_per_s"],
+        "unit": "ctx tok/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": main_res["ms_per_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "llama3-8b-128k", "seq_len": 131072, "batch": 1, "q_heads": 32, "kv_heads": 8,
+                   "head_dim": 128, "n_init": 128, "n_local": 4096, "block_size": 128, "n_repr": 4, "topk": 32,
+                   "chunk": 512, "parallelism": "single-gpu"},
+        "roofline": {"bound": "mfma", "kernel": "attend_mfma_kernel<128>", "achieved": achieved,
+                     "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
+                     "traffic": None, "avg_launch_ms": att["avg_ms"], "launches_per_step": att["launches"]},
+        "extra": extra,
+    }
+    if not args.no_cpu_baseline:
+        t = time.time()
+        line["cpu_baseline"] = cpu_baseline(synth)
+        log(f"cpu baseline: {line['cpu_baseline']['value']:.1f} ctx tok/s ({time.time() - t:.1f}s)")
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -449,7 +449,7 @@ infllm_status infllm_step(const infllm_params* p, const infllm_memory* m, const 
       INFLLM_OK)
     return st;
   const int32_t rows = m->batch * p->n_kv_heads;
-  if ((st = prep_topk(part.n_units > 0 ? rows : 0, scores, part.n_units, p->topk, idx)) != INFLLM_OK) return st;
+  if ((st = prep_topk(rows, scores, part.n_units, p->topk, idx)) != INFLLM_OK) return st;
   if ((st = prepare_attend(p, m, q, q_head_stride, n_q, past_len, idx, p->topk, out, out_head_stride, lse, workspace,
                            workspace_bytes, &at)) != INFLLM_OK)
     return st;
@@ -457,11 +457,10 @@ infllm_status infllm_step(const infllm_params* p, const infllm_memory* m, const 
   hipStream_t s = (hipStream_t)stream;
   if (ba.n_new > 0 && (st = launch_status(launch_build_units(ba, s))) != INFLLM_OK) return st;
   if ((st = launch_status(launch_append(aa, s))) != INFLLM_OK) return st;
-  if (part.n_units > 0) {
-    if ((st = launch_status(launch_score(sa, s))) != INFLLM_OK) return st;
-    if (p->topk > 0 && (st = launch_status(launch_select_topk(rows, scores, part.n_units, p->topk, idx, s))) != INFLLM_OK)
-      return st;
-  }
+  if (part.n_units > 0 && (st = launch_status(launch_score(sa, s))) != INFLLM_OK) return st;
+  // with no units yet this still writes the -1 padding of idx
+  if (p->topk > 0 && (st = launch_status(launch_select_topk(rows, scores, part.n_units, p->topk, idx, s))) != INFLLM_OK)
+    return st;
   if (n_q == 0) return INFLLM_OK;
   if ((st = launch_status(launch_attend(at, s))) != INFLLM_OK) return st;
   if (at.parts == 1) return INFLLM_OK;
