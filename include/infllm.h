@@ -61,7 +61,7 @@ typedef struct {
   int32_t n_repr;     /* r_k in [1, l_bs]: representative tokens per unit */
   int32_t topk;       /* k_m >= 0: units loaded per step */
   int32_t dtype;      /* infllm_dtype of q, k, v and the attention output */
-  float sm_scale;     /* softmax logit scale (1 when q or k arrive pre-scaled) */
+  float sm_scale;     /* softmax logit scale > 0 (1 when q or k arrive pre-scaled) */
 } infllm_params;
 
 /*

@@ -52,7 +52,7 @@ infllm_status check_params(const infllm_params* p) {
   if (p->n_init < 0 || p->n_local < 1 || p->block_size < 1 || p->topk < 0) return INFLLM_E_SHAPE;
   if (p->block_size > 256) return INFLLM_E_UNSUPPORTED;
   if (p->n_repr < 1 || p->n_repr > p->block_size) return INFLLM_E_SHAPE;
-  if (!std::isfinite(p->sm_scale)) return INFLLM_E_SHAPE;
+  if (!std::isfinite(p->sm_scale) || !(p->sm_scale > 0.f)) return INFLLM_E_SHAPE;
   return INFLLM_OK;
 }
 
@@ -353,7 +353,7 @@ infllm_status infllm_append(const infllm_params* p, const infllm_memory* m, cons
   infllm_status st = prep_append(p, m, q, q_head_stride, k, v, kv_head_stride, n_q, past_len, &a);
   if (st != INFLLM_OK) return st;
   if ((st = check_device()) != INFLLM_OK) return st;
-  return launch_status(launch_append(a, (hipStream_t)stream));
+  return launch_status(launch_append(a, (hipStream_t)stream, nullptr));
 }
 
 infllm_status infllm_build_units(const infllm_params* p, const infllm_memory* m, int32_t first_unit, int32_t n_new,
@@ -456,8 +456,13 @@ infllm_status infllm_step(const infllm_params* p, const infllm_memory* m, const 
   if ((st = check_device()) != INFLLM_OK) return st;
   hipStream_t s = (hipStream_t)stream;
   if (ba.n_new > 0 && (st = launch_status(launch_build_units(ba, s))) != INFLLM_OK) return st;
-  if ((st = launch_status(launch_append(aa, s))) != INFLLM_OK) return st;
-  if (part.n_units > 0 && (st = launch_status(launch_score(sa, s))) != INFLLM_OK) return st;
+  // the append's scan also yields the chunk's group-query sums, which scoring consumes directly
+  float* qbar = (float*)workspace;
+  if ((st = launch_status(launch_append(aa, s, part.n_units > 0 ? qbar : nullptr))) != INFLLM_OK) return st;
+  if (part.n_units > 0) {
+    sa.qbar_parts = qbar;
+    if ((st = launch_status(launch_score_given_qbar(sa, 1, s))) != INFLLM_OK) return st;
+  }
   // with no units yet this still writes the -1 padding of idx
   if (p->topk > 0 && (st = launch_status(launch_select_topk(rows, scores, part.n_units, p->topk, idx, s))) != INFLLM_OK)
     return st;

@@ -1,97 +1,219 @@
-// Append of the current tokens: K/V into the token-ordered store, and the
-// running group-query sum into the float64 ring that unit construction reads.
+// Append of the current tokens, in one launch:
+//  - K/V rows of the chunk into the token-ordered store (copy blocks);
+//  - the running group-query sum into the float64 ring that unit construction
+//    reads (scan blocks), and optionally the chunk's group-query total Qbar,
+//    which is exactly what unit scoring needs (the scan total, for free).
 //
 // The representative score of Section 3.2 needs, for every token m, the window
-// sum W_m = sum_{j=1..l_L} sum_{h in group} q^h_{m+j}.  Keeping the running sum
-// Pi_t = sum_{p<=t} sum_h q^h_p lets unit construction form W_m as one difference
-// of two ring slots, so its cost does not grow with l_L.  float64 keeps the
-// difference of two large running sums exact to ~1e-16 relative.
+// sum W_m = sum_{j=1..l_L} sum_{h in group} q^h_{m+j}.  With the running sum
+// Pi_t = sum_{p<=t} sum_h q^h_p kept per position, unit construction forms W_m
+// as one difference of two ring slots, so its cost does not grow with l_L.
+// float64 keeps the difference of two large running sums exact to ~1e-16.
+//
+// Scan block: one (sequence*kv head, 16-dim slice); 256 threads = 128 position
+// segments x 2 halves of 8 dims.  Each thread sums its segment (kSeg positions)
+// in registers, a wave-level shuffle scan and an LDS pass over the 4 waves give
+// the segment offsets, and each thread writes its kSeg ring rows.
 #include "launch.h"
 
 namespace infllm {
 namespace {
 
-// 16-byte vector copy of the chunk's K (or V) rows into the store.
-__global__ void copy_rows_kernel(const uint4* __restrict__ src, uint4* __restrict__ dst,
-                                 int64_t vec_per_head, int64_t src_head_stride_vec,
-                                 int64_t dst_head_stride_vec, int64_t dst_offset_vec,
-                                 int64_t total_vec) {
-  int64_t e = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (e >= total_vec) return;
-  int64_t head = e / vec_per_head;
-  int64_t r = e - head * vec_per_head;
-  dst[head * dst_head_stride_vec + dst_offset_vec + r] = src[head * src_head_stride_vec + r];
+constexpr int kSeg = 4;                 // positions per thread per tile
+constexpr int kTile = 128 * kSeg;       // positions per scan tile
+constexpr int kCopyPerThread = 4;       // 16-byte vectors per thread in copy blocks
+
+template <typename T>
+__device__ __forceinline__ void load8(const T* p, double* out) {
+  const uint4 raw = *(const uint4*)p;
+  if constexpr (sizeof(T) == 2) {
+    const bf16_t* v = (const bf16_t*)&raw;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) out[e] = (double)bf16_to_f32(v[e]);
+  } else {
+    const float* v = (const float*)&raw;
+    const uint4 raw2 = *(const uint4*)(p + 4);
+    const float* v2 = (const float*)&raw2;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      out[e] = (double)v[e];
+      out[4 + e] = (double)v2[e];
+    }
+  }
 }
 
-// One workgroup per (sequence*kv head, 32-dim slice); 8 segments of the chunk
-// are summed in parallel, then scanned, then re-walked to write every slot.
-template <typename T>
-__global__ void __launch_bounds__(256) qprefix_kernel(const T* __restrict__ q, int64_t q_head_stride,
-                                                      int n_q_heads, int n_kv_heads, int head_dim,
-                                                      int n_q, int64_t past_len,
-                                                      double* __restrict__ qprefix, int ring) {
-  constexpr int kSegs = 8;
-  const int bg = blockIdx.x;
-  const int b = bg / n_kv_heads, g = bg - b * n_kv_heads;
-  const int lane = threadIdx.x & 31;
-  const int seg = threadIdx.x >> 5;
-  const int d = blockIdx.y * 32 + lane;
-  const int G = n_q_heads / n_kv_heads;
-  const int seg_len = (n_q + kSegs - 1) / kSegs;
-  const int i0 = min(n_q, seg * seg_len), i1 = min(n_q, i0 + seg_len);
-  const T* qb = q + (int64_t)(b * n_q_heads + g * G) * q_head_stride + d;
-
-  double acc = 0.0;
-  for (int i = i0; i < i1; ++i) {
-    double s = 0.0;
-    for (int h = 0; h < G; ++h) s += (double)Elem<T>::load(qb + h * q_head_stride + (int64_t)i * head_dim);
-    acc += s;
+// GT: the query group size G when known at compile time (0: read it at run time).
+template <typename T, int GT>
+__global__ void __launch_bounds__(256) append_kernel(AppendArgs a, int n_scan_blocks, float* __restrict__ qbar) {
+  const int D = a.head_dim;
+  if ((int)blockIdx.x >= n_scan_blocks) {
+    // ---- copy role: K and V rows of the chunk into the store
+    constexpr int VEC = 16 / sizeof(T);
+    const int64_t vec_per_head = (int64_t)a.n_q * D / VEC;
+    const int64_t total = vec_per_head * a.batch * a.n_kv_heads;
+    const int64_t src_stride = a.kv_head_stride / VEC, dst_stride = a.capacity * D / VEC;
+    const int64_t dst_off = a.past_len * D / VEC;
+    const int64_t base = ((int64_t)blockIdx.x - n_scan_blocks) * 256 * kCopyPerThread + threadIdx.x;
+#pragma unroll
+    for (int j = 0; j < kCopyPerThread; ++j) {
+      const int64_t e = base + (int64_t)j * 256;
+      if (e < total) {
+        const int64_t head = e / vec_per_head, r = e - head * vec_per_head;
+        ((uint4*)a.k_store)[head * dst_stride + dst_off + r] = ((const uint4*)a.k_src)[head * src_stride + r];
+        ((uint4*)a.v_store)[head * dst_stride + dst_off + r] = ((const uint4*)a.v_src)[head * src_stride + r];
+      }
+    }
+    return;
   }
-  __shared__ double seg_sum[kSegs][32];
-  seg_sum[seg][lane] = acc;
+
+  // ---- scan role
+  const int slices = D / 16;
+  const int bg = blockIdx.x / slices;
+  const int b = bg / a.n_kv_heads, g = bg - b * a.n_kv_heads;
+  const int half = threadIdx.x & 1, seg = threadIdx.x >> 1;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int d0 = (blockIdx.x - bg * slices) * 16 + half * 8;
+  const int G = GT > 0 ? GT : a.n_q_heads / a.n_kv_heads;
+  const T* qb = (const T*)a.q + (int64_t)(b * a.n_q_heads + g * G) * a.q_head_stride + d0;
+  double* ring = a.qprefix + (int64_t)bg * a.ring * D + d0;
+
+  __shared__ double wave_tot[4][2][8];
+  const int slot0 = (int)(a.past_len % a.ring);  // ring > n_q: slot0 + i wraps at most once
+  double base[8], carry[8];
+  if (a.past_len > 0) {
+    const double* src = ring + (int64_t)(slot0 == 0 ? a.ring - 1 : slot0 - 1) * D;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) base[e] = src[e];
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) base[e] = 0.0;
+  }
+#pragma unroll
+  for (int e = 0; e < 8; ++e) carry[e] = base[e];
+  // every thread holds the base before any slot is written (new slots never alias it: ring > n_q)
   __syncthreads();
 
-  double* ring_bg = qprefix + (int64_t)bg * ring * head_dim;
-  double run = 0.0;
-  if (past_len > 0) run = ring_bg[((past_len - 1) % ring) * head_dim + d];
-  for (int s = 0; s < seg; ++s) run += seg_sum[s][lane];
-  // Every thread has read the base slot before any slot is written (the new
-  // slots never alias it because ring > n_q).
-  __syncthreads();
-  for (int i = i0; i < i1; ++i) {
-    double s = 0.0;
-    for (int h = 0; h < G; ++h) s += (double)Elem<T>::load(qb + h * q_head_stride + (int64_t)i * head_dim);
-    run += s;
-    ring_bg[((past_len + i) % ring) * head_dim + d] = run;
+  for (int t0 = 0; t0 < a.n_q; t0 += kTile) {
+    const int i0 = t0 + seg * kSeg;
+    double run[kSeg][8];
+    double tot[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) tot[e] = 0.0;
+#pragma unroll
+    for (int s = 0; s < kSeg; ++s) {
+      // clamp instead of branching so every load of the segment is issued up front
+      const int i = min(i0 + s, a.n_q - 1);
+      const bool valid = i0 + s < a.n_q;
+      double x[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) x[e] = 0.0;
+      if constexpr (GT > 0) {
+        double y[GT][8];
+#pragma unroll
+        for (int h = 0; h < GT; ++h) load8<T>(qb + h * a.q_head_stride + (int64_t)i * D, y[h]);
+#pragma unroll
+        for (int h = 0; h < GT; ++h)
+#pragma unroll
+          for (int e = 0; e < 8; ++e) x[e] += y[h][e];
+      } else {
+        for (int h = 0; h < G; ++h) {
+          double y[8];
+          load8<T>(qb + h * a.q_head_stride + (int64_t)i * D, y);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) x[e] += y[e];
+        }
+      }
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        tot[e] += valid ? x[e] : 0.0;
+        run[s][e] = tot[e];
+      }
+    }
+    // inclusive scan of segment totals across the 32 segments of this half in the wave
+    double incl[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) incl[e] = tot[e];
+#pragma unroll
+    for (int o = 2; o < 64; o <<= 1) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const double y = __shfl_up(incl[e], o);
+        if (lane >= o) incl[e] += y;
+      }
+    }
+    if (lane >= 62) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) wave_tot[wave][half][e] = incl[e];
+    }
+    __syncthreads();
+    double off[8], tile_tot[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      off[e] = incl[e] - tot[e];
+      tile_tot[e] = 0.0;
+    }
+    for (int w = 0; w < 4; ++w) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        const double y = wave_tot[w][half][e];
+        off[e] += (w < wave) ? y : 0.0;
+        tile_tot[e] += y;
+      }
+    }
+#pragma unroll
+    for (int s = 0; s < kSeg; ++s) {
+      const int i = i0 + s;
+      if (i < a.n_q) {
+        const int slot = slot0 + i - (slot0 + i >= a.ring ? a.ring : 0);
+        double* dst = ring + (int64_t)slot * D;
+        double2* d2 = (double2*)dst;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          d2[e] = make_double2(carry[2 * e] + off[2 * e] + run[s][2 * e],
+                               carry[2 * e + 1] + off[2 * e + 1] + run[s][2 * e + 1]);
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) carry[e] += tile_tot[e];
+    __syncthreads();
+  }
+  if (qbar != nullptr && seg == 0) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) qbar[(int64_t)bg * D + d0 + e] = (float)(carry[e] - base[e]);
   }
 }
 
 }  // namespace
 
-hipError_t launch_append(const AppendArgs& a, hipStream_t s) {
+hipError_t launch_append(const AppendArgs& a, hipStream_t s, float* qbar) {
   if (a.n_q == 0) return hipSuccess;
   const int esize = a.bf16 ? 2 : 4;
-  const int vec = 16 / esize;
+  const int n_scan = a.batch * a.n_kv_heads * (a.head_dim / 16);
+  int n_copy = 0;
   if (a.k_src != nullptr) {
-    int64_t vec_per_head = (int64_t)a.n_q * a.head_dim / vec;
-    int64_t heads = (int64_t)a.batch * a.n_kv_heads;
-    int64_t total = vec_per_head * heads;
-    int64_t src_stride = a.kv_head_stride / vec;
-    int64_t dst_stride = a.capacity * a.head_dim / vec;
-    int64_t dst_off = a.past_len * a.head_dim / vec;
-    dim3 grid((unsigned)((total + 255) / 256));
-    hipLaunchKernelGGL(copy_rows_kernel, grid, dim3(256), 0, s, (const uint4*)a.k_src, (uint4*)a.k_store,
-                       vec_per_head, src_stride, dst_stride, dst_off, total);
-    hipLaunchKernelGGL(copy_rows_kernel, grid, dim3(256), 0, s, (const uint4*)a.v_src, (uint4*)a.v_store,
-                       vec_per_head, src_stride, dst_stride, dst_off, total);
+    const int64_t total = (int64_t)a.n_q * a.head_dim / (16 / esize) * a.batch * a.n_kv_heads;
+    n_copy = (int)((total + 256 * kCopyPerThread - 1) / (256 * kCopyPerThread));
   }
-  dim3 grid(a.batch * a.n_kv_heads, a.head_dim / 32);
-  if (a.bf16)
-    hipLaunchKernelGGL(qprefix_kernel<bf16_t>, grid, dim3(256), 0, s, (const bf16_t*)a.q, a.q_head_stride,
-                       a.n_q_heads, a.n_kv_heads, a.head_dim, a.n_q, a.past_len, a.qprefix, a.ring);
-  else
-    hipLaunchKernelGGL(qprefix_kernel<float>, grid, dim3(256), 0, s, (const float*)a.q, a.q_head_stride,
-                       a.n_q_heads, a.n_kv_heads, a.head_dim, a.n_q, a.past_len, a.qprefix, a.ring);
+  dim3 grid(n_scan + n_copy);
+  const int G = a.n_q_heads / a.n_kv_heads;
+#define INFLLM_APPEND(T, GT) hipLaunchKernelGGL((append_kernel<T, GT>), grid, dim3(256), 0, s, a, n_scan, qbar)
+  if (a.bf16) {
+    switch (G) {
+      case 1: INFLLM_APPEND(bf16_t, 1); break;
+      case 2: INFLLM_APPEND(bf16_t, 2); break;
+      case 4: INFLLM_APPEND(bf16_t, 4); break;
+      case 8: INFLLM_APPEND(bf16_t, 8); break;
+      default: INFLLM_APPEND(bf16_t, 0); break;
+    }
+  } else {
+    switch (G) {
+      case 1: INFLLM_APPEND(float, 1); break;
+      case 2: INFLLM_APPEND(float, 2); break;
+      case 4: INFLLM_APPEND(float, 4); break;
+      default: INFLLM_APPEND(float, 0); break;
+    }
+  }
+#undef INFLLM_APPEND
   return hipGetLastError();
 }
 

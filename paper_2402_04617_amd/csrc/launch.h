@@ -22,7 +22,8 @@ struct AppendArgs {
   double* qprefix;
   bool bf16;
 };
-hipError_t launch_append(const AppendArgs& a, hipStream_t s);
+// qbar: optional [batch*Hkv][D] float32 output of the chunk's group-query sums.
+hipError_t launch_append(const AppendArgs& a, hipStream_t s, float* qbar);
 
 struct BuildArgs {
   int batch, n_q_heads, n_kv_heads, head_dim, n_init, n_local, block_size, n_repr;
@@ -48,6 +49,8 @@ struct ScoreArgs {
 };
 int score_qbar_parts(int G, int n_q);
 hipError_t launch_score(const ScoreArgs& a, hipStream_t s);
+// Scoring when a.qbar_parts already holds the query sums as `parts` partials.
+hipError_t launch_score_given_qbar(const ScoreArgs& a, int parts, hipStream_t s);
 
 hipError_t launch_select_topk(int rows, const float* scores, int n_units, int k, int32_t* idx,
                               hipStream_t s);

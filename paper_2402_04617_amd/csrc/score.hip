@@ -97,6 +97,11 @@ hipError_t launch_score(const ScoreArgs& a, hipStream_t s) {
   else
     hipLaunchKernelGGL(qbar_kernel<float>, g1, dim3(256), 0, s, (const float*)a.q, a.q_head_stride,
                        a.n_q_heads, a.n_kv_heads, a.head_dim, a.n_q, parts, a.qbar_parts);
+  return launch_score_given_qbar(a, parts, s);
+}
+
+hipError_t launch_score_given_qbar(const ScoreArgs& a, int parts, hipStream_t s) {
+  if (a.n_units == 0) return hipSuccess;
   dim3 g2((a.n_units + 255) / 256, a.batch * a.n_kv_heads);
   hipLaunchKernelGGL(score_kernel, g2, dim3(256), 0, s, (const float*)a.qbar_parts, parts,
                      (const float4*)a.unit_ksum, a.head_dim, a.n_units, a.max_units, a.scores);

@@ -75,7 +75,7 @@ def test_partition_errors(L):
     (dict(n_kv_heads=7), 2), (dict(n_q_heads=0), 2), (dict(head_dim=96), 4), (dict(head_dim=0), 2),
     (dict(n_local=0), 2), (dict(block_size=0), 2), (dict(block_size=512, n_repr=4), 4),
     (dict(n_repr=0), 2), (dict(n_repr=129), 2), (dict(topk=-1), 2), (dict(n_init=-1), 2),
-    (dict(sm_scale=float("inf")), 2),
+    (dict(sm_scale=float("inf")), 2), (dict(sm_scale=0.0), 2), (dict(sm_scale=-1.0), 2),
 ])
 def test_param_validation(L, kw, code):
     p = P(**kw)
