@@ -47,24 +47,27 @@ template <typename T, int GT>
 __global__ void __launch_bounds__(256) append_kernel(AppendArgs a, int n_scan_blocks, float* __restrict__ qbar) {
   const int D = a.head_dim;
   if ((int)blockIdx.x >= n_scan_blocks) {
-    // ---- copy role: K and V rows of the chunk into the store
+    // ---- copy role: K and V rows of the chunk into the store.  blockIdx.y is
+    // the (sequence, kv head); each thread moves kCopyPerThread 16-byte vectors.
     constexpr int VEC = 16 / sizeof(T);
-    const int64_t vec_per_head = (int64_t)a.n_q * D / VEC;
-    const int64_t total = vec_per_head * a.batch * a.n_kv_heads;
-    const int64_t src_stride = a.kv_head_stride / VEC, dst_stride = a.capacity * D / VEC;
-    const int64_t dst_off = a.past_len * D / VEC;
-    const int64_t base = ((int64_t)blockIdx.x - n_scan_blocks) * 256 * kCopyPerThread + threadIdx.x;
+    const int vec_per_head = a.n_q * D / VEC;
+    const int64_t head = blockIdx.y;
+    const uint4* src_k = (const uint4*)a.k_src + head * (a.kv_head_stride / VEC);
+    const uint4* src_v = (const uint4*)a.v_src + head * (a.kv_head_stride / VEC);
+    uint4* dst_k = (uint4*)a.k_store + head * (a.capacity * D / VEC) + a.past_len * D / VEC;
+    uint4* dst_v = (uint4*)a.v_store + head * (a.capacity * D / VEC) + a.past_len * D / VEC;
+    const int base = ((int)blockIdx.x - n_scan_blocks) * 256 * kCopyPerThread + threadIdx.x;
 #pragma unroll
     for (int j = 0; j < kCopyPerThread; ++j) {
-      const int64_t e = base + (int64_t)j * 256;
-      if (e < total) {
-        const int64_t head = e / vec_per_head, r = e - head * vec_per_head;
-        ((uint4*)a.k_store)[head * dst_stride + dst_off + r] = ((const uint4*)a.k_src)[head * src_stride + r];
-        ((uint4*)a.v_store)[head * dst_stride + dst_off + r] = ((const uint4*)a.v_src)[head * src_stride + r];
+      const int e = base + j * 256;
+      if (e < vec_per_head) {
+        dst_k[e] = src_k[e];
+        dst_v[e] = src_v[e];
       }
     }
     return;
   }
+  if (blockIdx.y != 0) return;
 
   // ---- scan role
   const int slices = D / 16;
@@ -191,10 +194,12 @@ hipError_t launch_append(const AppendArgs& a, hipStream_t s, float* qbar) {
   const int n_scan = a.batch * a.n_kv_heads * (a.head_dim / 16);
   int n_copy = 0;
   if (a.k_src != nullptr) {
-    const int64_t total = (int64_t)a.n_q * a.head_dim / (16 / esize) * a.batch * a.n_kv_heads;
-    n_copy = (int)((total + 256 * kCopyPerThread - 1) / (256 * kCopyPerThread));
+    const int vec_per_head = a.n_q * a.head_dim / (16 / esize);
+    n_copy = (vec_per_head + 256 * kCopyPerThread - 1) / (256 * kCopyPerThread);
   }
-  dim3 grid(n_scan + n_copy);
+  // x: scan blocks then copy blocks; y: (sequence, kv head) for the copy blocks
+  // (scan blocks with y > 0 exit at once)
+  dim3 grid(n_scan + n_copy, n_copy > 0 ? a.batch * a.n_kv_heads : 1);
   const int G = a.n_q_heads / a.n_kv_heads;
 #define INFLLM_APPEND(T, GT) hipLaunchKernelGGL((append_kernel<T, GT>), grid, dim3(256), 0, s, a, n_scan, qbar)
   if (a.bf16) {

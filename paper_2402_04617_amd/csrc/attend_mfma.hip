@@ -121,7 +121,7 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
   constexpr int PATCHES = (KB / 4) * CH;
   static_assert(PATCHES <= 256, "one patch per thread");
   const bool stager = tid < PATCHES;
-  const int kq = tid / CH, kc = tid % CH;
+  const int kq = (tid % PATCHES) / CH, kc = tid % CH;  // non-stagers load a duplicate patch, store nothing
   Stage st;
 
   // A tile inside one segment (I, one selected unit, or the L+X run) maps to 64
@@ -151,7 +151,6 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
     const int64_t r = tile_run_start(tile);  // uniform: keep it in scalar registers
     const int64_t run0 = ((int64_t)__builtin_amdgcn_readfirstlane((int)(r >> 32)) << 32) |
                          (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)r);
-    if (!stager) return;
     int64_t p0, p1, p2, p3;
     if (run0 >= 0) {
       st.mask = 0xF;
@@ -246,7 +245,10 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
 
   for (int t = t_begin; t < t_end; ++t) {
     const int buf = (t - t_begin) & 1;
-    if (t + 1 < t_end) load_tile(t + 1);
+    // Unconditional prefetch (the last iteration re-fetches its own tile and
+    // never stores it): no register join at the back edge, so the loads stay
+    // in flight across the whole iteration.
+    load_tile(min(t + 1, t_end - 1));
 
     const bf16_t* Kb = sm.k[buf];
     const bf16_t* Vb = sm.vt[buf];

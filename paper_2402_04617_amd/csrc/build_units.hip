@@ -15,6 +15,7 @@ namespace infllm {
 namespace {
 
 constexpr int kMaxBlock = 256;
+constexpr int kMaxSumElems = 2048;  // staged representative-key elements
 
 template <typename T, int D>
 __global__ void __launch_bounds__(1024) build_units_kernel(BuildArgs a) {
@@ -108,10 +109,19 @@ __global__ void __launch_bounds__(1024) build_units_kernel(BuildArgs a) {
   }
   __syncthreads();
 
-  // Sum of the representative keys, in ascending position order, float32.
+  // Sum of the representative keys, in ascending position order, float32:
+  // one load per (representative, dim) thread, then a fixed-order sum in LDS.
+  __shared__ float rk[kMaxSumElems];
+  const int nrep_load = min(a.n_repr, kMaxSumElems / D);
+  for (int e = tid; e < nrep_load * D; e += blockDim.x) {
+    const int j = e / D, d = e - j * D;
+    rk[e] = Elem<T>::load(kb + (m0 + chosen[j]) * D + d);
+  }
+  __syncthreads();
   for (int d = tid; d < D; d += blockDim.x) {
     float s = 0.f;
-    for (int j = 0; j < a.n_repr; ++j) s += Elem<T>::load(kb + (m0 + chosen[j]) * D + d);
+    for (int j = 0; j < nrep_load; ++j) s += rk[j * D + d];
+    for (int j = nrep_load; j < a.n_repr; ++j) s += Elem<T>::load(kb + (m0 + chosen[j]) * D + d);
     a.unit_ksum[(((int64_t)bg * (D / 4) + d / 4) * a.max_units + unit) * 4 + (d & 3)] = s;
   }
   if (a.repr_score != nullptr) {
