@@ -200,9 +200,9 @@ def decode_leg(seed, steps, warmup, torch):
             "tok_per_s": wl.batch * len(plan) / (ms / 1e3)}
 
 
-def cpu_baseline(synth, n_chunk_samples=16):
+def cpu_baseline(synth, n_chunk_samples=64):
     """The oracle on a bounded sample of the 128K encode: kv head 0 (of 8) with its 4 query heads;
-    all of that head's units are built, and every 16th chunk is scored, looked up and attended.
+    all of that head's units are built, and every 4th chunk is scored, looked up and attended.
     Extrapolated linearly to all chunks and all kv heads."""
     from oracle import infllm_oracle as O
     try:
