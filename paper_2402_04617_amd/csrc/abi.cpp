@@ -353,7 +353,7 @@ infllm_status infllm_append(const infllm_params* p, const infllm_memory* m, cons
   infllm_status st = prep_append(p, m, q, q_head_stride, k, v, kv_head_stride, n_q, past_len, &a);
   if (st != INFLLM_OK) return st;
   if ((st = check_device()) != INFLLM_OK) return st;
-  return launch_status(launch_append(a, (hipStream_t)stream, nullptr));
+  return launch_status(launch_append(a, (hipStream_t)stream, nullptr, nullptr));
 }
 
 infllm_status infllm_build_units(const infllm_params* p, const infllm_memory* m, int32_t first_unit, int32_t n_new,
@@ -455,10 +455,17 @@ infllm_status infllm_step(const infllm_params* p, const infllm_memory* m, const 
     return st;
   if ((st = check_device()) != INFLLM_OK) return st;
   hipStream_t s = (hipStream_t)stream;
-  if (ba.n_new > 0 && (st = launch_status(launch_build_units(ba, s))) != INFLLM_OK) return st;
+  // Unit construction reads ring slots of positions >= its first token m0; the
+  // append writes the slots of [past_len, past_len + n_q).  When the ring is
+  // large enough for those never to coincide, both run in one launch.
+  const int64_t m0 = (int64_t)p->n_init + (int64_t)units_built * p->block_size;
+  const bool fuse = ba.n_new > 0 && n_q > 0 && m0 >= past_len + n_q - m->ring;
+  if (ba.n_new > 0 && !fuse && (st = launch_status(launch_build_units(ba, s))) != INFLLM_OK) return st;
   // the append's scan also yields the chunk's group-query sums, which scoring consumes directly
   float* qbar = (float*)workspace;
-  if ((st = launch_status(launch_append(aa, s, part.n_units > 0 ? qbar : nullptr))) != INFLLM_OK) return st;
+  if ((st = launch_status(launch_append(aa, s, part.n_units > 0 ? qbar : nullptr, fuse ? &ba : nullptr))) !=
+      INFLLM_OK)
+    return st;
   if (part.n_units > 0) {
     sa.qbar_parts = qbar;
     if ((st = launch_status(launch_score_given_qbar(sa, 1, s))) != INFLLM_OK) return st;

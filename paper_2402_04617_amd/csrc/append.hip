@@ -10,11 +10,19 @@
 // as one difference of two ring slots, so its cost does not grow with l_L.
 // float64 keeps the difference of two large running sums exact to ~1e-16.
 //
+// In the whole-step path the same launch also carries the unit-construction
+// blocks of the units evicted since the previous step (see unit_build.h): they
+// read ring slots of earlier positions, which the chunk's new slots cannot
+// overwrite when the ring is large enough (checked on the host), so the two
+// latency-bound jobs overlap instead of running back to back.
+//
 // Scan block: one (sequence*kv head, 16-dim slice); 256 threads = 128 position
 // segments x 2 halves of 8 dims.  Each thread sums its segment (kSeg positions)
 // in registers, a wave-level shuffle scan and an LDS pass over the 4 waves give
 // the segment offsets, and each thread writes its kSeg ring rows.
-#include "launch.h"
+#include <cstring>
+
+#include "unit_build.h"
 
 namespace infllm {
 namespace {
@@ -42,21 +50,40 @@ __device__ __forceinline__ void load8(const T* p, double* out) {
   }
 }
 
+// Block roles along the 1-D grid: [unit construction | scan | copy].
+struct AppendGrid {
+  int n_build;          // unit-construction blocks (n_new * batch * Hkv), 0 when not fused
+  int n_scan;           // scan blocks
+  int n_copy_per_head;  // copy blocks per (sequence, kv head)
+};
+
 // GT: the query group size G when known at compile time (0: read it at run time).
-template <typename T, int GT>
-__global__ void __launch_bounds__(256) append_kernel(AppendArgs a, int n_scan_blocks, float* __restrict__ qbar) {
+template <typename T, int GT, int DT>
+__global__ void __launch_bounds__(256) append_kernel(AppendArgs a, BuildArgs ba, AppendGrid grid,
+                                                     float* __restrict__ qbar) {
   const int D = a.head_dim;
-  if ((int)blockIdx.x >= n_scan_blocks) {
-    // ---- copy role: K and V rows of the chunk into the store.  blockIdx.y is
-    // the (sequence, kv head); each thread moves kCopyPerThread 16-byte vectors.
+  __shared__ BuildSmem bsm;
+  int blk = blockIdx.x;
+  if (blk < grid.n_build) {
+    // ---- unit-construction role
+    const int bh = ba.batch * ba.n_kv_heads;
+    build_one_unit<T, DT, 256>(ba, blk / bh, blk % bh, bsm);
+    return;
+  }
+  blk -= grid.n_build;
+  if (blk >= grid.n_scan) {
+    // ---- copy role: K and V rows of the chunk into the store; each thread
+    // moves kCopyPerThread 16-byte vectors of one (sequence, kv head).
+    blk -= grid.n_scan;
     constexpr int VEC = 16 / sizeof(T);
     const int vec_per_head = a.n_q * D / VEC;
-    const int64_t head = blockIdx.y;
+    const int64_t head = blk / grid.n_copy_per_head;
+    const int cblk = blk % grid.n_copy_per_head;
     const uint4* src_k = (const uint4*)a.k_src + head * (a.kv_head_stride / VEC);
     const uint4* src_v = (const uint4*)a.v_src + head * (a.kv_head_stride / VEC);
     uint4* dst_k = (uint4*)a.k_store + head * (a.capacity * D / VEC) + a.past_len * D / VEC;
     uint4* dst_v = (uint4*)a.v_store + head * (a.capacity * D / VEC) + a.past_len * D / VEC;
-    const int base = ((int)blockIdx.x - n_scan_blocks) * 256 * kCopyPerThread + threadIdx.x;
+    const int base = cblk * 256 * kCopyPerThread + threadIdx.x;
 #pragma unroll
     for (int j = 0; j < kCopyPerThread; ++j) {
       const int e = base + j * 256;
@@ -67,15 +94,14 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a, int n_scan_bl
     }
     return;
   }
-  if (blockIdx.y != 0) return;
 
   // ---- scan role
   const int slices = D / 16;
-  const int bg = blockIdx.x / slices;
+  const int bg = blk / slices;
   const int b = bg / a.n_kv_heads, g = bg - b * a.n_kv_heads;
   const int half = threadIdx.x & 1, seg = threadIdx.x >> 1;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int d0 = (blockIdx.x - bg * slices) * 16 + half * 8;
+  const int d0 = (blk - bg * slices) * 16 + half * 8;
   const int G = GT > 0 ? GT : a.n_q_heads / a.n_kv_heads;
   const T* qb = (const T*)a.q + (int64_t)(b * a.n_q_heads + g * G) * a.q_head_stride + d0;
   double* ring = a.qprefix + (int64_t)bg * a.ring * D + d0;
@@ -188,20 +214,12 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a, int n_scan_bl
 
 }  // namespace
 
-hipError_t launch_append(const AppendArgs& a, hipStream_t s, float* qbar) {
-  if (a.n_q == 0) return hipSuccess;
-  const int esize = a.bf16 ? 2 : 4;
-  const int n_scan = a.batch * a.n_kv_heads * (a.head_dim / 16);
-  int n_copy = 0;
-  if (a.k_src != nullptr) {
-    const int vec_per_head = a.n_q * a.head_dim / (16 / esize);
-    n_copy = (vec_per_head + 256 * kCopyPerThread - 1) / (256 * kCopyPerThread);
-  }
-  // x: scan blocks then copy blocks; y: (sequence, kv head) for the copy blocks
-  // (scan blocks with y > 0 exit at once)
-  dim3 grid(n_scan + n_copy, n_copy > 0 ? a.batch * a.n_kv_heads : 1);
+template <int DT>
+static hipError_t launch_append_d(const AppendArgs& a, const BuildArgs& ba, const AppendGrid& g, hipStream_t s,
+                                  float* qbar) {
+  const dim3 grid(g.n_build + g.n_scan + g.n_copy_per_head * a.batch * a.n_kv_heads);
   const int G = a.n_q_heads / a.n_kv_heads;
-#define INFLLM_APPEND(T, GT) hipLaunchKernelGGL((append_kernel<T, GT>), grid, dim3(256), 0, s, a, n_scan, qbar)
+#define INFLLM_APPEND(T, GT) hipLaunchKernelGGL((append_kernel<T, GT, DT>), grid, dim3(256), 0, s, a, ba, g, qbar)
   if (a.bf16) {
     switch (G) {
       case 1: INFLLM_APPEND(bf16_t, 1); break;
@@ -220,6 +238,23 @@ hipError_t launch_append(const AppendArgs& a, hipStream_t s, float* qbar) {
   }
 #undef INFLLM_APPEND
   return hipGetLastError();
+}
+
+hipError_t launch_append(const AppendArgs& a, hipStream_t s, float* qbar, const BuildArgs* fused_build) {
+  AppendGrid g;
+  g.n_build = fused_build != nullptr ? fused_build->n_new * fused_build->batch * fused_build->n_kv_heads : 0;
+  if (a.n_q == 0 && g.n_build == 0) return hipSuccess;
+  const int esize = a.bf16 ? 2 : 4;
+  g.n_scan = a.n_q > 0 ? a.batch * a.n_kv_heads * (a.head_dim / 16) : 0;
+  g.n_copy_per_head = 0;
+  if (a.k_src != nullptr && a.n_q > 0) {
+    const int vec_per_head = a.n_q * a.head_dim / (16 / esize);
+    g.n_copy_per_head = (vec_per_head + 256 * kCopyPerThread - 1) / (256 * kCopyPerThread);
+  }
+  BuildArgs ba;
+  if (fused_build != nullptr) ba = *fused_build;
+  else std::memset(&ba, 0, sizeof(ba));
+  return a.head_dim == 128 ? launch_append_d<128>(a, ba, g, s, qbar) : launch_append_d<64>(a, ba, g, s, qbar);
 }
 
 }  // namespace infllm

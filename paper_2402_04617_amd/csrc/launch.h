@@ -22,8 +22,11 @@ struct AppendArgs {
   double* qprefix;
   bool bf16;
 };
+struct BuildArgs;
 // qbar: optional [batch*Hkv][D] float32 output of the chunk's group-query sums.
-hipError_t launch_append(const AppendArgs& a, hipStream_t s, float* qbar);
+// fused_build: optional unit construction carried by the same launch (its ring
+// reads must not overlap the chunk's new ring slots).
+hipError_t launch_append(const AppendArgs& a, hipStream_t s, float* qbar, const BuildArgs* fused_build);
 
 struct BuildArgs {
   int batch, n_q_heads, n_kv_heads, head_dim, n_init, n_local, block_size, n_repr;

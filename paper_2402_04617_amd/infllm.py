@@ -213,5 +213,6 @@ def alloc_memory(p: Params, batch: int, capacity: int, max_units: int, ring: int
 
 
 def recommended_ring(p: Params, chunk: int) -> int:
-    """Ring slots that cover the oldest window unit construction can still need."""
-    return p.n_local + p.block_size + chunk + 1
+    """Ring slots that cover the oldest window unit construction can still need, plus one chunk, so
+    that infllm_step can run unit construction and the append in a single launch."""
+    return p.n_local + p.block_size + 2 * chunk + 1

@@ -26,11 +26,11 @@ def wl_params(wl):
                     wl.n_repr, wl.topk, wl.dtype)
 
 
-def run_and_check(wl, seed, check_steps, q, k, v, score_rel=None):
+def run_and_check(wl, seed, check_steps, q, k, v, score_rel=None, ring=None):
     p = wl_params(wl)
     op = oparams(p)
     G = wl.group
-    L = Layer(p, wl.batch, wl.seq_len, chunk=wl.chunk)
+    L = Layer(p, wl.batch, wl.seq_len, chunk=wl.chunk, ring=ring)
     qd, kd, vd = dev(q, wl.dtype), dev(k, wl.dtype), dev(v, wl.dtype)
     so = O.StreamOracle(q, k, v, op)
     steps = wl.step_starts()
@@ -68,6 +68,18 @@ def test_stream_tiny_f32_every_step():
     s = Synth(wl, 0)
     q, k, v = s.full("q"), s.full("k"), s.full("v")
     run_and_check(wl, 0, set(range(len(wl.step_starts()))), q, k, v)
+
+
+def test_stream_tiny_f32_short_ring():
+    """A ring one chunk shorter than recommended_ring: infllm_step then runs unit construction
+    and the append as two launches (the single-launch form needs the extra chunk of slots)."""
+    wl = WORKLOADS["tiny-2k-f32"]
+    p = wl_params(wl)
+    ring = p.n_local + p.block_size + wl.chunk + 1
+    assert ring < F.recommended_ring(p, wl.chunk)
+    s = Synth(wl, 2)
+    q, k, v = s.full("q"), s.full("k"), s.full("v")
+    run_and_check(wl, 2, set(range(len(wl.step_starts()))), q, k, v, ring=ring)
 
 
 @pytest.mark.parametrize("seed", [0, 1])
