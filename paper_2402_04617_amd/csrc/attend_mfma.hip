@@ -6,17 +6,18 @@
 //            head g*G + r%G), so the G heads sharing a K/V tile are packed together;
 //            128 rows per workgroup, 32 per wave.
 //   keys   : the virtual key axis (see StepGeom) in tiles of 64 keys, gathered
-//            straight from the token-ordered store (a selected unit is contiguous),
-//            double-buffered through LDS; optionally split into parts whose partial
-//            softmaxes are merged afterwards by log-sum-exp.
+//            straight from the token-ordered store (a selected unit is contiguous)
+//            into LDS by direct global->LDS loads (no staging registers), double
+//            buffered; optionally split into parts whose partial softmaxes are
+//            merged afterwards by log-sum-exp.
 // Per wave and key tile:
 //   S^T = K Q^T  : A = K tile rows from LDS, B = the wave's Q rows held in VGPRs.
 //                  The 32x32 accumulator gives each lane one query row and 16 keys.
 //   online softmax in the exp2 domain, row max combined across the two lane halves.
 //   O^T += V^T P^T: B = P^T taken directly from the S^T accumulator (no shuffle);
-//                  A = V^T from LDS, where V is stored transposed with the key order
-//                  inside each 16-key group permuted to match the accumulator's key
-//                  order, so each A fragment is one 16-byte LDS read.
+//                  A = V^T fragments read from the key-major V tile with the LDS
+//                  transpose read (ds_read_b64_tr_b16), in the key order the
+//                  accumulator layout gives P^T.
 #include "launch.h"
 
 namespace infllm {
@@ -26,44 +27,51 @@ constexpr int KB = 64;      // keys per tile
 constexpr int NWAVE = 4;
 constexpr int ROWS_WG = 32 * NWAVE;
 
+typedef short i16x4 __attribute__((ext_vector_type(4)));
+#define INFLLM_LDS __attribute__((address_space(3)))
+
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
-__device__ __forceinline__ uint32_t dword(const u32x4& v, int w) { return v[w]; }
-
-// Stored column of key `key` (0..63) in a V^T row: groups of 16 keys, each group
-// ordered [0-3, 8-11, 4-7, 12-15].
-__device__ __forceinline__ int vt_col(int key) {
-  const int k16 = key & 15;
-  return (key & ~15) + 8 * ((k16 >> 2) & 1) + 4 * (k16 >> 3) + (k16 & 3);
+// Direct global->LDS loads (16 bytes per lane; lane i lands at LDS byte
+// lds + 16*i, lds taken from M0).  Written as inline assembly so that the
+// compiler does not guard every later LDS read with a wait for these loads: the
+// kernel waits for them itself (s_waitcnt before the barrier that publishes a
+// tile).  No compiler-generated code in these kernels uses M0.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+// Contiguous run: wave-uniform base address plus a per-lane 32-bit byte offset.
+__device__ __forceinline__ void lds_load_run(uint32_t lds, const void* base, uint32_t off) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, %2" : : "s"(lds), "v"(off), "s"(base) : "m0");
 }
+// Gather: a full per-lane address.
+__device__ __forceinline__ void lds_load_lane(uint32_t lds, const void* p) {
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" : : "s"(lds), "v"(p) : "m0");
+}
+#pragma clang diagnostic pop
 
-struct Stage {
-  u32x4 k0, k1, k2, k3, v0, v1, v2, v3;
-  uint32_t mask;
-};
-
-// LDS tiles are unpadded and XOR-swizzled at 16-byte (8 x bf16) granularity, so
-// that both the MFMA fragment reads (8 consecutive rows, one granule each) and
-// the staging writes spread over all LDS banks.
-//   K   [64 keys][D]:  granule g of row r stored at g ^ (r & 7)
-//   V^T [D][64 keys]:  granule g of row r stored at g ^ ((r & 7) ^ ((r >> 3) & 7))
+// Both LDS tiles are key-major [64 keys][D], unpadded, with the 16-byte granules
+// of row r XOR-swizzled by r & 7 (granule g stored at g ^ (r & 7)): the MFMA K
+// reads (8 consecutive rows, one granule each) and the transposed V reads
+// (4 rows x 32 bytes per 16 lanes) then spread over the LDS banks, and a 1 KB
+// direct-load instruction still writes one contiguous LDS range.
 template <int D>
-__device__ __forceinline__ int k_lds(int r, int g) { return r * D + 8 * (g ^ (r & 7)); }
-__device__ __forceinline__ int vt_lds(int r, int g) { return r * KB + 8 * (g ^ ((r & 7) ^ ((r >> 3) & 7))); }
+__device__ __forceinline__ int tile_off(int r, int g) { return r * D + 8 * (g ^ (r & 7)); }
 
 template <int D>
 struct Smem {
   bf16_t k[2][KB * D];
-  bf16_t vt[2][D * KB];
+  bf16_t v[2][KB * D];
   uint8_t kvalid[2][KB];
-  int has_invalid;
 };
 
 template <int D>
 __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
-  constexpr int CH = D / 8;      // 16-byte chunks per row
-  constexpr int KSTEPS = D / 16; // MFMA k-steps over the head dim
-  constexpr int DBLK = D / 32;   // 32-wide output blocks
+  constexpr int CH = D / 8;                   // 16-byte granules per row
+  constexpr int KSTEPS = D / 16;              // MFMA k-steps over the head dim
+  constexpr int DBLK = D / 32;                // 32-wide output blocks
+  constexpr int RPI = 64 / CH;                // tile rows per 1 KB load instruction
+  constexpr int NI = KB * D * 2 / (NWAVE * 1024);  // load instructions per wave per tile (K or V)
+  static_assert(NI * NWAVE * RPI == KB, "tile rows covered exactly once");
   __shared__ __attribute__((aligned(16))) Smem<D> sm;
 
   const StepGeom& geo = a.geom;
@@ -88,7 +96,8 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
   }
 
   const int tid = threadIdx.x;
-  const int lane = tid & 63, wave = tid >> 6;
+  const int lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 31, gsel = lane >> 5;
   const int row = rt * ROWS_WG + wave * 32 + n;
   const bool row_ok = row < R;
@@ -99,10 +108,13 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
   const bf16_t* kbase = (const bf16_t*)a.k_store + (int64_t)bg * a.capacity * D;
   const bf16_t* vbase = (const bf16_t*)a.v_store + (int64_t)bg * a.capacity * D;
 
-  if (tid == 0) {
-    int bad = 0;
-    for (int u = 0; u < geo.n_sel; ++u) bad |= (idx_row[u] < 0 || idx_row[u] >= geo.n_units);
-    sm.has_invalid = bad;
+  // Any skipped (out-of-range) unit entry?  Then every tile takes the per-key
+  // gather path and the validity mask.
+  bool has_invalid;
+  {
+    bool bad = false;
+    for (int u = lane; u < geo.n_sel; u += 64) bad |= (idx_row[u] < 0 || idx_row[u] >= geo.n_units);
+    has_invalid = __ballot(bad) != 0;
   }
 
   // Q rows of this wave as the B operand (8 bf16 per lane per k-step).
@@ -116,20 +128,22 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
     }
   }
 
-  // Staging: each thread moves 4 consecutive keys x 8 dims of K and of V (one
-  // patch; for D = 64 half the threads idle).
-  constexpr int PATCHES = (KB / 4) * CH;
-  static_assert(PATCHES <= 256, "one patch per thread");
-  const bool stager = tid < PATCHES;
-  const int kq = (tid % PATCHES) / CH, kc = tid % CH;  // non-stagers load a duplicate patch, store nothing
-  Stage st;
+  // Direct loads: instruction j of wave w fills LDS granules [(NI*w + j)*64, +64)
+  // of the tile, lane l writing granule slot l; that slot belongs to tile row
+  // r_j = (NI*w + j)*RPI + l / CH and holds its global granule (l % CH) ^ (r_j & 7).
+  int lrow[NI], lgran[NI];
+#pragma unroll
+  for (int j = 0; j < NI; ++j) {
+    lrow[j] = (NI * wave + j) * RPI + lane / CH;
+    lgran[j] = (lane % CH) ^ (lrow[j] & 7);
+  }
 
   // A tile inside one segment (I, one selected unit, or the L+X run) maps to 64
   // consecutive store positions: the common case, gathered with no per-key work.
   // Returns that first position (uniform across the workgroup) or -1.
   auto tile_run_start = [&](int tile) -> int64_t {
     const int v0 = tile * KB;
-    if (v0 + KB > geo.n_virtual) return -1;
+    if (has_invalid || v0 + KB > geo.n_virtual) return -1;
     if (v0 + KB <= geo.n_init) return v0;
     if (v0 < geo.n_init) return -1;
     const int w = v0 - geo.n_init;
@@ -139,80 +153,72 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
     const int u = w / geo.block_size;
     if ((w + KB - 1) / geo.block_size != u) return -1;
     const int bu = idx_row[u];
-    if (bu < 0 || bu >= geo.n_units) return -1;
     return (int64_t)geo.unit_base + (int64_t)bu * geo.block_size + (w - u * geo.block_size);
   };
+  auto uniform64 = [](int64_t x) -> int64_t {
+    return ((int64_t)__builtin_amdgcn_readfirstlane((int)(x >> 32)) << 32) |
+           (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)x);
+  };
 
-  // Both gather paths only produce positions; the loads themselves are common,
-  // unconditional and branch-free.  A key that is not part of the context
-  // (ragged end, skipped unit entry) reads position 0 -- always written -- and is
-  // masked to -inf before the softmax, so its (finite) K/V never contribute.
-  auto load_tile = [&](int tile) {
-    const int64_t r = tile_run_start(tile);  // uniform: keep it in scalar registers
-    const int64_t run0 = ((int64_t)__builtin_amdgcn_readfirstlane((int)(r >> 32)) << 32) |
-                         (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)r);
-    int64_t p0, p1, p2, p3;
+  // Byte offsets of this wave's 1 KB slices in the LDS tiles, and the per-lane
+  // byte offset of the granule each lane fetches within a contiguous run.
+  const uint32_t lds_k = (uint32_t)(uintptr_t)(INFLLM_LDS bf16_t*)sm.k[0] + NI * wave * 1024;
+  const uint32_t lds_v = (uint32_t)(uintptr_t)(INFLLM_LDS bf16_t*)sm.v[0] + NI * wave * 1024;
+  constexpr uint32_t kTileBytes = KB * D * 2;
+  uint32_t run_off[NI];
+#pragma unroll
+  for (int j = 0; j < NI; ++j) run_off[j] = (uint32_t)(lrow[j] * D + 8 * lgran[j]) * 2u;
+
+  // Issue the direct loads of tile `tile` (run start `run0`) into buffer `buf`.
+  // A key that is not part of the context (ragged end, skipped unit entry)
+  // reads position 0 -- always written -- and is masked to -inf before the
+  // softmax (the ragged end by the causal bound, a skipped entry by kvalid), so
+  // its K/V never contribute.
+  auto issue_tile = [&](int tile, int64_t run0, int buf) {
+    const uint32_t lk = lds_k + buf * kTileBytes, lv = lds_v + buf * kTileBytes;
     if (run0 >= 0) {
-      st.mask = 0xF;
-      p0 = run0 + 4 * kq;
-      p1 = p0 + 1;
-      p2 = p0 + 2;
-      p3 = p0 + 3;
+      const bf16_t* sk = kbase + run0 * D;
+      const bf16_t* sv = vbase + run0 * D;
+#pragma unroll
+      for (int j = 0; j < NI; ++j) {
+        lds_load_run(lk + j * 1024, sk, run_off[j]);
+        lds_load_run(lv + j * 1024, sv, run_off[j]);
+      }
     } else {
-      const int v = tile * KB + 4 * kq;
-      const int64_t q0 = (v + 0 < geo.n_virtual) ? virtual_pos(geo, idx_row, v + 0) : -1;
-      const int64_t q1 = (v + 1 < geo.n_virtual) ? virtual_pos(geo, idx_row, v + 1) : -1;
-      const int64_t q2 = (v + 2 < geo.n_virtual) ? virtual_pos(geo, idx_row, v + 2) : -1;
-      const int64_t q3 = (v + 3 < geo.n_virtual) ? virtual_pos(geo, idx_row, v + 3) : -1;
-      st.mask = (q0 >= 0 ? 1u : 0u) | (q1 >= 0 ? 2u : 0u) | (q2 >= 0 ? 4u : 0u) | (q3 >= 0 ? 8u : 0u);
-      p0 = q0 >= 0 ? q0 : 0;
-      p1 = q1 >= 0 ? q1 : 0;
-      p2 = q2 >= 0 ? q2 : 0;
-      p3 = q3 >= 0 ? q3 : 0;
-    }
-    st.k0 = *(const u32x4*)(kbase + p0 * D + 8 * kc);
-    st.k1 = *(const u32x4*)(kbase + p1 * D + 8 * kc);
-    st.k2 = *(const u32x4*)(kbase + p2 * D + 8 * kc);
-    st.k3 = *(const u32x4*)(kbase + p3 * D + 8 * kc);
-    st.v0 = *(const u32x4*)(vbase + p0 * D + 8 * kc);
-    st.v1 = *(const u32x4*)(vbase + p1 * D + 8 * kc);
-    st.v2 = *(const u32x4*)(vbase + p2 * D + 8 * kc);
-    st.v3 = *(const u32x4*)(vbase + p3 * D + 8 * kc);
-  };
-  // The buffer of tile t+1 is not read during iteration t (the barrier ending
-  // iteration t-1 retired its last readers), so K and V are written into it as
-  // soon as convenient, which keeps their staging registers short-lived.
-  auto store_k = [&](int buf) {
-    if (!stager) return;
-    bf16_t* kd = sm.k[buf];
-    *(u32x4*)(kd + k_lds<D>(4 * kq + 0, kc)) = st.k0;
-    *(u32x4*)(kd + k_lds<D>(4 * kq + 1, kc)) = st.k1;
-    *(u32x4*)(kd + k_lds<D>(4 * kq + 2, kc)) = st.k2;
-    *(u32x4*)(kd + k_lds<D>(4 * kq + 3, kc)) = st.k3;
-  };
-  auto store_v = [&](int buf) {
-    if (!stager) return;
-    const int col = vt_col(4 * kq);        // logical column of the 4-key run in a V^T row
-    const int g = col >> 3, half = (col >> 2) & 1;
-    bf16_t* vd = sm.vt[buf];
 #pragma unroll
-    for (int w = 0; w < 4; ++w) {  // dword w of the 16-byte chunk = dims 8c+2w, 8c+2w+1
-      const uint32_t a0 = dword(st.v0, w), a1 = dword(st.v1, w);
-      const uint32_t a2 = dword(st.v2, w), a3 = dword(st.v3, w);
-      uint2 lo, hi;  // lo: dim 2w for keys 0..3, hi: dim 2w+1
-      lo.x = (a0 & 0xFFFFu) | (a1 << 16);
-      lo.y = (a2 & 0xFFFFu) | (a3 << 16);
-      hi.x = (a0 >> 16) | (a1 & 0xFFFF0000u);
-      hi.y = (a2 >> 16) | (a3 & 0xFFFF0000u);
-      const int r = 8 * kc + 2 * w;
-      *(uint2*)(vd + vt_lds(r, g) + 4 * half) = lo;
-      *(uint2*)(vd + vt_lds(r + 1, g) + 4 * half) = hi;
-    }
-    if (kc == 0) {
-#pragma unroll
-      for (int i = 0; i < 4; ++i) sm.kvalid[buf][4 * kq + i] = (st.mask >> i) & 1u;
+      for (int j = 0; j < NI; ++j) {
+        const int v = tile * KB + lrow[j];
+        int64_t pos = v < geo.n_virtual ? virtual_pos(geo, idx_row, v) : -1;
+        if (lane % CH == 0) sm.kvalid[buf][lrow[j]] = pos >= 0;
+        pos = pos >= 0 ? pos : 0;
+        const int64_t e = pos * D + 8 * lgran[j];
+        lds_load_lane(lk + j * 1024, kbase + e);
+        lds_load_lane(lv + j * 1024, vbase + e);
+      }
     }
   };
+
+  // Loop-invariant per-lane LDS offsets (elements).
+  //  K fragment (S^T A operand) of k-step s: lane (n, gsel) reads row n (+32 for
+  //  the second key block), granule 2s + gsel; k-steps 4..7 repeat 0..3 one
+  //  64-element half-row further.
+  //  V^T fragment (O^T A operand) of output block db: a transposed read by lane
+  //  (h = lane/16, q = (lane%16)/4, m = lane%4) addresses key row
+  //  16*j + 4*(h/2) + 8*e + q and dims 32*db + 16*(h%2) + 4*m .. +4; each lane then
+  //  holds dim 32*db + lane%32 of keys 16*j + 4*gsel + 8*e + 0..3 -- the key order
+  //  of the P^T operand taken from the S^T accumulator.
+  int koff[4], voff[DBLK];
+#pragma unroll
+  for (int s = 0; s < 4; ++s) koff[s] = tile_off<D>(n, 2 * s + gsel);
+  {
+    const int h = lane >> 4, q = (lane & 15) >> 2, m = lane & 3;
+    const int vr = 4 * (h >> 1) + q;  // row within the 16-key step (e = 0)
+#pragma unroll
+    for (int db = 0; db < DBLK; ++db) {
+      const int d0 = 32 * db + 16 * (h & 1) + 4 * m;
+      voff[db] = vr * D + 8 * ((d0 >> 3) ^ (vr & 7)) + (d0 & 7);
+    }
+  }
 
   f32x16 oacc[DBLK];
 #pragma unroll
@@ -223,53 +229,26 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
   float l_run = 0.f;
   const float c2 = a.sm_scale * 1.4426950408889634f;
 
-  if (t_begin < t_end) {
-    load_tile(t_begin);
-    store_k(0);
-    store_v(0);
-  }
-  __syncthreads();
-  const bool has_invalid = sm.has_invalid != 0;
-
-  // Loop-invariant per-lane LDS offsets (elements) of the MFMA fragments under
-  // the swizzles: K k-steps 4..7 repeat k-steps 0..3 one 64-element half-row
-  // further; V^T offsets depend only on the parity of the 32-row block.
-  int koff[4], voff[2][4];
-#pragma unroll
-  for (int s = 0; s < 4; ++s) koff[s] = n * D + 8 * ((2 * s + gsel) ^ (n & 7));
-#pragma unroll
-  for (int par = 0; par < 2; ++par)
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-      voff[par][j] = n * KB + 8 * ((2 * j + gsel) ^ ((n & 7) ^ (((n >> 3) + 4 * par) & 7)));
-
-  for (int t = t_begin; t < t_end; ++t) {
-    const int buf = (t - t_begin) & 1;
-    // Unconditional prefetch (the last iteration re-fetches its own tile and
-    // never stores it): no register join at the back edge, so the loads stay
-    // in flight across the whole iteration.
-    load_tile(min(t + 1, t_end - 1));
-
+  // One key tile: S^T, masking (MASK only), online softmax, O^T update.
+  auto tile_step = [&](int t, int buf, auto mask_tag) {
+    constexpr bool MASK = decltype(mask_tag)::value;
     const bf16_t* Kb = sm.k[buf];
-    const bf16_t* Vb = sm.vt[buf];
+    const bf16_t* Vb = sm.v[buf];
     // S^T for keys [0,32) and [32,64) of the tile: two independent accumulator
-    // chains interleaved, K fragments read two k-steps ahead of their MFMA.
+    // chains interleaved, K fragments read one k-step ahead of their MFMA.
     f32x16 sacc[2];
     {
-      // lane (n, gsel) reads row 32*kb + n, granule 2*s + gsel (swizzled by n & 7)
-      const bf16_t* kr0 = Kb;
-      const bf16_t* kr1 = Kb + 32 * D;
-      auto kfrag = [&](const bf16_t* base, int s) {
-        return *(const bf16x8*)(base + koff[s & 3] + 64 * (s >> 2));
+      auto kfrag = [&](int kb, int s) {
+        return *(const bf16x8*)(Kb + 32 * kb * D + koff[s & 3] + 64 * (s >> 2));
       };
       bf16x8 a0[2], a1[2];
-      a0[0] = kfrag(kr0, 0);
-      a1[0] = kfrag(kr1, 0);
+      a0[0] = kfrag(0, 0);
+      a1[0] = kfrag(1, 0);
 #pragma unroll
       for (int s = 0; s < KSTEPS; ++s) {
         if (s + 1 < KSTEPS) {
-          a0[(s + 1) & 1] = kfrag(kr0, s + 1);
-          a1[(s + 1) & 1] = kfrag(kr1, s + 1);
+          a0[(s + 1) & 1] = kfrag(0, s + 1);
+          a1[(s + 1) & 1] = kfrag(1, s + 1);
         }
         if (s == 0) {
           const f32x16 zero = {};
@@ -281,30 +260,42 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
         }
       }
     }
-    // lane (n, gsel) reads V^T row 32*db + n, granule 2*j + gsel of P block j
-    auto vfrag = [&](int db, int j) { return *(const bf16x8*)(Vb + 32 * db * KB + voff[db & 1][j]); };
 
-    // Masks: current tokens (causal), the ragged end, skipped unit entries.
-    const int tile_v0 = t * KB;
-    const bool need_mask = (tile_v0 + KB > v_x0) || has_invalid;
-    float mx = -__builtin_inff();
-    if (need_mask) {
+    if constexpr (MASK) {
+      // Key kl of the tile is visible to query qi iff its virtual index is at most
+      // v_x0 + qi (causal within X; also excludes the ragged end) and, with skipped
+      // unit entries present, its kvalid flag is set.
+      const int lim = v_x0 + qi - t * KB - 4 * gsel;  // in units of the lane's key offset
+      uint32_t kv[4][2];
+      if (has_invalid) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int j4 = 0; j4 < 4; ++j4)
+            kv[j4][kb] = *(const uint32_t*)&sm.kvalid[buf][32 * kb + 8 * j4 + 4 * gsel];
+      }
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
         for (int j = 0; j < 16; ++j) {
-          const int kl = 32 * kb + 8 * (j >> 2) + 4 * gsel + (j & 3);
-          const int v = tile_v0 + kl;
-          const bool vis = sm.kvalid[buf][kl] && v < geo.n_virtual && (v < v_x0 || v - v_x0 <= qi);
+          const int c = 32 * kb + 8 * (j >> 2) + (j & 3);
+          bool vis = c <= lim;
+          if (has_invalid) vis = vis && ((kv[j >> 2][kb] >> (8 * (j & 3))) & 0xFFu) != 0;
           sacc[kb][j] = vis ? sacc[kb][j] : -__builtin_inff();
         }
       }
     }
+
+    float mx = -__builtin_inff();
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int j = 0; j < 16; ++j) mx = fmaxf(mx, sacc[kb][j]);
-    mx = fmaxf(mx, __shfl_xor(mx, 32)) * c2;  // row max of this tile, in the exp2 domain (c2 > 0)
+    {
+      // combine the two lane halves (same query row, other 16 keys of each block)
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+      mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * c2;  // exp2 domain (c2 > 0)
+    }
 
     // Rescale only when some row's max grew by more than 2^8 since the last
     // rescale; otherwise keep the stale max (p <= 256, exact after the final
@@ -334,14 +325,18 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
     }
     l_run += psum;
 
+    // O^T += V^T P^T over the four 16-key steps of P; DBLK independent
+    // accumulator chains, each V^T fragment two transposed 8-byte reads.
+    auto vfrag = [&](int db, int j) {
+      const INFLLM_LDS i16x4* p0 = (const INFLLM_LDS i16x4*)(Vb + voff[db] + 16 * j * D);
+      const INFLLM_LDS i16x4* p1 = (const INFLLM_LDS i16x4*)(Vb + voff[db] + (16 * j + 8) * D);
+      const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFLLM_LDS i16x4*)p0);
+      const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFLLM_LDS i16x4*)p1);
+      return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+    };
     bf16x8 va[DBLK];
 #pragma unroll
     for (int db = 0; db < DBLK; ++db) va[db] = vfrag(db, 0);
-    if (t + 1 < t_end) store_k(buf ^ 1);
-
-    // O^T += V^T P^T over the four 16-key blocks of P; DBLK independent
-    // accumulator chains per block, each fragment register refilled with the
-    // next block's fragment right after the MFMA that consumed it.
 #pragma unroll
     for (int j = 0; j < 4; ++j) {
 #pragma unroll
@@ -350,9 +345,35 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
         if (j + 1 < 4) va[db] = vfrag(db, j + 1);
       }
     }
+  };
 
-    if (t + 1 < t_end) store_v(buf ^ 1);
+  // Tiles wholly before X need no mask unless skipped unit entries exist.
+  const int t_plain = has_invalid ? t_begin : max(t_begin, min(t_end, v_x0 / KB));
+  // Each iteration: wait for this tile's loads (this wave's, then every wave's
+  // via the barrier, which also retires the last readers of the other buffer),
+  // start the next tile's loads into that buffer, compute, and look up the run
+  // start of the tile after next (its scalar load completes under the barrier).
+  int64_t run_next = -1;
+  if (t_begin < t_end) {
+    issue_tile(t_begin, uniform64(tile_run_start(t_begin)), 0);
+    if (t_begin + 1 < t_end) run_next = uniform64(tile_run_start(t_begin + 1));
+  }
+  int t = t_begin;
+  for (; t < t_plain; ++t) {
+    const int buf = (t - t_begin) & 1;
+    __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
+    if (t + 1 < t_end) issue_tile(t + 1, run_next, buf ^ 1);
+    tile_step(t, buf, std::false_type{});
+    if (t + 2 < t_end) run_next = uniform64(tile_run_start(t + 2));
+  }
+  for (; t < t_end; ++t) {
+    const int buf = (t - t_begin) & 1;
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (t + 1 < t_end) issue_tile(t + 1, run_next, buf ^ 1);
+    tile_step(t, buf, std::true_type{});
+    if (t + 2 < t_end) run_next = uniform64(tile_run_start(t + 2));
   }
 
   // Epilogue: combine the two lane halves' partial sums; write O and lse.
