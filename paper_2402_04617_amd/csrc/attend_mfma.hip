@@ -50,12 +50,19 @@ __device__ __forceinline__ void lds_load_lane(uint32_t lds, const void* p) {
 #pragma clang diagnostic pop
 
 // Both LDS tiles are key-major [64 keys][D], unpadded, with the 16-byte granules
-// of row r XOR-swizzled by r & 7 (granule g stored at g ^ (r & 7)): the MFMA K
-// reads (8 consecutive rows, one granule each) and the transposed V reads
-// (4 rows x 32 bytes per 16 lanes) then spread over the LDS banks, and a 1 KB
-// direct-load instruction still writes one contiguous LDS range.
+// of row r XOR-swizzled (granule g stored at g ^ swz(r)), and a 1 KB direct-load
+// instruction still writes one contiguous LDS range.  gfx950 LDS serves 256
+// bytes per clock (64 banks); for D = 128 (256-byte rows) the 4-bit swizzle
+// below makes both fragment reads conflict-free: the K reads (16 consecutive
+// rows, one granule each, per clock) and the transposed V reads (per 32 lanes:
+// 4 consecutive rows x 64 bytes).  For D = 64 the 3-bit swizzle r & 7.
 template <int D>
-__device__ __forceinline__ int tile_off(int r, int g) { return r * D + 8 * (g ^ (r & 7)); }
+__device__ __forceinline__ int swz(int r) {
+  if constexpr (D == 128) return ((r & 3) << 2) | ((r >> 2) & 3);
+  else return r & 7;
+}
+template <int D>
+__device__ __forceinline__ int tile_off(int r, int g) { return r * D + 8 * (g ^ swz<D>(r)); }
 
 template <int D>
 struct Smem {
@@ -130,12 +137,12 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
 
   // Direct loads: instruction j of wave w fills LDS granules [(NI*w + j)*64, +64)
   // of the tile, lane l writing granule slot l; that slot belongs to tile row
-  // r_j = (NI*w + j)*RPI + l / CH and holds its global granule (l % CH) ^ (r_j & 7).
+  // r_j = (NI*w + j)*RPI + l / CH and holds its global granule (l % CH) ^ swz(r_j).
   int lrow[NI], lgran[NI];
 #pragma unroll
   for (int j = 0; j < NI; ++j) {
     lrow[j] = (NI * wave + j) * RPI + lane / CH;
-    lgran[j] = (lane % CH) ^ (lrow[j] & 7);
+    lgran[j] = (lane % CH) ^ swz<D>(lrow[j]);
   }
 
   // A tile inside one segment (I, one selected unit, or the L+X run) maps to 64
@@ -198,25 +205,28 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
     }
   };
 
-  // Loop-invariant per-lane LDS offsets (elements).
+  // Loop-invariant per-lane LDS offsets (elements); the swizzle depends on the
+  // row only through r & 15, so +16 and +32 rows keep it.
   //  K fragment (S^T A operand) of k-step s: lane (n, gsel) reads row n (+32 for
-  //  the second key block), granule 2s + gsel; k-steps 4..7 repeat 0..3 one
-  //  64-element half-row further.
+  //  the second key block), granule 2s + gsel.
   //  V^T fragment (O^T A operand) of output block db: a transposed read by lane
   //  (h = lane/16, q = (lane%16)/4, m = lane%4) addresses key row
   //  16*j + 4*(h/2) + 8*e + q and dims 32*db + 16*(h%2) + 4*m .. +4; each lane then
   //  holds dim 32*db + lane%32 of keys 16*j + 4*gsel + 8*e + 0..3 -- the key order
   //  of the P^T operand taken from the S^T accumulator.
-  int koff[4], voff[DBLK];
+  int koff[KSTEPS], voff[DBLK][2];
 #pragma unroll
-  for (int s = 0; s < 4; ++s) koff[s] = tile_off<D>(n, 2 * s + gsel);
+  for (int s = 0; s < KSTEPS; ++s) koff[s] = tile_off<D>(n, 2 * s + gsel);
   {
     const int h = lane >> 4, q = (lane & 15) >> 2, m = lane & 3;
-    const int vr = 4 * (h >> 1) + q;  // row within the 16-key step (e = 0)
 #pragma unroll
-    for (int db = 0; db < DBLK; ++db) {
-      const int d0 = 32 * db + 16 * (h & 1) + 4 * m;
-      voff[db] = vr * D + 8 * ((d0 >> 3) ^ (vr & 7)) + (d0 & 7);
+    for (int e = 0; e < 2; ++e) {
+      const int vr = 4 * (h >> 1) + 8 * e + q;  // row within the 16-key step
+#pragma unroll
+      for (int db = 0; db < DBLK; ++db) {
+        const int d0 = 32 * db + 16 * (h & 1) + 4 * m;
+        voff[db][e] = tile_off<D>(vr, d0 >> 3) + (d0 & 7);
+      }
     }
   }
 
@@ -239,7 +249,7 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
     f32x16 sacc[2];
     {
       auto kfrag = [&](int kb, int s) {
-        return *(const bf16x8*)(Kb + 32 * kb * D + koff[s & 3] + 64 * (s >> 2));
+        return *(const bf16x8*)(Kb + 32 * kb * D + koff[s]);
       };
       bf16x8 a0[2], a1[2];
       a0[0] = kfrag(0, 0);
@@ -328,8 +338,8 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
     // O^T += V^T P^T over the four 16-key steps of P; DBLK independent
     // accumulator chains, each V^T fragment two transposed 8-byte reads.
     auto vfrag = [&](int db, int j) {
-      const INFLLM_LDS i16x4* p0 = (const INFLLM_LDS i16x4*)(Vb + voff[db] + 16 * j * D);
-      const INFLLM_LDS i16x4* p1 = (const INFLLM_LDS i16x4*)(Vb + voff[db] + (16 * j + 8) * D);
+      const INFLLM_LDS i16x4* p0 = (const INFLLM_LDS i16x4*)(Vb + voff[db][0] + 16 * j * D);
+      const INFLLM_LDS i16x4* p1 = (const INFLLM_LDS i16x4*)(Vb + voff[db][1] + 16 * j * D);
       const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFLLM_LDS i16x4*)p0);
       const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFLLM_LDS i16x4*)p1);
       return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
