@@ -49,6 +49,17 @@ __device__ __forceinline__ void lds_load_lane(uint32_t lds, const void* p) {
 }
 #pragma clang diagnostic pop
 
+// Values the compiler must treat as produced here (keeps derived addresses from
+// being hoisted out of the tile loop into long-lived registers).
+__device__ __forceinline__ uint32_t opaque_v(uint32_t x) {
+  asm volatile("" : "+v"(x));
+  return x;
+}
+__device__ __forceinline__ uint32_t opaque_s(uint32_t x) {
+  asm volatile("" : "+s"(x));
+  return x;
+}
+
 // Both LDS tiles are key-major [64 keys][D], unpadded, with the 16-byte granules
 // of row r XOR-swizzled (granule g stored at g ^ swz(r)), and a 1 KB direct-load
 // instruction still writes one contiguous LDS range.  gfx950 LDS serves 256
@@ -79,7 +90,7 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
   constexpr int RPI = 64 / CH;                // tile rows per 1 KB load instruction
   constexpr int NI = KB * D * 2 / (NWAVE * 1024);  // load instructions per wave per tile (K or V)
   static_assert(NI * NWAVE * RPI == KB, "tile rows covered exactly once");
-  __shared__ __attribute__((aligned(16))) Smem<D> sm;
+  __shared__ __attribute__((aligned(256))) Smem<D> sm;
 
   const StepGeom& geo = a.geom;
   const int G = a.n_q_heads / a.n_kv_heads;
@@ -138,12 +149,10 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
   // Direct loads: instruction j of wave w fills LDS granules [(NI*w + j)*64, +64)
   // of the tile, lane l writing granule slot l; that slot belongs to tile row
   // r_j = (NI*w + j)*RPI + l / CH and holds its global granule (l % CH) ^ swz(r_j).
-  int lrow[NI], lgran[NI];
-#pragma unroll
-  for (int j = 0; j < NI; ++j) {
-    lrow[j] = (NI * wave + j) * RPI + lane / CH;
-    lgran[j] = (lane % CH) ^ swz<D>(lrow[j]);
-  }
+  // Under the swizzle r_j = r_0 + RPI*j and granule_j = granule_0 ^ XJ*j.
+  constexpr int XJ = D == 128 ? 1 : 0;
+  const int lrow0 = NI * wave * RPI + lane / CH;
+  const int lgran0 = (lane % CH) ^ swz<D>(lrow0);
 
   // A tile inside one segment (I, one selected unit, or the L+X run) maps to 64
   // consecutive store positions: the common case, gathered with no per-key work.
@@ -169,38 +178,38 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
 
   // Byte offsets of this wave's 1 KB slices in the LDS tiles, and the per-lane
   // byte offset of the granule each lane fetches within a contiguous run.
-  const uint32_t lds_k = (uint32_t)(uintptr_t)(INFLLM_LDS bf16_t*)sm.k[0] + NI * wave * 1024;
-  const uint32_t lds_v = (uint32_t)(uintptr_t)(INFLLM_LDS bf16_t*)sm.v[0] + NI * wave * 1024;
+  const uint32_t lds_k0 = (uint32_t)(uintptr_t)(INFLLM_LDS bf16_t*)sm.k[0];
+  const uint32_t lds_v0 = (uint32_t)(uintptr_t)(INFLLM_LDS bf16_t*)sm.v[0];
+  const uint32_t lds_k = lds_k0 + NI * wave * 1024;
+  const uint32_t lds_v = lds_v0 + NI * wave * 1024;
   constexpr uint32_t kTileBytes = KB * D * 2;
-  uint32_t run_off[NI];
-#pragma unroll
-  for (int j = 0; j < NI; ++j) run_off[j] = (uint32_t)(lrow[j] * D + 8 * lgran[j]) * 2u;
+  // byte offset of instruction j's granule within a contiguous run:
+  // (run_off0 ^ 16*XJ*j) + 1024*j
+  const uint32_t run_off0 = (uint32_t)(lrow0 * D + 8 * lgran0) * 2u;
 
-  // Issue the direct loads of tile `tile` (run start `run0`) into buffer `buf`.
-  // A key that is not part of the context (ragged end, skipped unit entry)
+  // Direct loads of tile `tile` (run start `run0`) into buffer `buf` of K or of
+  // V.  A key that is not part of the context (ragged end, skipped unit entry)
   // reads position 0 -- always written -- and is masked to -inf before the
-  // softmax (the ragged end by the causal bound, a skipped entry by kvalid), so
-  // its K/V never contribute.
-  auto issue_tile = [&](int tile, int64_t run0, int buf) {
-    const uint32_t lk = lds_k + buf * kTileBytes, lv = lds_v + buf * kTileBytes;
+  // softmax (the ragged end by the causal bound, a skipped entry by kvalid, which
+  // the K load records), so its K/V never contribute.
+  auto issue = [&](int tile, int64_t run0, int buf, auto is_k) {
+    constexpr bool IS_K = decltype(is_k)::value;
+    const uint32_t ld = (IS_K ? lds_k : lds_v) + buf * kTileBytes;
+    const bf16_t* base = IS_K ? kbase : vbase;
     if (run0 >= 0) {
-      const bf16_t* sk = kbase + run0 * D;
-      const bf16_t* sv = vbase + run0 * D;
+      const bf16_t* src = base + run0 * D;
+      const uint32_t ro = opaque_v(run_off0);
 #pragma unroll
-      for (int j = 0; j < NI; ++j) {
-        lds_load_run(lk + j * 1024, sk, run_off[j]);
-        lds_load_run(lv + j * 1024, sv, run_off[j]);
-      }
+      for (int j = 0; j < NI; ++j) lds_load_run(ld + j * 1024, src + 512 * j, ro ^ (16u * XJ * j));
     } else {
 #pragma unroll
       for (int j = 0; j < NI; ++j) {
-        const int v = tile * KB + lrow[j];
+        const int r = lrow0 + RPI * j;
+        const int v = tile * KB + r;
         int64_t pos = v < geo.n_virtual ? virtual_pos(geo, idx_row, v) : -1;
-        if (lane % CH == 0) sm.kvalid[buf][lrow[j]] = pos >= 0;
+        if (IS_K && lane % CH == 0) sm.kvalid[buf][r] = pos >= 0;
         pos = pos >= 0 ? pos : 0;
-        const int64_t e = pos * D + 8 * lgran[j];
-        lds_load_lane(lk + j * 1024, kbase + e);
-        lds_load_lane(lv + j * 1024, vbase + e);
+        lds_load_lane(ld + j * 1024, base + pos * D + 8 * (lgran0 ^ (XJ * j)));
       }
     }
   };
@@ -214,21 +223,33 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
   //  16*j + 4*(h/2) + 8*e + q and dims 32*db + 16*(h%2) + 4*m .. +4; each lane then
   //  holds dim 32*db + lane%32 of keys 16*j + 4*gsel + 8*e + 0..3 -- the key order
   //  of the P^T operand taken from the S^T accumulator.
-  int koff[KSTEPS], voff[DBLK][2];
-#pragma unroll
-  for (int s = 0; s < KSTEPS; ++s) koff[s] = tile_off<D>(n, 2 * s + gsel);
+  // Under the swizzle these offsets are XOR-related (buffers start at multiples
+  // of 256 bytes, so the XOR commutes with adding the buffer address):
+  //   K, k-step s          : koff0 ^ 32*s                         (bytes)
+  //   V^T, block db, half e: (voff0 ^ 64*db ^ VX*e) + e*16*D      (bytes)
+  // so only two bases stay in registers and each tile derives its addresses.
+  constexpr uint32_t VX = D == 128 ? 32 : 0;
+  const uint32_t koff0 = 2u * tile_off<D>(n, gsel);
+  uint32_t voff0;
   {
     const int h = lane >> 4, q = (lane & 15) >> 2, m = lane & 3;
-#pragma unroll
-    for (int e = 0; e < 2; ++e) {
-      const int vr = 4 * (h >> 1) + 8 * e + q;  // row within the 16-key step
-#pragma unroll
-      for (int db = 0; db < DBLK; ++db) {
-        const int d0 = 32 * db + 16 * (h & 1) + 4 * m;
-        voff[db][e] = tile_off<D>(vr, d0 >> 3) + (d0 & 7);
-      }
-    }
+    const int vr = 4 * (h >> 1) + q, d0 = 16 * (h & 1) + 4 * m;
+    voff0 = 2u * (tile_off<D>(vr, d0 >> 3) + (d0 & 7));
   }
+  auto kfrag_at = [&](uint32_t kaddr, int kb, int s) {
+    return *(const INFLLM_LDS bf16x8*)(uintptr_t)((kaddr ^ (32u * s)) + kb * 64u * D);
+  };
+  auto vfrag_at = [&](uint32_t vaddr, int db, int j) {
+    const uint32_t a0 = (vaddr ^ (64u * db)) + j * 32u * D;
+    const uint32_t a1 = ((vaddr ^ (64u * db) ^ VX) + 16u * D) + j * 32u * D;
+    const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFLLM_LDS i16x4*)(uintptr_t)a0);
+    const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFLLM_LDS i16x4*)(uintptr_t)a1);
+    return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+  };
+  // per-tile fragment base addresses (the buffer address is made opaque so that
+  // the derived addresses are formed per tile instead of held in registers)
+  auto kaddr_of = [&](int kbuf) { return opaque_s(lds_k0 + kbuf * kTileBytes) + koff0; };
+  auto vaddr_of = [&](int vbuf) { return opaque_s(lds_v0 + vbuf * kTileBytes) + voff0; };
 
   f32x16 oacc[DBLK];
 #pragma unroll
@@ -239,78 +260,70 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
   float l_run = 0.f;
   const float c2 = a.sm_scale * 1.4426950408889634f;
 
-  // One key tile: S^T, masking (MASK only), online softmax, O^T update.
-  auto tile_step = [&](int t, int buf, auto mask_tag) {
-    constexpr bool MASK = decltype(mask_tag)::value;
-    const bf16_t* Kb = sm.k[buf];
-    const bf16_t* Vb = sm.v[buf];
-    // S^T for keys [0,32) and [32,64) of the tile: two independent accumulator
-    // chains interleaved, K fragments read one k-step ahead of their MFMA.
-    f32x16 sacc[2];
-    {
-      auto kfrag = [&](int kb, int s) {
-        return *(const bf16x8*)(Kb + 32 * kb * D + koff[s]);
-      };
-      bf16x8 a0[2], a1[2];
-      a0[0] = kfrag(0, 0);
-      a1[0] = kfrag(1, 0);
+  // ---- the pieces of one tile's work ----------------------------------------
+  // S^T = K Q^T for the tile in K buffer `kb`: two accumulator chains (keys
+  // [0,32) and [32,64)), K fragments read one k-step ahead.
+  auto qk = [&](int kbuf, f32x16 (&sacc)[2]) {
+    const uint32_t ka = kaddr_of(kbuf);
+    auto kfrag = [&](int kb, int s) { return kfrag_at(ka, kb, s); };
+    bf16x8 a0[2], a1[2];
+    a0[0] = kfrag(0, 0);
+    a1[0] = kfrag(1, 0);
 #pragma unroll
-      for (int s = 0; s < KSTEPS; ++s) {
-        if (s + 1 < KSTEPS) {
-          a0[(s + 1) & 1] = kfrag(0, s + 1);
-          a1[(s + 1) & 1] = kfrag(1, s + 1);
-        }
-        if (s == 0) {
-          const f32x16 zero = {};
-          sacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[0], qreg[0], zero, 0, 0, 0);
-          sacc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[0], qreg[0], zero, 0, 0, 0);
-        } else {
-          sacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[s & 1], qreg[s], sacc[0], 0, 0, 0);
-          sacc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[s & 1], qreg[s], sacc[1], 0, 0, 0);
-        }
+    for (int s = 0; s < KSTEPS; ++s) {
+      if (s + 1 < KSTEPS) {
+        a0[(s + 1) & 1] = kfrag(0, s + 1);
+        a1[(s + 1) & 1] = kfrag(1, s + 1);
+      }
+      if (s == 0) {
+        const f32x16 zero = {};
+        sacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[0], qreg[0], zero, 0, 0, 0);
+        sacc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[0], qreg[0], zero, 0, 0, 0);
+      } else {
+        sacc[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[s & 1], qreg[s], sacc[0], 0, 0, 0);
+        sacc[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[s & 1], qreg[s], sacc[1], 0, 0, 0);
       }
     }
-
-    if constexpr (MASK) {
-      // Key kl of the tile is visible to query qi iff its virtual index is at most
-      // v_x0 + qi (causal within X; also excludes the ragged end) and, with skipped
-      // unit entries present, its kvalid flag is set.
-      const int lim = v_x0 + qi - t * KB - 4 * gsel;  // in units of the lane's key offset
-      uint32_t kv[4][2];
-      if (has_invalid) {
+  };
+  // Mask of tile t: key kl is visible to query qi iff its virtual index is at
+  // most v_x0 + qi (causal within X; also excludes the ragged end) and, with
+  // skipped unit entries present, its kvalid flag (K buffer kbuf) is set.
+  auto apply_mask = [&](int t, int kbuf, f32x16 (&sacc)[2]) {
+    const int lim = v_x0 + qi - t * KB - 4 * gsel;
+    uint32_t kv[4][2];
+    if (has_invalid) {
 #pragma unroll
-        for (int kb = 0; kb < 2; ++kb)
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-          for (int j4 = 0; j4 < 4; ++j4)
-            kv[j4][kb] = *(const uint32_t*)&sm.kvalid[buf][32 * kb + 8 * j4 + 4 * gsel];
-      }
+        for (int j4 = 0; j4 < 4; ++j4)
+          kv[j4][kb] = *(const uint32_t*)&sm.kvalid[kbuf][32 * kb + 8 * j4 + 4 * gsel];
+    }
 #pragma unroll
-      for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
-        for (int j = 0; j < 16; ++j) {
-          const int c = 32 * kb + 8 * (j >> 2) + (j & 3);
-          bool vis = c <= lim;
-          if (has_invalid) vis = vis && ((kv[j >> 2][kb] >> (8 * (j & 3))) & 0xFFu) != 0;
-          sacc[kb][j] = vis ? sacc[kb][j] : -__builtin_inff();
-        }
+      for (int j = 0; j < 16; ++j) {
+        const int c = 32 * kb + 8 * (j >> 2) + (j & 3);
+        bool vis = c <= lim;
+        if (has_invalid) vis = vis && ((kv[j >> 2][kb] >> (8 * (j & 3))) & 0xFFu) != 0;
+        sacc[kb][j] = vis ? sacc[kb][j] : -__builtin_inff();
       }
     }
-
+  };
+  // Row max of the tile in the exp2 domain (both lane halves combined).
+  auto tile_max = [&](const f32x16 (&sacc)[2]) {
     float mx = -__builtin_inff();
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
       for (int j = 0; j < 16; ++j) mx = fmaxf(mx, sacc[kb][j]);
-    {
-      // combine the two lane halves (same query row, other 16 keys of each block)
-      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
-      mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * c2;  // exp2 domain (c2 > 0)
-    }
-
-    // Rescale only when some row's max grew by more than 2^8 since the last
-    // rescale; otherwise keep the stale max (p <= 256, exact after the final
-    // normalisation).  The decision is wave-uniform, so both lane halves of a
-    // row always use the same max.
+    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+    return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * c2;  // c2 > 0
+  };
+  // Running-max update.  Rescale only when some row's max grew by more than 2^8
+  // since the last rescale; otherwise keep the stale max (p <= 256, exact after
+  // the final normalisation).  The decision is wave-uniform, so both lane halves
+  // of a row always use the same max.
+  auto update_max = [&](float mx) {
     if (__ballot(mx > m_run + 8.f)) {
       const float m_new = fmaxf(m_run, mx);
       const float alpha = (m_new == -__builtin_inff()) ? 1.f : fast_exp2(m_run - m_new);
@@ -321,29 +334,27 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
         for (int j = 0; j < 16; ++j) oacc[db][j] *= alpha;
       m_run = m_new;
     }
+  };
+  // P = exp2(S*c2 - m) as the bf16 P^T operand, and its fp32 row sum.
+  auto softmax_p = [&](const f32x16 (&sacc)[2], bf16x8 (&pb)[2][2]) {
     const float neg_m = (m_run == -__builtin_inff()) ? 0.f : -m_run;
-    float psum = 0.f;
-    bf16x8 pb[2][2];
+    float psum[2] = {0.f, 0.f};
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
         const float p = fast_exp2(__builtin_fmaf(sacc[kb][j], c2, neg_m));
-        psum += p;
+        psum[j & 1] += p;
         pb[kb][j >> 3][j & 7] = (__bf16)p;
       }
     }
-    l_run += psum;
-
-    // O^T += V^T P^T over the four 16-key steps of P; DBLK independent
-    // accumulator chains, each V^T fragment two transposed 8-byte reads.
-    auto vfrag = [&](int db, int j) {
-      const INFLLM_LDS i16x4* p0 = (const INFLLM_LDS i16x4*)(Vb + voff[db][0] + 16 * j * D);
-      const INFLLM_LDS i16x4* p1 = (const INFLLM_LDS i16x4*)(Vb + voff[db][1] + 16 * j * D);
-      const i16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFLLM_LDS i16x4*)p0);
-      const i16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((INFLLM_LDS i16x4*)p1);
-      return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-    };
+    return psum[0] + psum[1];
+  };
+  // O^T += V^T P^T over the four 16-key steps (V buffer vbuf); DBLK independent
+  // accumulator chains, each V^T fragment two transposed 8-byte reads.
+  auto pv = [&](int vbuf, const bf16x8 (&pb)[2][2]) {
+    const uint32_t vaddr = vaddr_of(vbuf);
+    auto vfrag = [&](int db, int j) { return vfrag_at(vaddr, db, j); };
     bf16x8 va[DBLK];
 #pragma unroll
     for (int db = 0; db < DBLK; ++db) va[db] = vfrag(db, 0);
@@ -357,33 +368,163 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
     }
   };
 
+  // ---- software pipeline over the part's tiles ---------------------------------
+  // Tile x lives in K buffer and V buffer (x - t_begin) & 1.  Iteration t runs
+  // PV(t) and QK(t+1): the matrix cores work on QK(t+1) while the vector ALUs
+  // form P(t), and on PV(t) while they take the max of tile t+1.  Loads are
+  // issued one iteration ahead, K two tiles ahead and V one tile ahead, so each
+  // buffer is refilled only after the barrier that retires its last readers:
+  //   top of iteration t: wait for K(t+1), V(t) (this wave's loads, then every
+  //   wave's via the barrier); issue K(t+2) into the K buffer of tile t (QK(t)
+  //   ran in iteration t-1) and V(t+1) into the V buffer of tile t-1.
+  // Run starts are looked up at the end of an iteration, so their scalar loads
+  // complete under the barrier.
   // Tiles wholly before X need no mask unless skipped unit entries exist.
   const int t_plain = has_invalid ? t_begin : max(t_begin, min(t_end, v_x0 / KB));
-  // Each iteration: wait for this tile's loads (this wave's, then every wave's
-  // via the barrier, which also retires the last readers of the other buffer),
-  // start the next tile's loads into that buffer, compute, and look up the run
-  // start of the tile after next (its scalar load completes under the barrier).
-  int64_t run_next = -1;
+  int64_t run_k = -1, run_v = -1;  // run starts of the next K and V loads
+  f32x16 sA[2], sB[2];
+  auto iteration = [&](int t, f32x16 (&cur)[2], f32x16 (&nxt)[2], auto mask_next) {
+    const int bc = (t - t_begin) & 1, bn = bc ^ 1;
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (t + 2 < t_end) issue(t + 2, run_k, bc, std::true_type{});
+    issue(t + 1, run_v, bn, std::false_type{});
+
+    // Phase 1: QK(t+1) on the matrix cores, P(t) on the vector ALUs.  Chunk s
+    // issues the K fragment reads of k-step s+1, the two MFMAs of k-step s and
+    // four elements of P(t); scheduling fences keep that interleave.
+    const float neg_m = (m_run == -__builtin_inff()) ? 0.f : -m_run;
+    bf16x8 pb[2][2];
+    float psum[2] = {0.f, 0.f};  // two partial row sums (shorter dependency chains)
+    {
+      const uint32_t ka = kaddr_of(bn);
+      auto kfrag = [&](int kb, int s) { return kfrag_at(ka, kb, s); };
+      bf16x8 a0[2], a1[2];
+      a0[0] = kfrag(0, 0);
+      a1[0] = kfrag(1, 0);
+      constexpr int EPC = 32 / KSTEPS;  // P elements per chunk
+#pragma unroll
+      for (int s = 0; s < KSTEPS; ++s) {
+        if (s + 1 < KSTEPS) {
+          a0[(s + 1) & 1] = kfrag(0, s + 1);
+          a1[(s + 1) & 1] = kfrag(1, s + 1);
+        }
+        if (s == 0) {
+          const f32x16 zero = {};
+          nxt[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[0], qreg[0], zero, 0, 0, 0);
+          nxt[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[0], qreg[0], zero, 0, 0, 0);
+        } else {
+          nxt[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[s & 1], qreg[s], nxt[0], 0, 0, 0);
+          nxt[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[s & 1], qreg[s], nxt[1], 0, 0, 0);
+        }
+#pragma unroll
+        for (int i = 0; i < EPC; ++i) {
+          const int e = EPC * s + i, kb = e >> 4, j = e & 15;
+          const float p = fast_exp2(__builtin_fmaf(cur[kb][j], c2, neg_m));
+          psum[i & 1] += p;
+          pb[kb][j >> 3][j & 7] = (__bf16)p;
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+
+    // Phase 2: PV(t) on the matrix cores; mask and row max of tile t+1 on the
+    // vector ALUs, one 16-key group (of the 32 accumulator elements) per step.
+    float mx = -__builtin_inff();
+    {
+      constexpr bool MASK = decltype(mask_next)::value;
+      const uint32_t vaddr = vaddr_of(bc);
+      auto vfrag = [&](int db, int j) { return vfrag_at(vaddr, db, j); };
+      const int lim = v_x0 + qi - (t + 1) * KB - 4 * gsel;  // mask bound of tile t+1
+      uint32_t kv[4][2];
+      if (MASK && has_invalid) {
+#pragma unroll
+        for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+          for (int j4 = 0; j4 < 4; ++j4)
+            kv[j4][kb] = *(const uint32_t*)&sm.kvalid[bn][32 * kb + 8 * j4 + 4 * gsel];
+      }
+      bf16x8 va[DBLK];
+#pragma unroll
+      for (int db = 0; db < DBLK; ++db) va[db] = vfrag(db, 0);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+#pragma unroll
+        for (int db = 0; db < DBLK; ++db) {
+          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[db], pb[j >> 1][j & 1], oacc[db], 0, 0, 0);
+          if (j + 1 < 4) va[db] = vfrag(db, j + 1);
+        }
+        // 8 of the 32 scores of tile t+1: elements [8j, 8j+8)
+#pragma unroll
+        for (int i = 0; i < 8; ++i) {
+          const int e = 8 * j + i, kb = e >> 4, jj = e & 15;
+          if constexpr (MASK) {
+            const int c = 32 * kb + 8 * (jj >> 2) + (jj & 3);
+            bool vis = c <= lim;
+            if (has_invalid) vis = vis && ((kv[jj >> 2][kb] >> (8 * (jj & 3))) & 0xFFu) != 0;
+            nxt[kb][jj] = vis ? nxt[kb][jj] : -__builtin_inff();
+          }
+          mx = fmaxf(mx, nxt[kb][jj]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    {
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+      mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * c2;  // c2 > 0
+    }
+    l_run += psum[0] + psum[1];
+    update_max(mx);
+    run_v = run_k;
+    run_k = t + 3 < t_end ? uniform64(tile_run_start(t + 3)) : -1;
+  };
+  auto copy_state = [](f32x16 (&dst)[2], const f32x16 (&src)[2]) {
+    dst[0] = src[0];
+    dst[1] = src[1];
+  };
+
   if (t_begin < t_end) {
-    issue_tile(t_begin, uniform64(tile_run_start(t_begin)), 0);
-    if (t_begin + 1 < t_end) run_next = uniform64(tile_run_start(t_begin + 1));
-  }
-  int t = t_begin;
-  for (; t < t_plain; ++t) {
-    const int buf = (t - t_begin) & 1;
+    const int64_t r0 = uniform64(tile_run_start(t_begin));
+    issue(t_begin, r0, 0, std::true_type{});
+    issue(t_begin, r0, 0, std::false_type{});
+    if (t_begin + 1 < t_end) {
+      run_v = uniform64(tile_run_start(t_begin + 1));
+      issue(t_begin + 1, run_v, 1, std::true_type{});
+    }
+    if (t_begin + 2 < t_end) run_k = uniform64(tile_run_start(t_begin + 2));
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (t + 1 < t_end) issue_tile(t + 1, run_next, buf ^ 1);
-    tile_step(t, buf, std::false_type{});
-    if (t + 2 < t_end) run_next = uniform64(tile_run_start(t + 2));
-  }
-  for (; t < t_end; ++t) {
-    const int buf = (t - t_begin) & 1;
+    qk(0, sA);
+    if (t_begin >= t_plain) apply_mask(t_begin, 0, sA);
+    update_max(tile_max(sA));
+
+    int t = t_begin;
+    // next tile unmasked
+    for (; t + 2 < t_plain; t += 2) {
+      iteration(t, sA, sB, std::false_type{});
+      iteration(t + 1, sB, sA, std::false_type{});
+    }
+    if (t + 1 < t_plain) {
+      iteration(t, sA, sB, std::false_type{});
+      copy_state(sA, sB);
+      ++t;
+    }
+    // next tile masked
+    for (; t + 2 < t_end; t += 2) {
+      iteration(t, sA, sB, std::true_type{});
+      iteration(t + 1, sB, sA, std::true_type{});
+    }
+    if (t + 1 < t_end) {
+      iteration(t, sA, sB, std::true_type{});
+      copy_state(sA, sB);
+      ++t;
+    }
+    // drain: P and PV of the last tile
     __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
-    if (t + 1 < t_end) issue_tile(t + 1, run_next, buf ^ 1);
-    tile_step(t, buf, std::true_type{});
-    if (t + 2 < t_end) run_next = uniform64(tile_run_start(t + 2));
+    bf16x8 pb[2][2];
+    l_run += softmax_p(sA, pb);
+    pv((t - t_begin) & 1, pb);
   }
 
   // Epilogue: combine the two lane halves' partial sums; write O and lse.
