@@ -78,6 +78,9 @@ typedef struct {
  *              sum_{p <= t} sum_{h in group} q^h_p, the running sum of the group's
  *              queries.  Written by infllm_append, read by infllm_build_units.
  * Unit b of E covers positions [l_I + b*l_bs, l_I + (b+1)*l_bs).
+ * For bf16 the attention entry points need one [capacity][D] slice of k or v to
+ * span at most 4 GiB (capacity * D * 2 bytes; 16M tokens at D = 128), else
+ * INFLLM_E_UNSUPPORTED.
  */
 typedef struct {
   int32_t batch;

@@ -133,6 +133,8 @@ infllm_status prepare_attend(const infllm_params* p, const infllm_memory* m, con
   const int64_t n_virtual = part.n_init + (int64_t)n_sel * p->block_size + (past_len - part.local_begin) + n_q;
   if (n_virtual > INT32_MAX) return INFLLM_E_UNSUPPORTED;
   const bool bf16 = p->dtype == INFLLM_BF16;
+  // the bf16 kernels address one (sequence, kv head) slice of the store with 32-bit byte offsets
+  if (bf16 && (uint64_t)m->capacity * (uint64_t)p->head_dim * 2u > 0xFFFFFFFFull) return INFLLM_E_UNSUPPORTED;
   const int64_t rows = (int64_t)m->batch * p->n_q_heads * n_q;
   const size_t per_part = rows > 0 ? (size_t)rows * (size_t)(p->head_dim + 1) * 4u : 1;
   const int max_parts = (workspace == nullptr) ? 0 : (int)(workspace_bytes / per_part > 4096 ? 4096 : workspace_bytes / per_part);

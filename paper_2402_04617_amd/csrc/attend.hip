@@ -288,12 +288,13 @@ int attend_choose_parts(bool bf16, int batch, int n_q_heads, int n_kv_heads, int
     const int p = attend_decode_parts(n_virtual);
     return p <= max(1, max_parts) ? p : -1;  // decode parts are fixed by the key count
   }
-  const int rows_per_wg = bf16 ? 128 : 16;
+  const int rows_per_wg = bf16 ? kMfmaRowsPerWg : 16;
   const int key_tile = bf16 ? 64 : 32;
   const int cap = bf16 ? 8 : 16;
+  const int target = bf16 ? kMfmaTargetWgs : 512;
   const int row_tiles = batch * n_kv_heads * ((G * n_q + rows_per_wg - 1) / rows_per_wg);
   const int n_tiles = (n_virtual + key_tile - 1) / key_tile;
-  int p = (512 + row_tiles - 1) / row_tiles;
+  int p = (target + row_tiles - 1) / row_tiles;
   p = min(p, cap);
   p = min(p, max(1, n_tiles / 2));
   p = min(p, max(1, max_parts));

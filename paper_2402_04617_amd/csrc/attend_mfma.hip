@@ -4,12 +4,13 @@
 // Work decomposition
 //   rows   : per (sequence, kv head) the G*n_q query rows (row r -> query i = r/G,
 //            head g*G + r%G), so the G heads sharing a K/V tile are packed together;
-//            128 rows per workgroup, 32 per wave.
+//            256 rows per workgroup (one per compute unit), 32 per wave, so each
+//            K/V tile crosses into LDS once for all 8 waves.
 //   keys   : the virtual key axis (see StepGeom) in tiles of 64 keys, gathered
 //            straight from the token-ordered store (a selected unit is contiguous)
-//            into LDS by direct global->LDS loads (no staging registers), double
-//            buffered; optionally split into parts whose partial softmaxes are
-//            merged afterwards by log-sum-exp.
+//            into LDS by direct global->LDS loads (no staging registers) through
+//            three buffers; optionally split into parts whose partial softmaxes
+//            are merged afterwards by log-sum-exp.
 // Per wave and key tile:
 //   S^T = K Q^T  : A = K tile rows from LDS, B = the wave's Q rows held in VGPRs.
 //                  The 32x32 accumulator gives each lane one query row and 16 keys.
@@ -24,8 +25,9 @@ namespace infllm {
 namespace {
 
 constexpr int KB = 64;      // keys per tile
-constexpr int NWAVE = 4;
+constexpr int NWAVE = 8;
 constexpr int ROWS_WG = 32 * NWAVE;
+static_assert(ROWS_WG == kMfmaRowsPerWg, "row tiling shared with the part chooser");
 
 typedef short i16x4 __attribute__((ext_vector_type(4)));
 #define INFLLM_LDS __attribute__((address_space(3)))
@@ -75,21 +77,40 @@ __device__ __forceinline__ int swz(int r) {
 template <int D>
 __device__ __forceinline__ int tile_off(int r, int g) { return r * D + 8 * (g ^ swz<D>(r)); }
 
-template <int D>
-struct Smem {
-  bf16_t k[2][KB * D];
-  bf16_t v[2][KB * D];
-  uint8_t kvalid[2][KB];
-};
+constexpr int NBUF = 3;         // K and V tile buffers
+constexpr int kRunTable = 1024;  // run starts kept in LDS for the part's tiles
 
 template <int D>
-__global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
+struct Smem {
+  bf16_t k[NBUF][KB * D];
+  bf16_t v[NBUF][KB * D];
+  int64_t runs[kRunTable];  // run start of tile t_begin + i (see tile_run_start)
+  uint8_t kvalid[NBUF][KB];
+};
+
+// Publish LDS tiles to the workgroup: wait until at most N of this wave's
+// direct loads are still in flight (older loads -- the tiles about to be read
+// -- have landed in LDS) and its own LDS traffic is done, then barrier.  Written
+// out so that no wait for the younger loads is implied.
+template <int N>
+__device__ __forceinline__ void publish_barrier() {
+  asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N));
+  // LDS-only fences: order this wave's LDS accesses around the barrier without
+  // a wait for its outstanding global loads.
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "workgroup", "local");
+  __builtin_amdgcn_s_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
+}
+
+template <int D>
+__global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a) {
   constexpr int CH = D / 8;                   // 16-byte granules per row
   constexpr int KSTEPS = D / 16;              // MFMA k-steps over the head dim
   constexpr int DBLK = D / 32;                // 32-wide output blocks
   constexpr int RPI = 64 / CH;                // tile rows per 1 KB load instruction
   constexpr int NI = KB * D * 2 / (NWAVE * 1024);  // load instructions per wave per tile (K or V)
   static_assert(NI * NWAVE * RPI == KB, "tile rows covered exactly once");
+  static_assert(2 * NI <= KSTEPS, "one load per chunk of the MFMA phase");
   __shared__ __attribute__((aligned(256))) Smem<D> sm;
 
   const StepGeom& geo = a.geom;
@@ -210,6 +231,29 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
         if (IS_K && lane % CH == 0) sm.kvalid[buf][r] = pos >= 0;
         pos = pos >= 0 ? pos : 0;
         lds_load_lane(ld + j * 1024, base + pos * D + 8 * (lgran0 ^ (XJ * j)));
+      }
+    }
+  };
+  // The same loads split in two: per-lane byte offsets from the store base
+  // (formed at the top of an iteration; per-key gather on the uncommon path) and
+  // the loads themselves, issued one per chunk of the MFMA phase so that the
+  // waves of the workgroup do not queue a burst of them after the barrier.  The
+  // host guarantees that one (sequence, kv head) slice of the store spans less
+  // than 4 GiB, so the offsets fit 32 bits.
+  auto load_offsets = [&](int tile, int64_t run0, int buf, bool is_k, uint32_t (&off)[NI]) {
+    if (run0 >= 0) {
+      const uint32_t ro = opaque_v(run_off0) + (uint32_t)run0 * (2u * D);
+#pragma unroll
+      for (int j = 0; j < NI; ++j) off[j] = (ro ^ (16u * XJ * j)) + 1024u * j;
+    } else {
+#pragma unroll
+      for (int j = 0; j < NI; ++j) {
+        const int r = lrow0 + RPI * j;
+        const int v = tile * KB + r;
+        int64_t pos = v < geo.n_virtual ? virtual_pos(geo, idx_row, v) : -1;
+        if (is_k && lane % CH == 0) sm.kvalid[buf][r] = pos >= 0;
+        pos = pos >= 0 ? pos : 0;
+        off[j] = (uint32_t)pos * (2u * D) + 16u * (lgran0 ^ (XJ * j));
       }
     }
   };
@@ -369,26 +413,48 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
   };
 
   // ---- software pipeline over the part's tiles ---------------------------------
-  // Tile x lives in K buffer and V buffer (x - t_begin) & 1.  Iteration t runs
+  // Tile x lives in K buffer and V buffer (x - t_begin) % 3.  Iteration t runs
   // PV(t) and QK(t+1): the matrix cores work on QK(t+1) while the vector ALUs
   // form P(t), and on PV(t) while they take the max of tile t+1.  Loads are
-  // issued one iteration ahead, K two tiles ahead and V one tile ahead, so each
-  // buffer is refilled only after the barrier that retires its last readers:
-  //   top of iteration t: wait for K(t+1), V(t) (this wave's loads, then every
-  //   wave's via the barrier); issue K(t+2) into the K buffer of tile t (QK(t)
-  //   ran in iteration t-1) and V(t+1) into the V buffer of tile t-1.
-  // Run starts are looked up at the end of an iteration, so their scalar loads
-  // complete under the barrier.
+  // issued two iterations ahead, K three tiles ahead and V two tiles ahead, so
+  // each buffer is refilled only after the barrier that retires its last readers:
+  //   top of iteration t: wait for K(t+1), V(t) (issued two iterations ago; the
+  //   2*NI loads of the previous iteration may stay in flight), barrier; issue
+  //   K(t+3) into the K buffer of tile t (QK(t) ran in iteration t-1) and V(t+2)
+  //   into the V buffer of tile t-1.
+  // Every iteration issues exactly 2*NI loads per wave, which keeps the wait
+  // count constant: a tile past the part's end is simply loaded too (a tile past
+  // the key axis reads position 0), into a buffer nobody reads.  Run starts are
+  // looked up at the end of an iteration, so their scalar loads complete under
+  // the barrier.
   // Tiles wholly before X need no mask unless skipped unit entries exist.
   const int t_plain = has_invalid ? t_begin : max(t_begin, min(t_end, v_x0 / KB));
-  int64_t run_k = -1, run_v = -1;  // run starts of the next K and V loads
+  int64_t run_k = -1, run_v = -1;  // run starts of the next K and V loads: tiles t+3, t+2
+  // Run starts of the part's tiles, computed once by all lanes into LDS; the
+  // per-iteration lookup is then an LDS read (a global read here would wait
+  // behind the tile loads in flight).  Tiles past the table compute directly.
+  const int n_table = min(kRunTable, t_end + 4 - t_begin);
+  for (int i = tid; i < n_table; i += 64 * NWAVE) sm.runs[i] = tile_run_start(t_begin + i);
+  auto run_of = [&](int tile) -> int64_t {
+    const int i = tile - t_begin;
+    return uniform64(i < n_table ? sm.runs[i] : tile_run_start(tile));
+  };
+  // early half of a lookup: the LDS read (or -2 when the tile is past the table)
+  auto run_read = [&](int tile) -> int64_t {
+    const int i = tile - t_begin;
+    return i < n_table ? sm.runs[i] : -2;
+  };
+  auto run_finish = [&](int tile, int64_t r) -> int64_t { return uniform64(r != -2 ? r : tile_run_start(tile)); };
   f32x16 sA[2], sB[2];
   auto iteration = [&](int t, f32x16 (&cur)[2], f32x16 (&nxt)[2], auto mask_next) {
-    const int bc = (t - t_begin) & 1, bn = bc ^ 1;
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
-    if (t + 2 < t_end) issue(t + 2, run_k, bc, std::true_type{});
-    issue(t + 1, run_v, bn, std::false_type{});
+    const int bc = (t - t_begin) % NBUF;
+    const int bn = bc == NBUF - 1 ? 0 : bc + 1, bp = bc == 0 ? NBUF - 1 : bc - 1;
+    publish_barrier<2 * NI>();
+    uint32_t off_k[NI], off_v[NI];
+    load_offsets(t + 3, run_k, bc, true, off_k);
+    load_offsets(t + 2, run_v, bp, false, off_v);
+    const uint32_t ld_k = lds_k + bc * kTileBytes, ld_v = lds_v + bp * kTileBytes;
+    const int64_t run_next = run_read(t + 4);  // consumed after phase 2
 
     // Phase 1: QK(t+1) on the matrix cores, P(t) on the vector ALUs.  Chunk s
     // issues the K fragment reads of k-step s+1, the two MFMAs of k-step s and
@@ -417,6 +483,9 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
           nxt[0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a0[s & 1], qreg[s], nxt[0], 0, 0, 0);
           nxt[1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a1[s & 1], qreg[s], nxt[1], 0, 0, 0);
         }
+        // the s-th of this wave's 2*NI loads of K(t+3) and V(t+2)
+        if (s < NI) lds_load_run(ld_k + s * 1024, kbase, off_k[s]);
+        else if (s < 2 * NI) lds_load_run(ld_v + (s - NI) * 1024, vbase, off_v[s - NI]);
 #pragma unroll
         for (int i = 0; i < EPC; ++i) {
           const int e = EPC * s + i, kb = e >> 4, j = e & 15;
@@ -476,7 +545,7 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
     l_run += psum[0] + psum[1];
     update_max(mx);
     run_v = run_k;
-    run_k = t + 3 < t_end ? uniform64(tile_run_start(t + 3)) : -1;
+    run_k = run_finish(t + 4, run_next);
   };
   auto copy_state = [](f32x16 (&dst)[2], const f32x16 (&src)[2]) {
     dst[0] = src[0];
@@ -484,16 +553,19 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
   };
 
   if (t_begin < t_end) {
+    // K(t0), V(t0), K(t0+1) | V(t0+1), K(t0+2): the last two groups play the
+    // loads of "the previous iteration" for the first iteration's wait.
     const int64_t r0 = uniform64(tile_run_start(t_begin));
+    const int64_t r1 = uniform64(tile_run_start(t_begin + 1));
+    const int64_t r2 = uniform64(tile_run_start(t_begin + 2));
     issue(t_begin, r0, 0, std::true_type{});
     issue(t_begin, r0, 0, std::false_type{});
-    if (t_begin + 1 < t_end) {
-      run_v = uniform64(tile_run_start(t_begin + 1));
-      issue(t_begin + 1, run_v, 1, std::true_type{});
-    }
-    if (t_begin + 2 < t_end) run_k = uniform64(tile_run_start(t_begin + 2));
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
+    issue(t_begin + 1, r1, 1, std::true_type{});
+    issue(t_begin + 1, r1, 1, std::false_type{});
+    issue(t_begin + 2, r2, 2, std::true_type{});
+    run_v = r2;
+    run_k = uniform64(tile_run_start(t_begin + 3));
+    publish_barrier<4 * NI>();  // K(t0) has landed
     qk(0, sA);
     if (t_begin >= t_plain) apply_mask(t_begin, 0, sA);
     update_max(tile_max(sA));
@@ -519,12 +591,11 @@ __global__ void __launch_bounds__(256, 2) attend_mfma_kernel(AttendArgs a) {
       copy_state(sA, sB);
       ++t;
     }
-    // drain: P and PV of the last tile
-    __builtin_amdgcn_s_waitcnt(0);
-    __syncthreads();
+    // drain: P and PV of the last tile (then no load is left in flight)
+    publish_barrier<0>();
     bf16x8 pb[2][2];
     l_run += softmax_p(sA, pb);
-    pv((t - t_begin) & 1, pb);
+    pv((t - t_begin) % NBUF, pb);
   }
 
   // Epilogue: combine the two lane halves' partial sums; write O and lse.
@@ -573,9 +644,9 @@ hipError_t launch_attend_mfma(const AttendArgs& a, hipStream_t s) {
   const int n_row_tiles = (R + ROWS_WG - 1) / ROWS_WG;
   const int blocks = n_row_tiles * a.parts * a.batch * a.n_kv_heads;
   if (a.head_dim == 128)
-    hipLaunchKernelGGL(attend_mfma_kernel<128>, dim3(blocks), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(attend_mfma_kernel<128>, dim3(blocks), dim3(64 * NWAVE), 0, s, a);
   else
-    hipLaunchKernelGGL(attend_mfma_kernel<64>, dim3(blocks), dim3(256), 0, s, a);
+    hipLaunchKernelGGL(attend_mfma_kernel<64>, dim3(blocks), dim3(64 * NWAVE), 0, s, a);
   return hipGetLastError();
 }
 

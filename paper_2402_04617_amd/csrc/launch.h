@@ -58,6 +58,11 @@ hipError_t launch_score_given_qbar(const ScoreArgs& a, int parts, hipStream_t s)
 hipError_t launch_select_topk(int rows, const float* scores, int n_units, int k, int32_t* idx,
                               hipStream_t s);
 
+// Query rows per workgroup of the bf16 matrix-core attention kernel, and the
+// workgroup count the part chooser aims for (one per compute unit).
+constexpr int kMfmaRowsPerWg = 256;
+constexpr int kMfmaTargetWgs = 256;
+
 struct AttendArgs {
   int batch, n_q_heads, n_kv_heads, head_dim;
   int64_t capacity, q_head_stride, out_head_stride;
