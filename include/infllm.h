@@ -76,7 +76,13 @@ typedef struct {
  *              16-byte cell, unit-contiguous (the layout unit scoring streams).
  *   qprefix    [batch][Hkv][ring][D] float64 ring: slot (t mod ring) holds
  *              sum_{p <= t} sum_{h in group} q^h_p, the running sum of the group's
- *              queries.  Written by infllm_append, read by infllm_build_units.
+ *              queries.  Written and read by infllm_append.
+ *   rpart      [batch][Hkv][D/16][ring] float64 ring: slot (t mod ring) of row s
+ *              holds sum over dims d in [16s, 16s+16) of k_t[d] * W_t[d], where
+ *              W_t = qprefix(t + l_L) - qprefix(t) is the window query sum of token
+ *              t; summed over s it is l_L*G times the representative score r_t of
+ *              Section 3.2.  Written by infllm_append once position t + l_L is
+ *              appended, read by infllm_build_units.
  * Unit b of E covers positions [l_I + b*l_bs, l_I + (b+1)*l_bs).
  * For bf16 the attention entry points need one [capacity][D] slice of k or v to
  * span at most 4 GiB (capacity * D * 2 bytes; 16M tokens at D = 128), else
@@ -91,6 +97,7 @@ typedef struct {
   int32_t* repr_idx;
   float* unit_ksum;
   double* qprefix;
+  double* rpart;
   int32_t ring;
 } infllm_memory;
 
@@ -111,10 +118,14 @@ size_t infllm_workspace_bytes(const infllm_params* p, int32_t batch, int32_t n_q
  *     q + (b*Hq + h)*q_head_stride elements (q_head_stride >= n_q*D).
  *  k, v: chunk keys/values laid out the same way with kv_head_stride; both NULL
  *     when the caller has already written them into the store.
- * Copies k, v into the store and extends the qprefix ring (the window query sums
- * that the representative score r_m of Section 3.2 needs once tokens are
- * evicted).  Positions must be appended in order: slot (past_len - 1) must hold
- * the running sum through past_len - 1.  E_RANGE if past_len + n_q > capacity. */
+ * Copies k, v into the store, extends the qprefix ring and, for every appended
+ * position p with t = p - l_L >= l_I, writes the partial representative scores of
+ * token t into rpart (what the representative score r_t of Section 3.2 needs
+ * once t is evicted).  Positions must be appended in order: slot (past_len - 1)
+ * must hold the running sum through past_len - 1.  E_RANGE if past_len + n_q >
+ * capacity, or if the ring would lose the running sum of a token t before its
+ * scores are formed (it needs ring >= l_L + n_q in steady streaming); E_NULL if
+ * such a token lies inside the chunk (l_L < n_q) and k is NULL. */
 infllm_status infllm_append(const infllm_params* p, const infllm_memory* m, const void* q,
                             int64_t q_head_stride, const void* k, const void* v,
                             int64_t kv_head_stride, int32_t n_q, int64_t past_len, void* stream);
@@ -123,9 +134,10 @@ infllm_status infllm_append(const infllm_params* p, const infllm_memory* m, cons
  * For units [first_unit, first_unit + n_new) of every (sequence, kv head):
  * r_m = 1/(l_L*G) * sum_{h in group} sum_{j=1..l_L} q^h_{m+j} . k_m for each of its
  * l_bs tokens (G = Hq/Hkv), then R(B) = the r_k tokens of largest r_m (ties: lower
- * position).  Writes repr_idx and unit_ksum.  `past_len` is the number of
- * positions appended so far; every window m+1..m+l_L must lie below it and the
- * ring must still hold slots first_pos .. last_pos + l_L (E_RANGE otherwise).
+ * position).  r_m is the sum of the rpart rows that infllm_append wrote for m.
+ * Writes repr_idx and unit_ksum.  `past_len` is the number of positions appended
+ * so far; every window m+1..m+l_L must lie below it and the ring must still hold
+ * the unit's slots, first_pos >= past_len - ring (E_RANGE otherwise).
  * repr_score: optional [batch][Hkv][n_new][l_bs] float64 output of r_m. */
 infllm_status infllm_build_units(const infllm_params* p, const infllm_memory* m, int32_t first_unit,
                                  int32_t n_new, int64_t past_len, double* repr_score, void* stream);

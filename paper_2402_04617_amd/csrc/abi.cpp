@@ -6,6 +6,7 @@
 
 #include <atomic>
 #include <cmath>
+#include <algorithm>
 #include <cstring>
 
 #include "../../include/infllm.h"
@@ -209,12 +210,27 @@ infllm_status prep_append(const infllm_params* p, const infllm_memory* m, const 
     return st;
   if (m->ring < 1 || m->ring <= n_q) return INFLLM_E_SHAPE;
   if (past_len + n_q > m->capacity) return INFLLM_E_RANGE;
+  if (m->rpart == nullptr) return INFLLM_E_NULL;
+  {
+    // Partial representative scores are formed for tokens t = p - l_L (t >= l_I) of
+    // the appended positions p; the running sum at t must still be in the ring
+    // after this chunk's slots are written, and the key of a token inside the
+    // chunk comes from k.
+    const int64_t t_lo = std::max<int64_t>(p->n_init, past_len - p->n_local);
+    const int64_t t_hi = past_len + n_q - p->n_local;  // exclusive
+    if (t_hi > t_lo) {
+      if (t_lo + m->ring < past_len + n_q) return INFLLM_E_RANGE;
+      if (t_hi > past_len && k == nullptr) return INFLLM_E_NULL;
+    }
+  }
   a->batch = m->batch;
   a->n_q_heads = p->n_q_heads;
   a->n_kv_heads = p->n_kv_heads;
   a->head_dim = p->head_dim;
   a->n_q = n_q;
   a->ring = m->ring;
+  a->n_init = p->n_init;
+  a->n_local = p->n_local;
   a->past_len = past_len;
   a->capacity = m->capacity;
   a->q_head_stride = q_head_stride;
@@ -225,6 +241,7 @@ infllm_status prep_append(const infllm_params* p, const infllm_memory* m, const 
   a->k_store = m->k;
   a->v_store = m->v;
   a->qprefix = m->qprefix;
+  a->rpart = m->rpart;
   a->bf16 = p->dtype == INFLLM_BF16;
   return INFLLM_OK;
 }
@@ -235,7 +252,7 @@ infllm_status prep_build(const infllm_params* p, const infllm_memory* m, int32_t
   if ((st = check_params(p)) != INFLLM_OK) return st;
   if ((st = check_store(p, m)) != INFLLM_OK) return st;
   if ((st = check_units(m)) != INFLLM_OK) return st;
-  if (m->qprefix == nullptr) return INFLLM_E_NULL;
+  if (m->rpart == nullptr) return INFLLM_E_NULL;
   if (first_unit < 0 || n_new < 0 || past_len < 0 || m->ring < 1) return INFLLM_E_SHAPE;
   if ((int64_t)first_unit + n_new > m->max_units) return INFLLM_E_RANGE;
   if (past_len > m->capacity) return INFLLM_E_RANGE;
@@ -259,7 +276,7 @@ infllm_status prep_build(const infllm_params* p, const infllm_memory* m, int32_t
   a->ring = m->ring;
   a->capacity = m->capacity;
   a->k_store = m->k;
-  a->qprefix = m->qprefix;
+  a->rpart = m->rpart;
   a->repr_idx = m->repr_idx;
   a->unit_ksum = m->unit_ksum;
   a->repr_score = repr_score;

@@ -4,11 +4,13 @@
 //    reads (scan blocks), and optionally the chunk's group-query total Qbar,
 //    which is exactly what unit scoring needs (the scan total, for free).
 //
-// The representative score of Section 3.2 needs, for every token m, the window
-// sum W_m = sum_{j=1..l_L} sum_{h in group} q^h_{m+j}.  With the running sum
-// Pi_t = sum_{p<=t} sum_h q^h_p kept per position, unit construction forms W_m
-// as one difference of two ring slots, so its cost does not grow with l_L.
-// float64 keeps the difference of two large running sums exact to ~1e-16.
+// The representative score of Section 3.2 needs, for every token t, the window
+// sum W_t = sum_{j=1..l_L} sum_{h in group} q^h_{t+j}.  With the running sum
+// Pi_p = sum_{p'<=p} sum_h q^h_{p'} kept per position, W_t is one difference of
+// two ring slots, so its cost does not grow with l_L; float64 keeps the
+// difference of two large running sums exact to ~1e-16.  The scan forms it as
+// soon as position p = t + l_L arrives and stores k_t . W_t per 16-dim slice
+// (rpart), which is all that unit construction reads later.
 //
 // In the whole-step path the same launch also carries the unit-construction
 // blocks of the units evicted since the previous step (see unit_build.h): they
@@ -46,6 +48,25 @@ __device__ __forceinline__ void load8(const T* p, double* out) {
     for (int e = 0; e < 4; ++e) {
       out[e] = (double)v[e];
       out[4 + e] = (double)v2[e];
+    }
+  }
+}
+
+template <typename T>
+__device__ __forceinline__ void load8f(const T* p, float* out) {
+  const uint4 raw = *(const uint4*)p;
+  if constexpr (sizeof(T) == 2) {
+    const bf16_t* v = (const bf16_t*)&raw;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) out[e] = bf16_to_f32(v[e]);
+  } else {
+    const float* v = (const float*)&raw;
+    const uint4 raw2 = *(const uint4*)(p + 4);
+    const float* v2 = (const float*)&raw2;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      out[e] = v[e];
+      out[4 + e] = v2[e];
     }
   }
 }
@@ -101,7 +122,8 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a, BuildArgs ba,
   const int b = bg / a.n_kv_heads, g = bg - b * a.n_kv_heads;
   const int half = threadIdx.x & 1, seg = threadIdx.x >> 1;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int d0 = (blk - bg * slices) * 16 + half * 8;
+  const int slice = blk - bg * slices;
+  const int d0 = slice * 16 + half * 8;
   const int G = GT > 0 ? GT : a.n_q_heads / a.n_kv_heads;
   const T* qb = (const T*)a.q + (int64_t)(b * a.n_q_heads + g * G) * a.q_head_stride + d0;
   double* ring = a.qprefix + (int64_t)bg * a.ring * D + d0;
@@ -124,6 +146,28 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a, BuildArgs ba,
 
   for (int t0 = 0; t0 < a.n_q; t0 += kTile) {
     const int i0 = t0 + seg * kSeg;
+    // When every token t = p - l_L of this tile precedes the chunk (l_L >= the
+    // tile's end, the streaming case), its running sum and key are loaded now,
+    // together with the queries, and its partial score is formed right where
+    // the new running sum is written.  Loads use clamped indices (the values of
+    // inactive tokens are never used).
+    const bool early = t0 + kTile <= a.n_local;
+    double2 ht[kSeg][4];
+    float kt[kSeg][8];
+    if (early) {
+#pragma unroll
+      for (int s = 0; s < kSeg; ++s) {
+        const int ic = min(i0 + s, a.n_q - 1);
+        const int sp = slot0 + ic - (slot0 + ic >= a.ring ? a.ring : 0);
+        const int st = sp - a.n_local + (sp < a.n_local ? a.ring : 0);  // n_local < ring
+        const double2* src = (const double2*)(ring + (int64_t)st * D);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) ht[s][e] = src[e];
+        int64_t tk = a.past_len + ic - a.n_local;
+        tk = tk < 0 ? 0 : tk;
+        load8f<T>((const T*)a.k_store + ((int64_t)bg * a.capacity + tk) * D + d0, kt[s]);
+      }
+    }
     double run[kSeg][8];
     double tot[8];
 #pragma unroll
@@ -189,22 +233,72 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a, BuildArgs ba,
         tile_tot[e] += y;
       }
     }
+    double part[kSeg];
 #pragma unroll
     for (int s = 0; s < kSeg; ++s) {
       const int i = i0 + s;
+      part[s] = 0.0;
       if (i < a.n_q) {
         const int slot = slot0 + i - (slot0 + i >= a.ring ? a.ring : 0);
         double* dst = ring + (int64_t)slot * D;
         double2* d2 = (double2*)dst;
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
-          d2[e] = make_double2(carry[2 * e] + off[2 * e] + run[s][2 * e],
-                               carry[2 * e + 1] + off[2 * e + 1] + run[s][2 * e + 1]);
+        for (int e = 0; e < 4; ++e) {
+          const double2 nv = make_double2(carry[2 * e] + off[2 * e] + run[s][2 * e],
+                                          carry[2 * e + 1] + off[2 * e + 1] + run[s][2 * e + 1]);
+          d2[e] = nv;
+          if (early)
+            part[s] += (double)kt[s][2 * e] * (nv.x - ht[s][e].x) + (double)kt[s][2 * e + 1] * (nv.y - ht[s][e].y);
+        }
+      }
+    }
+    if (early) {
+#pragma unroll
+      for (int s = 0; s < kSeg; ++s) {
+        const int i = i0 + s;
+        const int64_t t = a.past_len + i - a.n_local;
+        part[s] += __shfl_xor(part[s], 1);  // the two 8-dim halves of the slice
+        if (i < a.n_q && t >= a.n_init && half == 0)
+          a.rpart[((int64_t)bg * slices + slice) * a.ring + (int)(t % a.ring)] = part[s];
       }
     }
 #pragma unroll
     for (int e = 0; e < 8; ++e) carry[e] += tile_tot[e];
     __syncthreads();
+
+    // Otherwise the partial representative scores of the tokens t = p - l_L
+    // (t >= l_I) of this tile's positions p are formed now: both running sums are
+    // in the ring (the barrier above published this tile's slots; the host
+    // checked that the ring still holds slot t).  The key of a token inside the
+    // chunk comes from k_src.
+#pragma unroll
+    for (int s = 0; s < (early ? 0 : kSeg); ++s) {
+      const int i = i0 + s;
+      const int64_t t = a.past_len + i - a.n_local;
+      const bool act = i < a.n_q && t >= a.n_init;
+      double part = 0.0;
+      if (act) {
+        const int sp = slot0 + i - (slot0 + i >= a.ring ? a.ring : 0);
+        const int st = sp - a.n_local + (sp < a.n_local ? a.ring : 0);  // n_local < ring
+        const double2* hp = (const double2*)(ring + (int64_t)sp * D);
+        const double2* ht = (const double2*)(ring + (int64_t)st * D);
+        double kt[8];
+        if (t >= a.past_len)
+          load8<T>((const T*)a.k_src + (int64_t)bg * a.kv_head_stride + (t - a.past_len) * D + d0, kt);
+        else
+          load8<T>((const T*)a.k_store + ((int64_t)bg * a.capacity + t) * D + d0, kt);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const double2 x = hp[e], y = ht[e];
+          part += kt[2 * e] * (x.x - y.x) + kt[2 * e + 1] * (x.y - y.y);
+        }
+      }
+      part += __shfl_xor(part, 1);  // the two 8-dim halves of the slice
+      if (act && half == 0) {
+        const int st = (int)(t % a.ring);
+        a.rpart[((int64_t)bg * slices + slice) * a.ring + st] = part;
+      }
+    }
   }
   if (qbar != nullptr && seg == 0) {
 #pragma unroll

@@ -12,7 +12,7 @@
 namespace infllm {
 
 struct AppendArgs {
-  int batch, n_q_heads, n_kv_heads, head_dim, n_q, ring;
+  int batch, n_q_heads, n_kv_heads, head_dim, n_q, ring, n_init, n_local;
   int64_t past_len, capacity, q_head_stride, kv_head_stride;
   const void* q;
   const void* k_src;
@@ -20,6 +20,7 @@ struct AppendArgs {
   void* k_store;
   void* v_store;
   double* qprefix;
+  double* rpart;  // [B*Hkv][D/16][ring] partial representative scores
   bool bf16;
 };
 struct BuildArgs;
@@ -33,7 +34,7 @@ struct BuildArgs {
   int first_unit, n_new, max_units, ring;
   int64_t capacity;
   const void* k_store;
-  const double* qprefix;
+  const double* rpart;
   int32_t* repr_idx;
   float* unit_ksum;
   double* repr_score;  // nullable

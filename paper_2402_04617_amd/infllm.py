@@ -42,7 +42,8 @@ class Params(ctypes.Structure):
 class Memory(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("capacity", ctypes.c_int64), ("k", ctypes.c_void_p),
                 ("v", ctypes.c_void_p), ("max_units", ctypes.c_int32), ("repr_idx", ctypes.c_void_p),
-                ("unit_ksum", ctypes.c_void_p), ("qprefix", ctypes.c_void_p), ("ring", ctypes.c_int32)]
+                ("unit_ksum", ctypes.c_void_p), ("qprefix", ctypes.c_void_p), ("rpart", ctypes.c_void_p),
+                ("ring", ctypes.c_int32)]
 
 
 _lib = None
@@ -188,6 +189,7 @@ class LayerMemory:
     repr_idx: "object"
     unit_ksum: "object"
     qprefix: "object"
+    rpart: "object"
     struct: Memory
 
 
@@ -207,9 +209,10 @@ def alloc_memory(p: Params, batch: int, capacity: int, max_units: int, ring: int
     repr_idx = torch.zeros((batch, p.n_kv_heads, mu, p.n_repr), dtype=torch.int32, device=device)
     unit_ksum = torch.zeros((batch, p.n_kv_heads, D // 4, mu, 4), dtype=torch.float32, device=device)
     qprefix = torch.zeros((batch, p.n_kv_heads, ring, D), dtype=torch.float64, device=device)
+    rpart = torch.zeros((batch, p.n_kv_heads, D // 16, ring), dtype=torch.float64, device=device)
     st = Memory(batch, capacity, k.data_ptr(), v.data_ptr(), max_units, repr_idx.data_ptr(),
-                unit_ksum.data_ptr(), qprefix.data_ptr(), ring)
-    return LayerMemory(k, v, repr_idx, unit_ksum, qprefix, st)
+                unit_ksum.data_ptr(), qprefix.data_ptr(), rpart.data_ptr(), ring)
+    return LayerMemory(k, v, repr_idx, unit_ksum, qprefix, rpart, st)
 
 
 def recommended_ring(p: Params, chunk: int) -> int:

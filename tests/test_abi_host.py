@@ -97,7 +97,7 @@ def test_workspace_bytes(L):
 
 def mem(**kw):
     base = dict(batch=1, capacity=1 << 17, k=FAKE, v=FAKE, max_units=2048, repr_idx=FAKE,
-                unit_ksum=FAKE, qprefix=FAKE, ring=4096 + 128 + 512 + 1)
+                unit_ksum=FAKE, qprefix=FAKE, rpart=FAKE, ring=4096 + 128 + 2 * 512 + 1)
     base.update(kw)
     return F.Memory(**base)
 
@@ -118,7 +118,15 @@ def test_append_validation(L):
     assert f(bp, ctypes.byref(small), FAKE, 512 * 128, None, None, 0, 512, 0, None) == 2  # ring <= n_q
     noq = mem(qprefix=None)
     assert f(bp, ctypes.byref(noq), FAKE, 512 * 128, None, None, 0, 512, 0, None) == 1
+    nor = mem(rpart=None)
+    assert f(bp, ctypes.byref(nor), FAKE, 512 * 128, None, None, 0, 512, 0, None) == 1
     assert f(bp, bm, FAKE, 512 * 128, None, None, 0, -1, 0, None) == 2
+    # streaming past l_L: the ring must keep the running sum of token p - l_L (ring >= l_L + n_q)
+    short = mem(ring=4096 + 511)
+    assert f(bp, ctypes.byref(short), FAKE, 512 * 128, None, None, 0, 512, 10000, None) == 3
+    # a token inside the chunk (l_L < n_q) needs the chunk's keys
+    p2 = P(n_local=256)
+    assert f(ctypes.byref(p2), bm, FAKE, 512 * 128, None, None, 0, 512, 10000, None) == 1
 
 
 def test_build_validation(L):
@@ -131,9 +139,11 @@ def test_build_validation(L):
     assert f(bp, bm, 2040, 16, 1 << 17, None, None) == 3     # beyond max_units
     assert f(bp, bm, -1, 1, 10000, None, None) == 2
     # ring too short for the oldest slot: unit 0 starts at 128, ring holds [past-ring, past)
-    assert f(bp, bm, 0, 1, 128 + 4833, None, None) == 3
+    assert f(bp, bm, 0, 1, 128 + 5249 + 123, None, None) == 3
     nou = mem(unit_ksum=None)
     assert f(bp, ctypes.byref(nou), 0, 1, 4352, None, None) == 1
+    nor = mem(rpart=None)
+    assert f(bp, ctypes.byref(nor), 0, 1, 4352, None, None) == 1
     assert f(bp, bm, 0, 0, 0, None, None) == 0  # nothing to build: no device needed
 
 
