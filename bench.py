@@ -16,6 +16,7 @@ decode) are reported in the same line.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
 import sys
@@ -29,6 +30,40 @@ sys.path.insert(0, ROOT)
 
 PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
+
+# HBM traffic of one 128K-encode attention launch, from two rocprofv3 --pmc passes (FETCH_SIZE, then
+# WRITE_SIZE; KiB per dispatch, averaged over the launches of `bench.py --legs none --steps 1 --warmup 0`),
+# each divided by what the same counter reads per KiB moved by the plain copy of `bench.py
+# --copy-calibration 1024`.  Valid only for the attention source it was taken on (sha256 below);
+# reported as null once that file changes.
+ATTN_SRC = os.path.join(ROOT, "paper_2402_04617_amd", "csrc", "attend_mfma.hip")
+ATTN_TRAFFIC = {"src_sha256": "90782a63b156b11502f600b78746edc06358618a85d56715b1017137c4625604",
+                "fetch_kib": 19964.19, "write_kib": 33024.0,  # per attention dispatch (768 dispatches)
+                "copy_fetch": 524300.06 / 1048576.0,  # FETCH_SIZE KiB per KiB read by the copy
+                "copy_write": 1048576.0 / 1048576.0}  # WRITE_SIZE KiB per KiB written by the copy
+
+
+def attention_traffic_bytes():
+    t = ATTN_TRAFFIC
+    if t is None:
+        return None
+    with open(ATTN_SRC, "rb") as f:
+        if hashlib.sha256(f.read()).hexdigest() != t["src_sha256"]:
+            return None
+    return 1024.0 * (t["fetch_kib"] / t["copy_fetch"] + t["write_kib"] / t["copy_write"])
+
+
+def copy_calibration(mib, torch, reps=3):
+    """A plain device copy of `mib` MiB (read mib, write mib) repeated `reps` times: the reference
+    dispatch whose FETCH_SIZE / WRITE_SIZE per KiB moved calibrates the attention kernel's counters."""
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(reps):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_mib": mib, "reps": reps, "kernel": "elementwise neg (read N, write N)"}), flush=True)
 
 
 def log(msg):
@@ -62,6 +97,23 @@ def attention_flops(wl, steps):
         n_init, n_units, local_begin = F.infllm_partition(p, past)
         ctx = n_init + min(wl.topk, n_units) * wl.block_size + (past - local_begin)
         total += 4 * wl.head_dim * wl.n_q_heads * wl.batch * (n * ctx + n * (n + 1) // 2)
+    return total
+
+
+def attention_bytes(wl, steps, parts):
+    """Algorithmic HBM bytes of the attention launches of a pass: each query row read once, each
+    visible context key and value read once per kv head, and the output written once per part
+    (float32 partial rows plus LSE when a launch splits the keys, the bf16 output otherwise)."""
+    from paper_2402_04617_amd import infllm as F
+    p = params_of(wl)
+    e = 2 if wl.dtype == "bf16" else 4
+    total = 0
+    for (past, n), np_ in zip(steps, parts):
+        n_init, n_units, local_begin = F.infllm_partition(p, past)
+        keys = n_init + min(wl.topk, n_units) * wl.block_size + (past - local_begin) + n
+        rows = wl.batch * wl.n_q_heads * n
+        total += rows * wl.head_dim * e + 2 * wl.batch * wl.n_kv_heads * keys * wl.head_dim * e
+        total += np_ * rows * (wl.head_dim + 1) * 4 if np_ > 1 else rows * wl.head_dim * e
     return total
 
 
@@ -127,21 +179,21 @@ class Stream:
         return built
 
     def attention_replay(self, steps, idx_hist):
-        """Attention kernels alone, same launches as in the step, each bracketed by HIP events on the
-        launching stream; returns per-launch durations (ms) of the attention kernel."""
+        """The attention kernels alone, the same launches as in the step (lookups recorded from a real
+        pass), issued back to back on the launching stream between two HIP events: returns the average
+        launch duration (ms) and the number of key parts of each launch."""
         F, torch, wl, S, D = self.F, self.torch, self.wl, self.wl.seq_len, self.wl.head_dim
-        evs = []
-        for i, (past, n) in enumerate(steps):
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record()
-            parts = F.infllm_attend_partial(self.p, self.mem.struct, self.ptr("q", past), S * D, n, past,
-                                            idx_hist[i], wl.topk, self.out, wl.chunk * D, self.lse, self.ws)
-            b.record()
-            if parts > 1:
-                F.infllm_lse_merge(self.p, wl.batch, n, parts, self.ws, self.out, wl.chunk * D, self.lse)
-            evs.append((a, b))
+        parts_seen = []
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
-        return [a.elapsed_time(b) for a, b in evs]
+        a.record()
+        for i, (past, n) in enumerate(steps):
+            parts_seen.append(F.infllm_attend_partial(self.p, self.mem.struct, self.ptr("q", past), S * D, n, past,
+                                                      idx_hist[i], wl.topk, self.out, wl.chunk * D, self.lse,
+                                                      self.ws))
+        b.record()
+        torch.cuda.synchronize()
+        return a.elapsed_time(b) / len(steps), parts_seen
 
 
 def time_steps(torch, fn, steps, warmup):
@@ -173,11 +225,12 @@ def encode_leg(name, seed, steps, warmup, torch, want_roofline=True):
         # one more (untimed) pass recording the lookup of every chunk, then the attention replay
         idx_hist = torch.zeros((len(plan),) + tuple(st.idx.shape), dtype=torch.int32, device="cuda")
         st.run(plan, on_step=lambda i: idx_hist[i].copy_(st.idx))
-        durs = st.attention_replay(plan, idx_hist)
+        avg_ms, parts = st.attention_replay(plan, idx_hist)
         flops = attention_flops(wl, plan)
-        tot_ms = float(np.sum(durs))
-        res["attention"] = {"launches": len(durs), "avg_ms": tot_ms / len(durs), "total_ms": tot_ms,
-                            "algorithmic_flops": flops, "tflops": flops / (tot_ms / 1e3) / 1e12}
+        tot_ms = avg_ms * len(plan)
+        res["attention"] = {"launches": len(plan), "avg_ms": avg_ms, "total_ms": tot_ms,
+                            "algorithmic_flops": flops, "tflops": flops / (tot_ms / 1e3) / 1e12,
+                            "algorithmic_bytes_per_launch": attention_bytes(wl, plan, parts) / len(plan)}
     return res, synth, st
 
 
@@ -246,6 +299,8 @@ def main():
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--legs", default="1m,decode", help="extra legs: comma list of 1m, decode (or 'none')")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run the plain-copy calibration dispatch of MIB MiB (for the traffic counters)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -255,6 +310,10 @@ def main():
         sys.exit(2)
 
     import torch
+    if args.copy_calibration > 0:
+        torch.cuda.set_device(0)
+        copy_calibration(args.copy_calibration, torch)
+        return
     from paper_2402_04617_amd import infllm as F
     F.lib()
     torch.cuda.set_device(0)
@@ -297,7 +356,9 @@ def main():
                    "chunk": 512, "parallelism": "single-gpu"},
         "roofline": {"bound": "mfma", "kernel": "attend_mfma_kernel<128>", "achieved": achieved,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
-                     "traffic": None, "avg_launch_ms": att["avg_ms"], "launches_per_step": att["launches"]},
+                     "traffic": attention_traffic_bytes(), "traffic_unit": "B/launch",
+                     "algorithmic_bytes": att["algorithmic_bytes_per_launch"], "avg_launch_ms": att["avg_ms"],
+                     "launches_per_step": att["launches"]},
         "extra": extra,
     }
     if not args.no_cpu_baseline:

@@ -17,7 +17,7 @@ BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libinfllm.so")
 
 SOURCES = ["abi.cpp", "append.hip", "build_units.hip", "score.hip", "topk.hip", "attend_mfma.hip",
-           "attend.hip", "merge.hip"]
+           "attend.hip", "attend_decode.hip", "merge.hip"]
 
 # Packed fp32 ops are disabled for all device code (the host pass warns that it
 # does not know the feature; that is harmless).

@@ -139,7 +139,8 @@ infllm_status prepare_attend(const infllm_params* p, const infllm_memory* m, con
   const int64_t rows = (int64_t)m->batch * p->n_q_heads * n_q;
   const size_t per_part = rows > 0 ? (size_t)rows * (size_t)(p->head_dim + 1) * 4u : 1;
   const int max_parts = (workspace == nullptr) ? 0 : (int)(workspace_bytes / per_part > 4096 ? 4096 : workspace_bytes / per_part);
-  const int parts = attend_choose_parts(bf16, m->batch, p->n_q_heads, p->n_kv_heads, n_q, (int)n_virtual, max_parts);
+  const int parts = attend_choose_parts(bf16, m->batch, p->n_q_heads, p->n_kv_heads, n_q, n_sel, (int)n_virtual,
+                                        max_parts);
   if (parts < 1) return INFLLM_E_WORKSPACE;
   if (parts > 1 && !aligned16(workspace)) return INFLLM_E_SHAPE;
 

@@ -19,7 +19,8 @@
 // latency-bound jobs overlap instead of running back to back.
 //
 // Scan block: one (sequence*kv head, 16-dim slice); 256 threads = 128 position
-// segments x 2 halves of 8 dims.  Each thread sums its segment (kSeg positions)
+// segments x 2 halves of 8 dims.  Chunks of a few positions (decoding) use thin
+// scan blocks instead, one thread per (sequence*kv head, dim).  Each thread sums its segment (kSeg positions)
 // in registers, a wave-level shuffle scan and an LDS pass over the 4 waves give
 // the segment offsets, and each thread writes its kSeg ring rows.
 #include <cstring>
@@ -32,6 +33,7 @@ namespace {
 constexpr int kSeg = 4;                 // positions per thread per tile
 constexpr int kTile = 128 * kSeg;       // positions per scan tile
 constexpr int kCopyPerThread = 4;       // 16-byte vectors per thread in copy blocks
+constexpr int kThinMaxQ = 8;            // chunks this short take the one-thread-per-dim scan
 
 template <typename T>
 __device__ __forceinline__ void load8(const T* p, double* out) {
@@ -75,6 +77,7 @@ __device__ __forceinline__ void load8f(const T* p, float* out) {
 struct AppendGrid {
   int n_build;          // unit-construction blocks (n_new * batch * Hkv), 0 when not fused
   int n_scan;           // scan blocks
+  bool thin;            // scan blocks are thin (one thread per (sequence*kv head, dim))
   int n_copy_per_head;  // copy blocks per (sequence, kv head)
 };
 
@@ -113,6 +116,66 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a, BuildArgs ba,
         dst_v[e] = src_v[e];
       }
     }
+    return;
+  }
+
+  if (grid.thin) {
+    // ---- thin scan role, for chunks of at most kThinMaxQ positions (decoding):
+    // one thread per (sequence*kv head, dim) walks the positions in order.  The
+    // 16 threads of a slice are adjacent lanes, so the partial score of a slice
+    // is a 16-lane sum.
+    const int gid = blk * 256 + threadIdx.x;
+    if (gid >= a.batch * a.n_kv_heads * D) return;  // whole waves: the total is a multiple of 64
+    const int bg = gid / D, d = gid - bg * D;
+    const int b = bg / a.n_kv_heads, g = bg - b * a.n_kv_heads;
+    const int G = GT > 0 ? GT : a.n_q_heads / a.n_kv_heads;
+    const T* qb = (const T*)a.q + (int64_t)(b * a.n_q_heads + g * G) * a.q_head_stride + d;
+    double* col = a.qprefix + (int64_t)bg * a.ring * D + d;
+    const int slot0 = (int)(a.past_len % a.ring);
+    // every load that does not depend on this launch's writes is issued first
+    double x[kThinMaxQ], ht[kThinMaxQ];
+    float kt[kThinMaxQ];
+#pragma unroll
+    for (int i = 0; i < kThinMaxQ; ++i) {
+      x[i] = 0.0;
+      ht[i] = 0.0;
+      kt[i] = 0.f;
+      if (i < a.n_q) {
+        for (int h = 0; h < G; ++h) x[i] += (double)Elem<T>::load(qb + h * a.q_head_stride + (int64_t)i * D);
+        const int64_t t = a.past_len + i - a.n_local;
+        if (t >= a.n_init && t < a.past_len) {
+          const int sp = slot0 + i - (slot0 + i >= a.ring ? a.ring : 0);
+          const int st = sp - a.n_local + (sp < a.n_local ? a.ring : 0);  // n_local < ring
+          ht[i] = col[(int64_t)st * D];
+          kt[i] = Elem<T>::load((const T*)a.k_store + ((int64_t)bg * a.capacity + t) * D + d);
+        }
+      }
+    }
+    double run = 0.0;
+    if (a.past_len > 0) run = col[(int64_t)(slot0 == 0 ? a.ring - 1 : slot0 - 1) * D];
+    const double base = run;
+#pragma unroll
+    for (int i = 0; i < kThinMaxQ; ++i) {
+      if (i >= a.n_q) break;
+      run += x[i];
+      const int sp = slot0 + i - (slot0 + i >= a.ring ? a.ring : 0);
+      col[(int64_t)sp * D] = run;
+      const int64_t t = a.past_len + i - a.n_local;
+      if (t >= a.n_init) {
+        double h = ht[i], k = kt[i];
+        if (t >= a.past_len) {
+          // token of this chunk: its running sum was written by this thread above
+          const int st = sp - a.n_local + (sp < a.n_local ? a.ring : 0);
+          h = col[(int64_t)st * D];
+          k = Elem<T>::load((const T*)a.k_src + (int64_t)bg * a.kv_head_stride + (t - a.past_len) * D + d);
+        }
+        double part = k * (run - h);
+#pragma unroll
+        for (int o = 1; o < 16; o <<= 1) part += __shfl_xor(part, o);
+        if ((d & 15) == 0) a.rpart[((int64_t)bg * (D / 16) + d / 16) * a.ring + (int)(t % a.ring)] = part;
+      }
+    }
+    if (qbar != nullptr) qbar[(int64_t)bg * D + d] = (float)(run - base);
     return;
   }
 
@@ -339,7 +402,10 @@ hipError_t launch_append(const AppendArgs& a, hipStream_t s, float* qbar, const 
   g.n_build = fused_build != nullptr ? fused_build->n_new * fused_build->batch * fused_build->n_kv_heads : 0;
   if (a.n_q == 0 && g.n_build == 0) return hipSuccess;
   const int esize = a.bf16 ? 2 : 4;
-  g.n_scan = a.n_q > 0 ? a.batch * a.n_kv_heads * (a.head_dim / 16) : 0;
+  g.thin = a.n_q <= kThinMaxQ;
+  g.n_scan = a.n_q <= 0 ? 0
+             : g.thin ? (a.batch * a.n_kv_heads * a.head_dim + 255) / 256
+                      : a.batch * a.n_kv_heads * (a.head_dim / 16);
   g.n_copy_per_head = 0;
   if (a.k_src != nullptr && a.n_q > 0) {
     const int vec_per_head = a.n_q * a.head_dim / (16 / esize);

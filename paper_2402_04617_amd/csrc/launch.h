@@ -63,6 +63,13 @@ hipError_t launch_select_topk(int rows, const float* scores, int n_units, int k,
 // workgroup count the part chooser aims for (one per compute unit).
 constexpr int kMfmaRowsPerWg = 256;
 constexpr int kMfmaTargetWgs = 256;
+// Workgroups the bf16 decode kernel aims for (two per compute unit), and the
+// fewest keys it gives one workgroup.
+constexpr int kDecodeTargetWgs = 512;
+constexpr int kDecodeMinKeysPerWg = 256;
+// Most selected units the decode kernel stages in LDS; longer lookups decode on
+// the matrix-core kernel.
+constexpr int kDecodeMaxSel = 1024;
 
 struct AttendArgs {
   int batch, n_q_heads, n_kv_heads, head_dim;
@@ -81,7 +88,7 @@ struct AttendArgs {
   bool bf16;
 };
 // Number of key parts the attention uses for this shape, limited by max_parts.
-int attend_choose_parts(bool bf16, int batch, int n_q_heads, int n_kv_heads, int n_q, int n_virtual,
+int attend_choose_parts(bool bf16, int batch, int n_q_heads, int n_kv_heads, int n_q, int n_sel, int n_virtual,
                         int max_parts);
 hipError_t launch_attend(const AttendArgs& a, hipStream_t s);
 

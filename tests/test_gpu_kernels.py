@@ -187,6 +187,9 @@ ATTEND_CASES = [
     ("bf16", 4, 2, 128, 128, 4096, 128, 32, 13000, 1, 3),   # decode
     ("bf16", 8, 2, 64, 16, 300, 32, 5, 1000, 1, 2),         # decode, G=8, D=64
     ("bf16", 3, 1, 128, 16, 300, 32, 5, 1000, 1, 1),        # decode shape with G=3 (MFMA path)
+    ("bf16", 2, 4, 128, 4, 700, 16, 9, 2500, 1, 2),         # decode, G=2: runs not aligned to load tiles
+    ("bf16", 1, 3, 64, 7, 333, 24, 6, 1200, 1, 1),          # decode, G=1, D=64
+    ("bf16", 8, 2, 64, 16, 1000, 32, 20, 3000, 1, 2),       # decode, G=8, D=64, several key parts
     ("f32", 2, 1, 64, 16, 256, 32, 4, 1000, 64, 1),
     ("f32", 2, 1, 64, 16, 256, 32, 4, 1000, 1, 1),
     ("f32", 4, 2, 128, 128, 512, 128, 4, 3000, 37, 2),
@@ -236,8 +239,8 @@ def test_chunk_attend(case):
     _attend_case(case)
 
 
-@pytest.mark.parametrize("case", [ATTEND_CASES[0], ATTEND_CASES[3], ATTEND_CASES[11]],
-                         ids=["bf16", "bf16-batch", "f32"])
+@pytest.mark.parametrize("case", [ATTEND_CASES[0], ATTEND_CASES[3], ATTEND_CASES[9], ATTEND_CASES[14]],
+                         ids=["bf16", "bf16-batch", "bf16-decode", "f32"])
 def test_chunk_attend_single_part_and_invalid_entries(case):
     _attend_case(case, workspace=False)
     _attend_case(case, invalid_entry=True)
