@@ -19,10 +19,13 @@
 // latency-bound jobs overlap instead of running back to back.
 //
 // Scan block: one (sequence*kv head, 16-dim slice); 256 threads = 128 position
-// segments x 2 halves of 8 dims.  Chunks of a few positions (decoding) use thin
-// scan blocks instead, one thread per (sequence*kv head, dim).  Each thread sums its segment (kSeg positions)
-// in registers, a wave-level shuffle scan and an LDS pass over the 4 waves give
-// the segment offsets, and each thread writes its kSeg ring rows.
+// segments x 2 halves of 8 dims.  Each thread first issues every load of its
+// segment (kSeg positions: the group's query pieces, and in the streaming case
+// the running sums and keys of the tokens t = p - l_L), then sums in float64; a
+// wave-level shuffle scan and an LDS pass over the 4 waves give the segment
+// offsets, and each thread writes its kSeg ring rows.  Chunks of a few positions
+// (decoding) use thin scan blocks instead, one thread per (sequence*kv head,
+// dim).  Copy blocks likewise load all their vectors before storing any.
 #include <cstring>
 
 #include "unit_build.h"
@@ -30,45 +33,42 @@
 namespace infllm {
 namespace {
 
-constexpr int kSeg = 4;                 // positions per thread per tile
-constexpr int kTile = 128 * kSeg;       // positions per scan tile
-constexpr int kCopyPerThread = 4;       // 16-byte vectors per thread in copy blocks
-constexpr int kThinMaxQ = 8;            // chunks this short take the one-thread-per-dim scan
+constexpr int kThreads = 256;                  // threads of every block of the launch (one wave per SIMD:
+                                               // a scan thread keeps a whole segment's loads in flight)
+constexpr int kWaves = kThreads / 64;
+constexpr int kSeg = 4;                        // positions per thread per tile
+constexpr int kTile = (kThreads / 2) * kSeg;   // positions per scan tile
+constexpr int kCopyPerThread = 4;              // 16-byte vectors per thread in copy blocks
+constexpr int kThinMaxQ = 8;                   // chunks this short take the one-thread-per-dim scan
 
+// Eight consecutive elements as raw 16-byte words (one for bf16, two for float32).
 template <typename T>
-__device__ __forceinline__ void load8(const T* p, double* out) {
-  const uint4 raw = *(const uint4*)p;
-  if constexpr (sizeof(T) == 2) {
-    const bf16_t* v = (const bf16_t*)&raw;
+struct Raw8 {
+  uint4 w[sizeof(T) / 2];
+};
+template <typename T>
+__device__ __forceinline__ Raw8<T> load_raw8(const T* p) {
+  Raw8<T> r;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) out[e] = (double)bf16_to_f32(v[e]);
-  } else {
-    const float* v = (const float*)&raw;
-    const uint4 raw2 = *(const uint4*)(p + 4);
-    const float* v2 = (const float*)&raw2;
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      out[e] = (double)v[e];
-      out[4 + e] = (double)v2[e];
-    }
-  }
+  for (int j = 0; j < (int)(sizeof(T) / 2); ++j) r.w[j] = ((const uint4*)p)[j];
+  return r;
 }
-
 template <typename T>
-__device__ __forceinline__ void load8f(const T* p, float* out) {
-  const uint4 raw = *(const uint4*)p;
+__device__ __forceinline__ void raw8_to_float(const Raw8<T>& r, float* out) {
   if constexpr (sizeof(T) == 2) {
-    const bf16_t* v = (const bf16_t*)&raw;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) out[e] = bf16_to_f32(v[e]);
-  } else {
-    const float* v = (const float*)&raw;
-    const uint4 raw2 = *(const uint4*)(p + 4);
-    const float* v2 = (const float*)&raw2;
+    const uint32_t w[4] = {r.w[0].x, r.w[0].y, r.w[0].z, r.w[0].w};
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      out[e] = v[e];
-      out[4 + e] = v2[e];
+      out[2 * e] = __uint_as_float(w[e] << 16);
+      out[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      out[4 * j + 0] = __uint_as_float(r.w[j].x);
+      out[4 * j + 1] = __uint_as_float(r.w[j].y);
+      out[4 * j + 2] = __uint_as_float(r.w[j].z);
+      out[4 * j + 3] = __uint_as_float(r.w[j].w);
     }
   }
 }
@@ -83,15 +83,15 @@ struct AppendGrid {
 
 // GT: the query group size G when known at compile time (0: read it at run time).
 template <typename T, int GT, int DT>
-__global__ void __launch_bounds__(256) append_kernel(AppendArgs a, BuildArgs ba, AppendGrid grid,
-                                                     float* __restrict__ qbar) {
+__global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArgs ba, AppendGrid grid,
+                                                          float* __restrict__ qbar) {
   const int D = a.head_dim;
   __shared__ BuildSmem bsm;
   int blk = blockIdx.x;
   if (blk < grid.n_build) {
     // ---- unit-construction role
     const int bh = ba.batch * ba.n_kv_heads;
-    build_one_unit<T, DT, 256>(ba, blk / bh, blk % bh, bsm);
+    build_one_unit<T, DT, kThreads>(ba, blk / bh, blk % bh, bsm);
     return;
   }
   blk -= grid.n_build;
@@ -107,15 +107,19 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a, BuildArgs ba,
     const uint4* src_v = (const uint4*)a.v_src + head * (a.kv_head_stride / VEC);
     uint4* dst_k = (uint4*)a.k_store + head * (a.capacity * D / VEC) + a.past_len * D / VEC;
     uint4* dst_v = (uint4*)a.v_store + head * (a.capacity * D / VEC) + a.past_len * D / VEC;
-    const int base = cblk * 256 * kCopyPerThread + threadIdx.x;
-#pragma unroll
-    for (int j = 0; j < kCopyPerThread; ++j) {
-      const int e = base + j * 256;
-      if (e < vec_per_head) {
-        dst_k[e] = src_k[e];
-        dst_v[e] = src_v[e];
-      }
-    }
+    const int base = cblk * kThreads * kCopyPerThread + threadIdx.x;
+    // all loads first (clamped indices), then the guarded stores
+    const int e0 = base, e1 = base + kThreads, e2 = base + 2 * kThreads, e3 = base + 3 * kThreads;
+    static_assert(kCopyPerThread == 4, "copy role moves four vectors per thread");
+    const int last = vec_per_head - 1;
+    const uint4 k0 = src_k[min(e0, last)], k1 = src_k[min(e1, last)], k2 = src_k[min(e2, last)],
+                k3 = src_k[min(e3, last)];
+    const uint4 v0 = src_v[min(e0, last)], v1 = src_v[min(e1, last)], v2 = src_v[min(e2, last)],
+                v3 = src_v[min(e3, last)];
+    if (e0 < vec_per_head) { dst_k[e0] = k0; dst_v[e0] = v0; }
+    if (e1 < vec_per_head) { dst_k[e1] = k1; dst_v[e1] = v1; }
+    if (e2 < vec_per_head) { dst_k[e2] = k2; dst_v[e2] = v2; }
+    if (e3 < vec_per_head) { dst_k[e3] = k3; dst_v[e3] = v3; }
     return;
   }
 
@@ -124,7 +128,7 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a, BuildArgs ba,
     // one thread per (sequence*kv head, dim) walks the positions in order.  The
     // 16 threads of a slice are adjacent lanes, so the partial score of a slice
     // is a 16-lane sum.
-    const int gid = blk * 256 + threadIdx.x;
+    const int gid = blk * kThreads + threadIdx.x;
     if (gid >= a.batch * a.n_kv_heads * D) return;  // whole waves: the total is a multiple of 64
     const int bg = gid / D, d = gid - bg * D;
     const int b = bg / a.n_kv_heads, g = bg - b * a.n_kv_heads;
@@ -156,7 +160,7 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a, BuildArgs ba,
     const double base = run;
 #pragma unroll
     for (int i = 0; i < kThinMaxQ; ++i) {
-      if (i >= a.n_q) break;
+      if (i >= a.n_q) continue;  // (not break: the loop stays unrolled, the arrays in registers)
       run += x[i];
       const int sp = slot0 + i - (slot0 + i >= a.ring ? a.ring : 0);
       col[(int64_t)sp * D] = run;
@@ -191,7 +195,7 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a, BuildArgs ba,
   const T* qb = (const T*)a.q + (int64_t)(b * a.n_q_heads + g * G) * a.q_head_stride + d0;
   double* ring = a.qprefix + (int64_t)bg * a.ring * D + d0;
 
-  __shared__ double wave_tot[4][2][8];
+  __shared__ double wave_tot[kWaves][2][8];
   const int slot0 = (int)(a.past_len % a.ring);  // ring > n_q: slot0 + i wraps at most once
   double base[8], carry[8];
   if (a.past_len > 0) {
@@ -207,16 +211,24 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a, BuildArgs ba,
   // every thread holds the base before any slot is written (new slots never alias it: ring > n_q)
   __syncthreads();
 
+  constexpr int GQ = GT > 0 ? GT : 1;  // query pieces loaded up front per position
   for (int t0 = 0; t0 < a.n_q; t0 += kTile) {
     const int i0 = t0 + seg * kSeg;
     // When every token t = p - l_L of this tile precedes the chunk (l_L >= the
     // tile's end, the streaming case), its running sum and key are loaded now,
     // together with the queries, and its partial score is formed right where
     // the new running sum is written.  Loads use clamped indices (the values of
-    // inactive tokens are never used).
+    // inactive positions are never used).
     const bool early = t0 + kTile <= a.n_local;
+    Raw8<T> qr[kSeg][GQ];
     double2 ht[kSeg][4];
-    float kt[kSeg][8];
+    Raw8<T> kr[kSeg];
+#pragma unroll
+    for (int s = 0; s < kSeg; ++s) {
+      const int ic = min(i0 + s, a.n_q - 1);
+#pragma unroll
+      for (int h = 0; h < GQ; ++h) qr[s][h] = load_raw8<T>(qb + h * a.q_head_stride + (int64_t)ic * D);
+    }
     if (early) {
 #pragma unroll
       for (int s = 0; s < kSeg; ++s) {
@@ -228,7 +240,7 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a, BuildArgs ba,
         for (int e = 0; e < 4; ++e) ht[s][e] = src[e];
         int64_t tk = a.past_len + ic - a.n_local;
         tk = tk < 0 ? 0 : tk;
-        load8f<T>((const T*)a.k_store + ((int64_t)bg * a.capacity + tk) * D + d0, kt[s]);
+        kr[s] = load_raw8<T>((const T*)a.k_store + ((int64_t)bg * a.capacity + tk) * D + d0);
       }
     }
     double run[kSeg][8];
@@ -237,26 +249,25 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a, BuildArgs ba,
     for (int e = 0; e < 8; ++e) tot[e] = 0.0;
 #pragma unroll
     for (int s = 0; s < kSeg; ++s) {
-      // clamp instead of branching so every load of the segment is issued up front
       const int i = min(i0 + s, a.n_q - 1);
       const bool valid = i0 + s < a.n_q;
       double x[8];
 #pragma unroll
       for (int e = 0; e < 8; ++e) x[e] = 0.0;
       if constexpr (GT > 0) {
-        double y[GT][8];
 #pragma unroll
-        for (int h = 0; h < GT; ++h) load8<T>(qb + h * a.q_head_stride + (int64_t)i * D, y[h]);
+        for (int h = 0; h < GT; ++h) {
+          float y[8];
+          raw8_to_float<T>(qr[s][h], y);
 #pragma unroll
-        for (int h = 0; h < GT; ++h)
-#pragma unroll
-          for (int e = 0; e < 8; ++e) x[e] += y[h][e];
+          for (int e = 0; e < 8; ++e) x[e] += (double)y[e];
+        }
       } else {
         for (int h = 0; h < G; ++h) {
-          double y[8];
-          load8<T>(qb + h * a.q_head_stride + (int64_t)i * D, y);
+          float y[8];
+          raw8_to_float<T>(h == 0 ? qr[s][0] : load_raw8<T>(qb + h * a.q_head_stride + (int64_t)i * D), y);
 #pragma unroll
-          for (int e = 0; e < 8; ++e) x[e] += y[e];
+          for (int e = 0; e < 8; ++e) x[e] += (double)y[e];
         }
       }
 #pragma unroll
@@ -288,7 +299,8 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a, BuildArgs ba,
       off[e] = incl[e] - tot[e];
       tile_tot[e] = 0.0;
     }
-    for (int w = 0; w < 4; ++w) {
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
         const double y = wave_tot[w][half][e];
@@ -300,6 +312,8 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a, BuildArgs ba,
 #pragma unroll
     for (int s = 0; s < kSeg; ++s) {
       const int i = i0 + s;
+      float kt[8];
+      raw8_to_float<T>(kr[s], kt);
       part[s] = 0.0;
       if (i < a.n_q) {
         const int slot = slot0 + i - (slot0 + i >= a.ring ? a.ring : 0);
@@ -311,7 +325,7 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a, BuildArgs ba,
                                           carry[2 * e + 1] + off[2 * e + 1] + run[s][2 * e + 1]);
           d2[e] = nv;
           if (early)
-            part[s] += (double)kt[s][2 * e] * (nv.x - ht[s][e].x) + (double)kt[s][2 * e + 1] * (nv.y - ht[s][e].y);
+            part[s] += (double)kt[2 * e] * (nv.x - ht[s][e].x) + (double)kt[2 * e + 1] * (nv.y - ht[s][e].y);
         }
       }
     }
@@ -334,32 +348,38 @@ __global__ void __launch_bounds__(256) append_kernel(AppendArgs a, BuildArgs ba,
     // in the ring (the barrier above published this tile's slots; the host
     // checked that the ring still holds slot t).  The key of a token inside the
     // chunk comes from k_src.
+    if (!early) {
+      double2 hp[kSeg][4], hq[kSeg][4];
+      Raw8<T> kk[kSeg];
 #pragma unroll
-    for (int s = 0; s < (early ? 0 : kSeg); ++s) {
-      const int i = i0 + s;
-      const int64_t t = a.past_len + i - a.n_local;
-      const bool act = i < a.n_q && t >= a.n_init;
-      double part = 0.0;
-      if (act) {
-        const int sp = slot0 + i - (slot0 + i >= a.ring ? a.ring : 0);
+      for (int s = 0; s < kSeg; ++s) {
+        const int ic = min(i0 + s, a.n_q - 1);
+        int64_t t = a.past_len + ic - a.n_local;
+        t = t < 0 ? 0 : t;
+        const int sp = slot0 + ic - (slot0 + ic >= a.ring ? a.ring : 0);
         const int st = sp - a.n_local + (sp < a.n_local ? a.ring : 0);  // n_local < ring
-        const double2* hp = (const double2*)(ring + (int64_t)sp * D);
-        const double2* ht = (const double2*)(ring + (int64_t)st * D);
-        double kt[8];
-        if (t >= a.past_len)
-          load8<T>((const T*)a.k_src + (int64_t)bg * a.kv_head_stride + (t - a.past_len) * D + d0, kt);
-        else
-          load8<T>((const T*)a.k_store + ((int64_t)bg * a.capacity + t) * D + d0, kt);
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
-          const double2 x = hp[e], y = ht[e];
-          part += kt[2 * e] * (x.x - y.x) + kt[2 * e + 1] * (x.y - y.y);
+          hp[s][e] = ((const double2*)(ring + (int64_t)sp * D))[e];
+          hq[s][e] = ((const double2*)(ring + (int64_t)st * D))[e];
         }
+        kk[s] = t >= a.past_len
+                    ? load_raw8<T>((const T*)a.k_src + (int64_t)bg * a.kv_head_stride + (t - a.past_len) * D + d0)
+                    : load_raw8<T>((const T*)a.k_store + ((int64_t)bg * a.capacity + t) * D + d0);
       }
-      part += __shfl_xor(part, 1);  // the two 8-dim halves of the slice
-      if (act && half == 0) {
-        const int st = (int)(t % a.ring);
-        a.rpart[((int64_t)bg * slices + slice) * a.ring + st] = part;
+#pragma unroll
+      for (int s = 0; s < kSeg; ++s) {
+        const int i = i0 + s;
+        const int64_t t = a.past_len + i - a.n_local;
+        const bool act = i < a.n_q && t >= a.n_init;
+        float kt[8];
+        raw8_to_float<T>(kk[s], kt);
+        double p = 0.0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e)
+          p += (double)kt[2 * e] * (hp[s][e].x - hq[s][e].x) + (double)kt[2 * e + 1] * (hp[s][e].y - hq[s][e].y);
+        p += __shfl_xor(p, 1);  // the two 8-dim halves of the slice
+        if (act && half == 0) a.rpart[((int64_t)bg * slices + slice) * a.ring + (int)(t % a.ring)] = p;
       }
     }
   }
@@ -376,7 +396,8 @@ static hipError_t launch_append_d(const AppendArgs& a, const BuildArgs& ba, cons
                                   float* qbar) {
   const dim3 grid(g.n_build + g.n_scan + g.n_copy_per_head * a.batch * a.n_kv_heads);
   const int G = a.n_q_heads / a.n_kv_heads;
-#define INFLLM_APPEND(T, GT) hipLaunchKernelGGL((append_kernel<T, GT, DT>), grid, dim3(256), 0, s, a, ba, g, qbar)
+#define INFLLM_APPEND(T, GT) \
+  hipLaunchKernelGGL((append_kernel<T, GT, DT>), grid, dim3(kThreads), 0, s, a, ba, g, qbar)
   if (a.bf16) {
     switch (G) {
       case 1: INFLLM_APPEND(bf16_t, 1); break;
@@ -404,12 +425,12 @@ hipError_t launch_append(const AppendArgs& a, hipStream_t s, float* qbar, const 
   const int esize = a.bf16 ? 2 : 4;
   g.thin = a.n_q <= kThinMaxQ;
   g.n_scan = a.n_q <= 0 ? 0
-             : g.thin ? (a.batch * a.n_kv_heads * a.head_dim + 255) / 256
+             : g.thin ? (a.batch * a.n_kv_heads * a.head_dim + kThreads - 1) / kThreads
                       : a.batch * a.n_kv_heads * (a.head_dim / 16);
   g.n_copy_per_head = 0;
   if (a.k_src != nullptr && a.n_q > 0) {
     const int vec_per_head = a.n_q * a.head_dim / (16 / esize);
-    g.n_copy_per_head = (vec_per_head + 256 * kCopyPerThread - 1) / (256 * kCopyPerThread);
+    g.n_copy_per_head = (vec_per_head + kThreads * kCopyPerThread - 1) / (kThreads * kCopyPerThread);
   }
   BuildArgs ba;
   if (fused_build != nullptr) ba = *fused_build;
