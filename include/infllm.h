@@ -178,7 +178,12 @@ infllm_status infllm_chunk_attend(const infllm_params* p, const infllm_memory* m
  * workspace and reports the part count; infllm_lse_merge combines them
  * (LSE = log sum_s exp(lse_s), O = sum_s exp(lse_s - LSE) O_s) into out / lse.
  * With one part, infllm_attend_partial writes out and lse directly and
- * infllm_lse_merge must not be called.  Arguments as in infllm_chunk_attend. */
+ * infllm_lse_merge must not be called.  Arguments as in infllm_chunk_attend.
+ * Workspace layout of the partials (rows = batch*Hq*n_q): [n_parts][rows][D]
+ * values, then [n_parts][rows] float32 lse, then for bf16 inputs [n_parts][rows]
+ * int32 exponents e.  Float32 inputs store float32 values; bf16 inputs store each
+ * part's row as fp16 values v with O_s = v * 2^e, e chosen per row so that its
+ * largest magnitude lies in [2^14, 2^15) (11-bit precision relative to it). */
 infllm_status infllm_attend_partial(const infllm_params* p, const infllm_memory* m, const void* q,
                                     int64_t q_head_stride, int32_t n_q, int64_t past_len,
                                     const int32_t* idx, int32_t k, void* out, int64_t out_head_stride,

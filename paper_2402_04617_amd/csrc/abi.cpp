@@ -98,9 +98,26 @@ int64_t max_virtual_keys(const infllm_params* p, int32_t n_q) {
   return (int64_t)p->n_init + (int64_t)p->topk * p->block_size + p->n_local + p->block_size - 1 + n_q;
 }
 
+// Workspace bytes of one part's partial row: fp16 values, lse and exponent for
+// bf16 inputs; float32 values and lse for float32 inputs.
+size_t part_row_bytes(const infllm_params* p) {
+  return p->dtype == INFLLM_BF16 ? (size_t)p->head_dim * 2u + 8u : (size_t)(p->head_dim + 1) * 4u;
+}
+
 size_t attend_ws_bytes(const infllm_params* p, int32_t batch, int32_t n_q, int parts) {
   const int64_t rows = (int64_t)batch * p->n_q_heads * n_q;
-  return (size_t)parts * (size_t)rows * (size_t)(p->head_dim + 1) * 4u;
+  return (size_t)parts * (size_t)rows * part_row_bytes(p);
+}
+
+// Partial arrays inside the workspace: [parts][rows][D] values, then [parts][rows]
+// lse, then (bf16) [parts][rows] exponents.
+void partial_layout(const infllm_params* p, void* workspace, int parts, int64_t rows, void** o, float** lse,
+                    int32_t** ex) {
+  const size_t vbytes = (size_t)parts * (size_t)rows * (size_t)p->head_dim * (p->dtype == INFLLM_BF16 ? 2u : 4u);
+  char* w = (char*)workspace;
+  *o = w;
+  *lse = w ? (float*)(w + vbytes) : nullptr;
+  *ex = (w && p->dtype == INFLLM_BF16) ? (int32_t*)(w + vbytes + (size_t)parts * (size_t)rows * 4u) : nullptr;
 }
 
 size_t qbar_ws_bytes(const infllm_params* p, int32_t batch, int32_t n_q) {
@@ -137,7 +154,7 @@ infllm_status prepare_attend(const infllm_params* p, const infllm_memory* m, con
   // the bf16 kernels address one (sequence, kv head) slice of the store with 32-bit byte offsets
   if (bf16 && (uint64_t)m->capacity * (uint64_t)p->head_dim * 2u > 0xFFFFFFFFull) return INFLLM_E_UNSUPPORTED;
   const int64_t rows = (int64_t)m->batch * p->n_q_heads * n_q;
-  const size_t per_part = rows > 0 ? (size_t)rows * (size_t)(p->head_dim + 1) * 4u : 1;
+  const size_t per_part = rows > 0 ? (size_t)rows * part_row_bytes(p) : 1;
   const int max_parts = (workspace == nullptr) ? 0 : (int)(workspace_bytes / per_part > 4096 ? 4096 : workspace_bytes / per_part);
   const int parts = attend_choose_parts(bf16, m->batch, p->n_q_heads, p->n_kv_heads, n_q, n_sel, (int)n_virtual,
                                         max_parts);
@@ -170,8 +187,7 @@ infllm_status prepare_attend(const infllm_params* p, const infllm_memory* m, con
   a->out = out;
   a->lse = lse;
   a->parts = parts;
-  a->part_o = (float*)workspace;
-  a->part_lse = workspace ? (float*)((char*)workspace + (size_t)parts * rows * p->head_dim * 4u) : nullptr;
+  partial_layout(p, workspace, parts, rows, &a->part_o, &a->part_lse, &a->part_exp);
   a->bf16 = bf16;
   return INFLLM_OK;
 }
@@ -186,8 +202,13 @@ MergeArgs merge_args(const infllm_params* p, int32_t batch, int32_t n_q, int32_t
   ma.n_q = n_q;
   ma.n_q_heads = p->n_q_heads;
   ma.out_head_stride = out_head_stride;
-  ma.part_o = (const float*)workspace;
-  ma.part_lse = (const float*)((const char*)workspace + (size_t)n_parts * rows * p->head_dim * 4u);
+  void* po;
+  float* pl;
+  int32_t* pe;
+  partial_layout(p, const_cast<void*>(workspace), n_parts, rows, &po, &pl, &pe);
+  ma.part_o = po;
+  ma.part_lse = pl;
+  ma.part_exp = pe;
   ma.out = out;
   ma.lse = lse;
   ma.bf16 = p->dtype == INFLLM_BF16;

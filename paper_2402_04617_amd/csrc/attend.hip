@@ -111,7 +111,7 @@ __global__ void __launch_bounds__(256) attend_f32_kernel(AttendArgs a) {
     if (a.lse != nullptr && sub == 0) a.lse[grow] = lse_v;
   } else {
     const int64_t rows_total = (int64_t)a.batch * a.n_q_heads * geo.n_q;
-    float* op = a.part_o + ((int64_t)part * rows_total + grow) * D;
+    float* op = (float*)a.part_o + ((int64_t)part * rows_total + grow) * D;
 #pragma unroll
     for (int e = 0; e < DPT; ++e) op[sub * DPT + e] = o[e] * inv;
     if (sub == 0) a.part_lse[(int64_t)part * rows_total + grow] = lse_v;

@@ -114,6 +114,7 @@ __global__ void __launch_bounds__(64 * kDecodeWaves) attend_decode_kernel(Attend
   __shared__ float cm[kDecodeWaves][G], cl[kDecodeWaves][G];
   __shared__ __attribute__((aligned(16))) float co[kDecodeWaves][G][D];
   __shared__ int32_t sidx[kDecodeMaxSel];
+  __shared__ float fo[G][D];  // this part's output rows before the fp16 write
 
   const StepGeom& geo = a.geom;
   const int part = blockIdx.x % a.parts;
@@ -265,7 +266,9 @@ __global__ void __launch_bounds__(64 * kDecodeWaves) attend_decode_kernel(Attend
   }
   __syncthreads();
 
-  // Combine the waves (exp2 domain) and write this workgroup's part.
+  // Combine the waves (exp2 domain).  One part: write the bf16 output directly.
+  // Several: stage the part's rows in LDS, then each wave writes whole rows as
+  // fp16 scaled by their per-row exponent.
   const int64_t rows_total = (int64_t)a.batch * a.n_q_heads;  // n_q == 1
   for (int e = tid; e < G * D; e += 64 * kDecodeWaves) {
     const int h = e / D, d = e - h * D;
@@ -283,11 +286,8 @@ __global__ void __launch_bounds__(64 * kDecodeWaves) attend_decode_kernel(Attend
     }
     const float o = L > 0.f ? O / L : 0.f;
     const int64_t grow_ = (int64_t)b * a.n_q_heads + g * G + h;
-    if (a.parts == 1) {
-      ((bf16_t*)a.out)[grow_ * a.out_head_stride + d] = f32_to_bf16(o);
-    } else {
-      a.part_o[((int64_t)part * rows_total + grow_) * D + d] = o;
-    }
+    if (a.parts == 1) ((bf16_t*)a.out)[grow_ * a.out_head_stride + d] = f32_to_bf16(o);
+    else fo[h][d] = o;
     if (d == 0) {
       const float lse_v = L > 0.f ? (M + __log2f(L)) * 0.6931471805599453f : -__builtin_inff();
       if (a.parts == 1) {
@@ -296,6 +296,29 @@ __global__ void __launch_bounds__(64 * kDecodeWaves) attend_decode_kernel(Attend
         a.part_lse[(int64_t)part * rows_total + grow_] = lse_v;
       }
     }
+  }
+  if (a.parts == 1) return;
+  __syncthreads();
+  constexpr int PL = D / 64;  // values per lane of a row
+  for (int h = wave; h < G; h += kDecodeWaves) {
+    float v[PL];
+    float amax = 0.f;
+#pragma unroll
+    for (int j = 0; j < PL; ++j) {
+      v[j] = fo[h][lane * PL + j];
+      amax = fmaxf(amax, fabsf(v[j]));
+    }
+    const int ex = partial_row_exponent(wave_max(amax));
+    const float sc = exp2_int(-ex);
+    const int64_t grow_ = (int64_t)b * a.n_q_heads + g * G + h;
+    uint16_t* op = (uint16_t*)a.part_o + ((int64_t)part * rows_total + grow_) * D + lane * PL;
+    if constexpr (PL == 2) {
+      *(uint32_t*)op = pack_f16x2(v[0] * sc, v[1] * sc);
+    } else {
+      const _Float16 hv = (_Float16)(v[0] * sc);
+      *op = __builtin_bit_cast(uint16_t, hv);
+    }
+    if (lane == 0) a.part_exp[(int64_t)part * rows_total + grow_] = ex;
   }
 }
 

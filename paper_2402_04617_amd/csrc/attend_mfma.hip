@@ -621,18 +621,33 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
     }
     if (a.lse != nullptr && gsel == 0) a.lse[grow] = lse_v;
   } else {
+    // fp16 partial row scaled by 2^-e (both lane halves of the row agree on e)
     const int64_t rows_total = (int64_t)a.batch * a.n_q_heads * geo.n_q;
-    float* op = a.part_o + ((int64_t)part * rows_total + grow) * D;
+    float amax = 0.f;
+#pragma unroll
+    for (int db = 0; db < DBLK; ++db)
+#pragma unroll
+      for (int j = 0; j < 16; ++j) amax = fmaxf(amax, fabsf(oacc[db][j]));
+    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(amax), __float_as_uint(amax), false, false);
+    amax = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * inv;
+    const int ex = partial_row_exponent(amax);
+    const float sc = inv * exp2_int(-ex);
+    bf16_t* op = (bf16_t*)a.part_o + ((int64_t)part * rows_total + grow) * D;
 #pragma unroll
     for (int db = 0; db < DBLK; ++db) {
 #pragma unroll
       for (int jq = 0; jq < 4; ++jq) {
         const int d = 32 * db + 8 * jq + 4 * gsel;
-        *(float4*)(op + d) = make_float4(oacc[db][4 * jq] * inv, oacc[db][4 * jq + 1] * inv,
-                                         oacc[db][4 * jq + 2] * inv, oacc[db][4 * jq + 3] * inv);
+        uint2 w;
+        w.x = pack_f16x2(oacc[db][4 * jq] * sc, oacc[db][4 * jq + 1] * sc);
+        w.y = pack_f16x2(oacc[db][4 * jq + 2] * sc, oacc[db][4 * jq + 3] * sc);
+        *(uint2*)(op + d) = w;
       }
     }
-    if (gsel == 0) a.part_lse[(int64_t)part * rows_total + grow] = lse_v;
+    if (gsel == 0) {
+      a.part_lse[(int64_t)part * rows_total + grow] = lse_v;
+      a.part_exp[(int64_t)part * rows_total + grow] = ex;
+    }
   }
 }
 

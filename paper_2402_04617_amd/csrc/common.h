@@ -78,6 +78,26 @@ __device__ __forceinline__ int xcd_logical_block(int linear, int total) {
   return (linear % kNumXcd) * per + linear / kNumXcd;
 }
 
+// Split-key partial rows.  A part's normalised output row O_s (a convex
+// combination of value rows) is stored, for bfloat16 inputs, as fp16 values
+// O_s * 2^-e with one exponent e per row chosen so that the row's largest
+// magnitude lands in [2^14, 2^15): every element keeps fp16's 11-bit precision
+// relative to that maximum, at half the bytes of float32.  Float32 inputs keep
+// float32 rows.
+__device__ __forceinline__ int partial_row_exponent(float row_absmax) {
+  if (!(row_absmax > 0.f) || row_absmax == __builtin_inff()) return 0;  // zero, NaN or inf: unscaled
+  const int eb = (int)((__float_as_uint(row_absmax) >> 23) & 255u);
+  const int e = eb - 127 - 14;
+  return e < -100 ? -100 : (e > 100 ? 100 : e);
+}
+__device__ __forceinline__ float exp2_int(int e) { return __uint_as_float((uint32_t)(127 + e) << 23); }  // |e| <= 100
+__device__ __forceinline__ uint32_t pack_f16x2(float lo, float hi) {
+  const _Float16 a = (_Float16)lo, b = (_Float16)hi;  // round to nearest even
+  return (uint32_t)__builtin_bit_cast(uint16_t, a) | ((uint32_t)__builtin_bit_cast(uint16_t, b) << 16);
+}
+__device__ __forceinline__ float f16_lo(uint32_t w) { return (float)__builtin_bit_cast(_Float16, (uint16_t)(w & 0xFFFFu)); }
+__device__ __forceinline__ float f16_hi(uint32_t w) { return (float)__builtin_bit_cast(_Float16, (uint16_t)(w >> 16)); }
+
 __device__ __forceinline__ float wave_max(float x) {
 #pragma unroll
   for (int o = 32; o > 0; o >>= 1) x = fmaxf(x, __shfl_xor(x, o));

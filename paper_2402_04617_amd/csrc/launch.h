@@ -82,8 +82,11 @@ struct AttendArgs {
   const int32_t* idx;
   void* out;     // final output (one part)
   float* lse;    // nullable
-  float* part_o;    // [parts][rows][D] fp32
-  float* part_lse;  // [parts][rows]
+  // Split-key partials (parts > 1), see the layout in common.h: float32 rows for
+  // float32 inputs; for bf16 inputs fp16 rows scaled by 2^-part_exp[row].
+  void* part_o;        // [parts][rows][D]
+  float* part_lse;     // [parts][rows]
+  int32_t* part_exp;   // [parts][rows] (bf16 only)
   int parts;
   bool bf16;
 };
@@ -95,8 +98,9 @@ hipError_t launch_attend(const AttendArgs& a, hipStream_t s);
 struct MergeArgs {
   int rows, head_dim, parts, n_q, n_q_heads;
   int64_t out_head_stride;
-  const float* part_o;
+  const void* part_o;
   const float* part_lse;
+  const int32_t* part_exp;
   void* out;
   float* lse;
   bool bf16;

@@ -88,12 +88,13 @@ def test_workspace_bytes(L):
     p = P()
     ws = L.infllm_workspace_bytes(ctypes.byref(p), 1, 512)
     rows = 32 * 512
-    assert ws >= 2 * rows * 129 * 4 and ws % 256 == 0
+    row_bytes = 2 * 128 + 8  # bf16 inputs: an fp16 partial row, its lse and its exponent
+    assert ws >= 2 * rows * row_bytes and ws % 256 == 0
     # decode: room for the most key parts any batch can use, one per 256 keys of the bounded key
     # count l_I + k_m*l_bs + l_L + l_bs - 1 + 1
     wsd = L.infllm_workspace_bytes(ctypes.byref(p), 16, 1)
     nv = 128 + 32 * 128 + 4096 + 127 + 1
-    assert wsd >= (nv // 256) * 16 * 32 * 129 * 4
+    assert wsd >= (nv // 256) * 16 * 32 * row_bytes
 
 
 def mem(**kw):
