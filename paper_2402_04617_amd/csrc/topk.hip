@@ -5,6 +5,8 @@
 // and how many keys equal to T to keep; a pass in index order then keeps every
 // key > T and the lowest-indexed keys == T, writing survivors with a block-wide
 // ballot scan so the output is ascending by construction.  Deterministic.
+// Rows of up to kThreads*kMaxPer keys keep their keys in registers for all
+// passes (radix_select_reg); longer rows re-read them from memory.
 #include "launch.h"
 
 namespace infllm {
@@ -12,6 +14,7 @@ namespace {
 
 constexpr int kThreads = 512;
 constexpr int kWaves = kThreads / 64;
+constexpr int kMaxPer = 16;  // most keys per thread held in registers
 
 __device__ __forceinline__ uint32_t order_key(float x) {
   if (x != x) return 0u;        // NaN below everything
@@ -40,18 +43,11 @@ __device__ __forceinline__ int block_scan(bool pred, int* wave_tot, int* total) 
   return off + pre;
 }
 
-__global__ void __launch_bounds__(kThreads) topk_kernel(const float* __restrict__ scores, int n, int k,
-                                                        int32_t* __restrict__ idx) {
-  const int row = blockIdx.x;
-  const float* s = scores + (int64_t)row * n;
-  int32_t* out = idx + (int64_t)row * k;
-  const int k_eff = min(k, n);
-  for (int j = k_eff + threadIdx.x; j < k; j += kThreads) out[j] = -1;
-  if (k_eff == 0) return;
-
+// Radix-select path (see above); s, out: this row.
+__device__ void radix_select(const float* __restrict__ s, int n, int k_eff, int32_t* __restrict__ out,
+                             int* wave_tot) {
   __shared__ uint32_t hist[256];
   __shared__ uint32_t sh_digit, sh_remaining;
-  __shared__ int wave_tot[kWaves];
 
   const bool all = (k_eff == n);
   uint32_t thr = 0;
@@ -114,12 +110,158 @@ __global__ void __launch_bounds__(kThreads) topk_kernel(const float* __restrict_
   }
 }
 
+// Exclusive ranks, in index order, of the set predicates of PER strided tiles
+// (thread t holds element t + j*kThreads of tile j): per-(tile, wave) ballot
+// counts through LDS, two barriers in all.
+template <int PER>
+__device__ __forceinline__ void tiled_scan(const bool (&pred)[PER], int (&rank)[PER], int* total) {
+  __shared__ int cnt[PER][kWaves];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const unsigned long long below = (1ull << lane) - 1ull;
+  unsigned long long m[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    m[j] = __ballot(pred[j]);
+    if (lane == 0) cnt[j][wave] = __popcll(m[j]);
+  }
+  __syncthreads();
+  int base = 0;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    int before = 0, tot = 0;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) {
+      const int c = cnt[j][w];
+      before += (w < wave) ? c : 0;
+      tot += c;
+    }
+    rank[j] = base + before + __popcll(m[j] & below);
+    base += tot;
+  }
+  *total = base;
+  __syncthreads();  // cnt may be written again by the next scan
+}
+
+// Common path: the same radix select with the row's keys held in registers
+// (thread t: keys t, t + kThreads, ...; read once), the histogram of a pass
+// built with one atomic per wave where the wave's live digits agree (typical of
+// the leading digits), double-buffered histograms (two barriers per pass), and
+// a final pass whose index-order ranks come from one tiled ballot scan (two
+// when only some keys equal to T are kept).
+template <int PER>
+__device__ void radix_select_reg(const float* __restrict__ s, int n, int k_eff, int32_t* __restrict__ out) {
+  __shared__ uint32_t hist[2][256];
+  __shared__ uint32_t sh_digit, sh_remaining, sh_eq_total;
+  const int t = threadIdx.x, lane = t & 63;
+  uint32_t key[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) key[j] = order_key(s[min(t + j * kThreads, n - 1)]);
+  for (int j = t; j < 256; j += kThreads) hist[0][j] = 0;
+  __syncthreads();
+  uint32_t prefix = 0, mask = 0;
+  int remaining = k_eff;
+  uint32_t eq_total = 0;
+  for (int pass = 0; pass < 4; ++pass) {
+    const int shift = 24 - 8 * pass;
+    uint32_t* h = hist[pass & 1];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) {
+      const bool live = t + j * kThreads < n && (key[j] & mask) == prefix;
+      const uint32_t d = (key[j] >> shift) & 255u;
+      const unsigned long long lm = __ballot(live);
+      if (lm == 0) continue;
+      const uint32_t d0 = (uint32_t)__builtin_amdgcn_readlane((int)d, __builtin_ctzll(lm));
+      if (__ballot(live && d != d0) == 0) {
+        if (lane == 0) atomicAdd(&h[d0], (uint32_t)__popcll(lm));
+      } else if (live) {
+        atomicAdd(&h[d], 1u);
+      }
+    }
+    __syncthreads();
+    if (t < 64) {
+      // lane l owns bins 4l..4l+3; suffix sums give counts of keys >= each bin
+      const uint32_t h0 = h[4 * t], h1 = h[4 * t + 1], h2 = h[4 * t + 2], h3 = h[4 * t + 3];
+      const uint32_t own = h0 + h1 + h2 + h3;
+      uint32_t suf = own;  // inclusive suffix over lanes >= l
+#pragma unroll
+      for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t x = __shfl_down(suf, o);
+        suf += (t + o < 64) ? x : 0u;
+      }
+      const uint32_t above = suf - own;  // keys in bins > 4l+3
+      const uint32_t ge3 = above + h3, ge2 = ge3 + h2, ge1 = ge2 + h1, ge0 = ge1 + h0;
+      const uint32_t rem = (uint32_t)remaining;
+      // the digit d* with count(>= d*) >= rem > count(> d*)
+      if (ge3 >= rem && above < rem) { sh_digit = 4 * t + 3; sh_remaining = rem - above; sh_eq_total = h3; }
+      if (ge2 >= rem && ge3 < rem) { sh_digit = 4 * t + 2; sh_remaining = rem - ge3; sh_eq_total = h2; }
+      if (ge1 >= rem && ge2 < rem) { sh_digit = 4 * t + 1; sh_remaining = rem - ge2; sh_eq_total = h1; }
+      if (ge0 >= rem && ge1 < rem) { sh_digit = 4 * t; sh_remaining = rem - ge1; sh_eq_total = h0; }
+    } else {
+      for (int j = t - 64; j < 256; j += kThreads - 64) hist[(pass + 1) & 1][j] = 0;
+    }
+    __syncthreads();
+    prefix |= sh_digit << shift;
+    mask |= 255u << shift;
+    remaining = (int)sh_remaining;
+    eq_total = sh_eq_total;
+  }
+  const uint32_t thr = prefix;
+  // Final pass: ranks in index order (tile j = indices [j*kThreads, (j+1)*kThreads))
+  // from per-(tile, wave) ballot counts, one barrier per scan.
+  bool keep[PER];
+  if ((uint32_t)remaining == eq_total) {
+#pragma unroll
+    for (int j = 0; j < PER; ++j) keep[j] = t + j * kThreads < n && key[j] >= thr;
+  } else {
+    bool eq[PER];
+#pragma unroll
+    for (int j = 0; j < PER; ++j) eq[j] = t + j * kThreads < n && key[j] == thr;
+    int eq_rank[PER], tot;
+    tiled_scan<PER>(eq, eq_rank, &tot);
+#pragma unroll
+    for (int j = 0; j < PER; ++j)
+      keep[j] = t + j * kThreads < n && (key[j] > thr || (eq[j] && eq_rank[j] < remaining));
+  }
+  int pos[PER], tot;
+  tiled_scan<PER>(keep, pos, &tot);
+#pragma unroll
+  for (int j = 0; j < PER; ++j)
+    if (keep[j] && pos[j] < k_eff) out[pos[j]] = t + j * kThreads;
+}
+
+// PER: keys per thread of the common path (0: radix select only).
+template <int PER>
+__global__ void __launch_bounds__(kThreads) topk_kernel(const float* __restrict__ scores, int n, int k,
+                                                        int32_t* __restrict__ idx) {
+  const int row = blockIdx.x;
+  const float* s = scores + (int64_t)row * n;
+  int32_t* out = idx + (int64_t)row * k;
+  const int k_eff = min(k, n);
+  for (int j = k_eff + threadIdx.x; j < k; j += kThreads) out[j] = -1;
+  if (k_eff == 0) return;
+  __shared__ int wave_tot[kWaves];
+  if constexpr (PER > 0) {
+    if (k_eff < n) {
+      radix_select_reg<PER>(s, n, k_eff, out);
+      return;
+    }
+  }
+  radix_select(s, n, k_eff, out, wave_tot);
+}
+
 }  // namespace
 
 hipError_t launch_select_topk(int rows, const float* scores, int n_units, int k, int32_t* idx,
                               hipStream_t s) {
   if (rows == 0 || k == 0) return hipSuccess;
-  hipLaunchKernelGGL(topk_kernel, dim3(rows), dim3(kThreads), 0, s, scores, n_units, k, idx);
+  const int per = (n_units + kThreads - 1) / kThreads;
+  const dim3 grid(rows), block(kThreads);
+  if (per <= 1) hipLaunchKernelGGL(topk_kernel<1>, grid, block, 0, s, scores, n_units, k, idx);
+  else if (per <= 2) hipLaunchKernelGGL(topk_kernel<2>, grid, block, 0, s, scores, n_units, k, idx);
+  else if (per <= 4) hipLaunchKernelGGL(topk_kernel<4>, grid, block, 0, s, scores, n_units, k, idx);
+  else if (per <= 8) hipLaunchKernelGGL(topk_kernel<8>, grid, block, 0, s, scores, n_units, k, idx);
+  else if (per <= kMaxPer) hipLaunchKernelGGL(topk_kernel<kMaxPer>, grid, block, 0, s, scores, n_units, k, idx);
+  else hipLaunchKernelGGL(topk_kernel<0>, grid, block, 0, s, scores, n_units, k, idx);
   return hipGetLastError();
 }
 

@@ -30,7 +30,8 @@ def rand_inputs(rng, Hq, Hkv, S, D, dtype, qk_std=None, B=1):
 
 # ------------------------------------------------------------------ a5: top-k
 @pytest.mark.parametrize("n,k", [(0, 4), (1, 4), (5, 5), (7, 3), (100, 32), (987, 32), (8155, 32),
-                                 (9000, 64), (300, 1), (50, 0), (4096, 100)])
+                                 (9000, 64), (300, 1), (50, 0), (4096, 100), (600, 256), (16384, 32),
+                                 (20000, 32), (2000, 300), (3000, 64), (700, 65)])
 def test_select_topk_bit_exact(n, k):
     rng = np.random.default_rng(n * 131 + k)
     rows = 8
