@@ -37,9 +37,9 @@ PEAK_HBM_GBS = 8000.0
 # --copy-calibration 1024`.  Valid only for the attention source it was taken on (sha256 below);
 # reported as null once that file changes.
 ATTN_SRC = os.path.join(ROOT, "paper_2402_04617_amd", "csrc", "attend_mfma.hip")
-ATTN_TRAFFIC = {"src_sha256": "90782a63b156b11502f600b78746edc06358618a85d56715b1017137c4625604",
-                "fetch_kib": 19964.19, "write_kib": 33024.0,  # per attention dispatch (768 dispatches)
-                "copy_fetch": 524300.06 / 1048576.0,  # FETCH_SIZE KiB per KiB read by the copy
+ATTN_TRAFFIC = {"src_sha256": "c0c8ff0b35f49e24b9743b3f377bec50fc244858c5630bb9cab5a69ff2de3a12",
+                "fetch_kib": 19898.07, "write_kib": 16896.0,  # per attention dispatch (768 dispatches)
+                "copy_fetch": 524300.13 / 1048576.0,  # FETCH_SIZE KiB per KiB read by the copy
                 "copy_write": 1048576.0 / 1048576.0}  # WRITE_SIZE KiB per KiB written by the copy
 
 
@@ -51,6 +51,23 @@ def attention_traffic_bytes():
         if hashlib.sha256(f.read()).hexdigest() != t["src_sha256"]:
             return None
     return 1024.0 * (t["fetch_kib"] / t["copy_fetch"] + t["write_kib"] / t["copy_write"])
+
+
+def measured_peaks():
+    """Peaks measured on this GPU by the library's probe program (a child process): bf16 MFMA loop,
+    streaming HBM read and copy.  None when the probe has not been built or fails."""
+    import subprocess
+    exe = os.path.join(ROOT, "paper_2402_04617_amd", "infllm_peaks")
+    if not os.path.exists(exe):
+        return None
+    try:
+        r = subprocess.run([exe], capture_output=True, text=True, timeout=120)
+    except subprocess.TimeoutExpired:
+        return None
+    if r.returncode != 0:
+        log(f"peak probe failed: {r.stderr.strip()}")
+        return None
+    return json.loads(r.stdout.strip().splitlines()[-1])
 
 
 def copy_calibration(mib, torch, reps=3):
@@ -103,17 +120,19 @@ def attention_flops(wl, steps):
 def attention_bytes(wl, steps, parts):
     """Algorithmic HBM bytes of the attention launches of a pass: each query row read once, each
     visible context key and value read once per kv head, and the output written once per part
-    (float32 partial rows plus LSE when a launch splits the keys, the bf16 output otherwise)."""
+    (partial rows when a launch splits the keys, the bf16 output otherwise)."""
     from paper_2402_04617_amd import infllm as F
     p = params_of(wl)
     e = 2 if wl.dtype == "bf16" else 4
+    # a split-key partial row: fp16 values + lse + exponent (bf16), float32 values + lse (f32)
+    part_row = 2 * wl.head_dim + 8 if wl.dtype == "bf16" else 4 * (wl.head_dim + 1)
     total = 0
     for (past, n), np_ in zip(steps, parts):
         n_init, n_units, local_begin = F.infllm_partition(p, past)
         keys = n_init + min(wl.topk, n_units) * wl.block_size + (past - local_begin) + n
         rows = wl.batch * wl.n_q_heads * n
         total += rows * wl.head_dim * e + 2 * wl.batch * wl.n_kv_heads * keys * wl.head_dim * e
-        total += np_ * rows * (wl.head_dim + 1) * 4 if np_ > 1 else rows * wl.head_dim * e
+        total += np_ * rows * part_row if np_ > 1 else rows * wl.head_dim * e
     return total
 
 
@@ -361,6 +380,11 @@ def main():
                      "launches_per_step": att["launches"]},
         "extra": extra,
     }
+    peaks = measured_peaks()
+    if peaks is not None:
+        line["roofline"]["measured_peaks"] = peaks
+        line["roofline"]["frac_of_measured"] = achieved / peaks["mfma_bf16_tflops"]
+        log(f"measured peaks: {peaks}")
     if not args.no_cpu_baseline:
         t = time.time()
         line["cpu_baseline"] = cpu_baseline(synth)

@@ -15,6 +15,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libinfllm.so")
+PEAKS = os.path.join(PKG, "infllm_peaks")
 
 SOURCES = ["abi.cpp", "append.hip", "build_units.hip", "score.hip", "topk.hip", "attend_mfma.hip",
            "attend.hip", "attend_decode.hip", "merge.hip"]
@@ -57,6 +58,12 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
     if r.returncode != 0:
         raise RuntimeError("link failed:\n" + r.stdout + r.stderr)
     os.replace(tmp, LIB)
+    # the measured-peak probe that bench.py runs next to the library (a separate program)
+    cmd = [hipcc, *FLAGS, os.path.join(PKG, "probes", "peaks.hip"), "-o", PEAKS + ".tmp"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("hipcc failed on probes/peaks.hip:\n" + r.stdout + r.stderr)
+    os.replace(PEAKS + ".tmp", PEAKS)
     return LIB
 
 
