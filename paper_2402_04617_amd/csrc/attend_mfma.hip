@@ -600,31 +600,21 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
     pv((t - t_begin) % NBUF, pb);
   }
 
-  // Epilogue: combine the two lane halves' partial sums; write O and lse.
+  // Epilogue: combine the two lane halves' partial sums; write O (bf16, one part)
+  // or the scaled fp16 partial row and lse.  The accumulator layout gives each
+  // lane 8-byte pieces of its row; they are staged through LDS (the tile buffers
+  // are free once every wave has passed the barrier below) so that each store
+  // moves 16 contiguous bytes and a wave's store covers four whole rows.
   const float l_tot = l_run + __shfl_xor(l_run, 32);
   const float inv = l_tot > 0.f ? 1.f / l_tot : 0.f;
   const float lse_v = (m_run == -__builtin_inff() || l_tot <= 0.f)
                           ? -__builtin_inff()
                           : (m_run + __log2f(l_tot)) * 0.6931471805599453f;
-  if (!row_ok) return;
-  const int64_t grow = ((int64_t)(b * a.n_q_heads + qh)) * geo.n_q + qi;
-  if (a.parts == 1) {
-    bf16_t* op = (bf16_t*)a.out + (int64_t)(b * a.n_q_heads + qh) * a.out_head_stride + (int64_t)qi * D;
-#pragma unroll
-    for (int db = 0; db < DBLK; ++db) {
-#pragma unroll
-      for (int jq = 0; jq < 4; ++jq) {
-        const int d = 32 * db + 8 * jq + 4 * gsel;
-        uint2 w;
-        w.x = (uint32_t)f32_to_bf16(oacc[db][4 * jq] * inv) | ((uint32_t)f32_to_bf16(oacc[db][4 * jq + 1] * inv) << 16);
-        w.y = (uint32_t)f32_to_bf16(oacc[db][4 * jq + 2] * inv) | ((uint32_t)f32_to_bf16(oacc[db][4 * jq + 3] * inv) << 16);
-        *(uint2*)(op + d) = w;
-      }
-    }
-    if (a.lse != nullptr && gsel == 0) a.lse[grow] = lse_v;
-  } else {
+  const bool one_part = a.parts == 1;
+  float sc = inv;
+  int ex = 0;
+  if (!one_part) {
     // fp16 partial row scaled by 2^-e (both lane halves of the row agree on e)
-    const int64_t rows_total = (int64_t)a.batch * a.n_q_heads * geo.n_q;
     float amax = 0.f;
 #pragma unroll
     for (int db = 0; db < DBLK; ++db)
@@ -632,23 +622,64 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
       for (int j = 0; j < 16; ++j) amax = fmaxf(amax, fabsf(oacc[db][j]));
     const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(amax), __float_as_uint(amax), false, false);
     amax = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * inv;
-    const int ex = partial_row_exponent(amax);
-    const float sc = inv * exp2_int(-ex);
-    bf16_t* op = (bf16_t*)a.part_o + ((int64_t)part * rows_total + grow) * D;
+    ex = partial_row_exponent(amax);
+    sc = inv * exp2_int(-ex);
+  }
+  constexpr int kRowBytes = D * 2;
+  constexpr int kStageRow = kRowBytes + 16;  // padded: the 32 rows of a wave spread over the LDS banks
+  static_assert(NWAVE * 32 * kStageRow <= (int)sizeof(sm.k) + (int)sizeof(sm.v), "staging fits the tile buffers");
+  __syncthreads();  // every wave is done with the tile buffers
+  {
+    INFLLM_LDS char* stage = (INFLLM_LDS char*)(INFLLM_LDS bf16_t*)sm.k[0] + wave * 32 * kStageRow;
 #pragma unroll
     for (int db = 0; db < DBLK; ++db) {
 #pragma unroll
       for (int jq = 0; jq < 4; ++jq) {
         const int d = 32 * db + 8 * jq + 4 * gsel;
-        uint2 w;
-        w.x = pack_f16x2(oacc[db][4 * jq] * sc, oacc[db][4 * jq + 1] * sc);
-        w.y = pack_f16x2(oacc[db][4 * jq + 2] * sc, oacc[db][4 * jq + 3] * sc);
-        *(uint2*)(op + d) = w;
+        const float o0 = oacc[db][4 * jq] * sc, o1 = oacc[db][4 * jq + 1] * sc;
+        const float o2 = oacc[db][4 * jq + 2] * sc, o3 = oacc[db][4 * jq + 3] * sc;
+        u32x2 w;
+        if (one_part) {
+          w[0] = (uint32_t)f32_to_bf16(o0) | ((uint32_t)f32_to_bf16(o1) << 16);
+          w[1] = (uint32_t)f32_to_bf16(o2) | ((uint32_t)f32_to_bf16(o3) << 16);
+        } else {
+          w[0] = pack_f16x2(o0, o1);
+          w[1] = pack_f16x2(o2, o3);
+        }
+        *(INFLLM_LDS u32x2*)(stage + n * kStageRow + d * 2) = w;
       }
     }
-    if (gsel == 0) {
+  }
+  if (row_ok && gsel == 0) {
+    const int64_t grow = ((int64_t)(b * a.n_q_heads + qh)) * geo.n_q + qi;
+    if (one_part) {
+      if (a.lse != nullptr) a.lse[grow] = lse_v;
+    } else {
+      const int64_t rows_total = (int64_t)a.batch * a.n_q_heads * geo.n_q;
       a.part_lse[(int64_t)part * rows_total + grow] = lse_v;
       a.part_exp[(int64_t)part * rows_total + grow] = ex;
+    }
+  }
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront", "local");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront", "local");
+  {
+    constexpr int CPR = kRowBytes / 16;  // 16-byte chunks per row
+    const INFLLM_LDS char* stage = (const INFLLM_LDS char*)(const INFLLM_LDS bf16_t*)sm.k[0] + wave * 32 * kStageRow;
+    const int64_t rows_total = (int64_t)a.batch * a.n_q_heads * geo.n_q;
+#pragma unroll
+    for (int k = 0; k < 32 * CPR / 64; ++k) {
+      const int c = 64 * k + lane, r = c / CPR, ch = c % CPR;
+      const int row = rt * ROWS_WG + wave * 32 + r;
+      if (row >= R) continue;
+      const u32x4 w = *(const INFLLM_LDS u32x4*)(stage + r * kStageRow + ch * 16);
+      const int ri = row / G, rh = g * G + (row - ri * G);
+      char* dst;
+      if (one_part)
+        dst = (char*)a.out + ((int64_t)(b * a.n_q_heads + rh) * a.out_head_stride + (int64_t)ri * D) * 2;
+      else
+        dst = (char*)a.part_o + ((int64_t)part * rows_total + (int64_t)(b * a.n_q_heads + rh) * geo.n_q + ri) * kRowBytes;
+      *(u32x4*)(dst + ch * 16) = w;
     }
   }
 }
