@@ -79,12 +79,14 @@ __device__ __forceinline__ int tile_off(int r, int g) { return r * D + 8 * (g ^ 
 
 constexpr int NBUF = 3;         // K and V tile buffers
 constexpr int kRunTable = 1024;  // run starts kept in LDS for the part's tiles
+constexpr int kSelLds = 1024;    // lookup entries kept in LDS
 
 template <int D>
 struct Smem {
   bf16_t k[NBUF][KB * D];
   bf16_t v[NBUF][KB * D];
   int64_t runs[kRunTable];  // run start of tile t_begin + i (see tile_run_start)
+  int32_t sidx[kSelLds];    // the lookup row (its first kSelLds entries)
   uint8_t kvalid[NBUF][KB];
 };
 
@@ -147,15 +149,16 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
   const bf16_t* kbase = (const bf16_t*)a.k_store + (int64_t)bg * a.capacity * D;
   const bf16_t* vbase = (const bf16_t*)a.v_store + (int64_t)bg * a.capacity * D;
 
-  // Any skipped (out-of-range) unit entry?  Then every tile takes the per-key
-  // gather path and the validity mask.
-  bool has_invalid;
-  {
-    bool bad = false;
-    for (int u = lane; u < geo.n_sel; u += 64) bad |= (idx_row[u] < 0 || idx_row[u] >= geo.n_units);
-    has_invalid = __ballot(bad) != 0;
+  // The lookup row goes to LDS (run starts then read LDS, not global memory) in
+  // the same round trip as the Q rows; one barrier publishes it together with
+  // the check for skipped (out-of-range) entries, which send every tile through
+  // the per-key gather path and the validity mask.
+  bool bad = false;
+  for (int u = tid; u < geo.n_sel; u += 64 * NWAVE) {
+    const int x = idx_row[u];
+    if (u < kSelLds) sm.sidx[u] = x;
+    bad |= (x < 0 || x >= geo.n_units);
   }
-
   // Q rows of this wave as the B operand (8 bf16 per lane per k-step).
   bf16x8 qreg[KSTEPS];
   {
@@ -166,6 +169,7 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
       qreg[s] = __builtin_bit_cast(bf16x8, raw);
     }
   }
+  const bool has_invalid = __syncthreads_or(bad) != 0;
 
   // Direct loads: instruction j of wave w fills LDS granules [(NI*w + j)*64, +64)
   // of the tile, lane l writing granule slot l; that slot belongs to tile row
@@ -189,7 +193,7 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
     if (w + KB > sel_len) return -1;
     const int u = w / geo.block_size;
     if ((w + KB - 1) / geo.block_size != u) return -1;
-    const int bu = idx_row[u];
+    const int bu = u < kSelLds ? sm.sidx[u] : idx_row[u];
     return (int64_t)geo.unit_base + (int64_t)bu * geo.block_size + (w - u * geo.block_size);
   };
   auto uniform64 = [](int64_t x) -> int64_t {
