@@ -37,8 +37,8 @@ PEAK_HBM_GBS = 8000.0
 # --copy-calibration 1024`.  Valid only for the attention source it was taken on (sha256 below);
 # reported as null once that file changes.
 ATTN_SRC = os.path.join(ROOT, "paper_2402_04617_amd", "csrc", "attend_mfma.hip")
-ATTN_TRAFFIC = {"src_sha256": "c0c8ff0b35f49e24b9743b3f377bec50fc244858c5630bb9cab5a69ff2de3a12",
-                "fetch_kib": 19898.07, "write_kib": 16896.0,  # per attention dispatch (768 dispatches)
+ATTN_TRAFFIC = {"src_sha256": "9a04b4ecc0c366b54266c09b4cceaf67ee83788032abf51acc8cf395f946b39a",
+                "fetch_kib": 19935.20, "write_kib": 16896.0,  # per attention dispatch (768 dispatches)
                 "copy_fetch": 524300.13 / 1048576.0,  # FETCH_SIZE KiB per KiB read by the copy
                 "copy_write": 1048576.0 / 1048576.0}  # WRITE_SIZE KiB per KiB written by the copy
 
