@@ -11,6 +11,13 @@ l_L, unit (block) size l_bs, representative tokens per unit r_k, units loaded pe
 step k_m, current tokens l_X.  For grouped-query attention the paper is silent;
 the readings used here are listed with each function.
 
+Positional remap (Section 3.2, "Positional Encoding"; Appendix "Positional
+Encoding"), optional: with rotary frequencies given, q and k arrive without
+positions and the oracle applies them.  Tokens beyond the local window (I and the
+memory units) sit at the fixed distance l_L from every current token; L and X
+keep their true positions.  Without frequencies the inputs carry their positions
+already and no rotation is applied.
+
 Every function has a pin in tests/test_oracle_pins.py (brute force, closed
 forms, special cases reducing to library attention, invariants).
 """
@@ -33,6 +40,9 @@ class Params:
     n_repr: int       # r_k
     topk: int         # k_m
     sm_scale: float = 1.0
+    # Rotary angular frequencies theta_i (radians per position) of the D/2 dimension
+    # pairs (2i, 2i+1) for the positional remap; None: positions pre-applied.
+    rope_inv_freq: Optional[Tuple[float, ...]] = None
 
     @property
     def group(self) -> int:
@@ -44,6 +54,24 @@ class Partition:
     n_init: int       # |I| (fewer than l_I while the past is short)
     n_units: int      # whole units formed from the evicted tokens E
     local_begin: int  # first position of L; L = [local_begin, l_P)
+
+
+def rotate(x: np.ndarray, positions, inv_freq: Sequence[float]) -> np.ndarray:
+    """Rotary position encoding R(p) x: dimension pair i = (2i, 2i+1) turned by the angle p * theta_i.
+
+    x: [..., S, D] (or [..., D] with a scalar position); positions: [S] or a scalar.
+    The pairing is the interleaved one; a model trained with the half-split
+    pairing (i, i + D/2) is the same model after one fixed permutation of the
+    head dimensions applied to q and k alike, which leaves every q . k unchanged.
+    Angles are formed in float64.  Returns float64.
+    """
+    x = np.asarray(x, dtype=np.float64)
+    ang = np.multiply.outer(np.asarray(positions, dtype=np.float64), np.asarray(inv_freq, dtype=np.float64))
+    c, s = np.cos(ang), np.sin(ang)
+    out = np.empty_like(x)
+    out[..., 0::2] = x[..., 0::2] * c - x[..., 1::2] * s
+    out[..., 1::2] = x[..., 0::2] * s + x[..., 1::2] * c
+    return out
 
 
 def partition(past_len: int, p: Params) -> Partition:
@@ -78,7 +106,9 @@ def representative_scores(q_group: np.ndarray, k_head: np.ndarray, unit: int, p:
     q_group: [G][S][D] queries of the group's heads (positions up to m + l_L must
     exist); k_head: [S][D] keys of the kv head.  q_summed, if given, is the same
     group's query sum sum_h q^h as float64 [S][D], precomputed once per sequence
-    (q_group then only supplies G).  Returns float64 [l_bs].
+    (q_group then only supplies G).  With the positional remap, q_{m+j} and k_m
+    are rotated to their own positions (the local window keeps true distances).
+    Returns float64 [l_bs].
     """
     G = q_group.shape[0]
     m0 = unit_start(unit, p)
@@ -90,6 +120,11 @@ def representative_scores(q_group: np.ndarray, k_head: np.ndarray, unit: int, p:
     else:
         qw = q_summed[m0 + 1: m0 + lbs + lL]
     ku = np.asarray(k_head[m0: m0 + lbs, :], dtype=np.float64)
+    if p.rope_inv_freq is not None:
+        # Positional remap: while token m is in the local window its queries see it
+        # at the true distance j, so both sides keep their own positions.
+        qw = rotate(qw, np.arange(m0 + 1, m0 + lbs + lL), p.rope_inv_freq)
+        ku = rotate(ku, np.arange(m0, m0 + lbs), p.rope_inv_freq)
     dots = ku @ qw.T  # dots[t, a] = k_{m0+t} . q~_{m0+1+a}
     r = np.empty(lbs)
     for t in range(lbs):
@@ -119,11 +154,14 @@ def representatives(r: np.ndarray, p: Params) -> np.ndarray:
     return top_indices(r, p.n_repr)
 
 
-def unit_relevance(q_chunk_group: np.ndarray, k_head: np.ndarray, rep_pos: np.ndarray) -> np.ndarray:
+def unit_relevance(q_chunk_group: np.ndarray, k_head: np.ndarray, rep_pos: np.ndarray,
+                   p: Optional[Params] = None) -> np.ndarray:
     """sim(X, B) = sum_{i=1..l_X} sum_{j=1..r_k} q_{i+l_P} . k^B_{b_j} for every unit B (Section 3.2).
 
     No normalisation (the formula has none).  GQA reading: one score per kv head,
-    summed over the query heads of its group as well.
+    summed over the query heads of its group as well.  With the positional remap
+    (p given with frequencies) every memory key sits at distance l_L from every
+    current token: the queries are rotated by R(l_L), the keys not at all.
     q_chunk_group: [G][l_X][D]; rep_pos: [n_units][r_k] absolute key positions.
     Returns float64 [n_units].
     """
@@ -131,6 +169,8 @@ def unit_relevance(q_chunk_group: np.ndarray, k_head: np.ndarray, rep_pos: np.nd
         return np.zeros(0)
     D = k_head.shape[1]
     qx = np.asarray(q_chunk_group, dtype=np.float64).reshape(-1, D)        # every (head, i)
+    if p is not None and p.rope_inv_freq is not None:
+        qx = rotate(qx, float(p.n_local), p.rope_inv_freq)
     keys = np.asarray(k_head[rep_pos.reshape(-1)], dtype=np.float64)        # every (unit, j)
     dots = qx @ keys.T                                                        # all q_i . k_{b_j}
     return dots.reshape(qx.shape[0], rep_pos.shape[0], rep_pos.shape[1]).sum(axis=(0, 2))
@@ -175,16 +215,30 @@ def attend(q_chunk: np.ndarray, k: np.ndarray, v: np.ndarray, past_len: int,
     O = np.empty((Hq, nq, D))
     lse = np.empty((Hq, nq))
     causal = np.tril(np.ones((nq, nq), dtype=bool))
+    remap = p.rope_inv_freq is not None
+    part = partition(past_len, p)
     for g in range(p.n_kv_heads):
         pos = context_positions(past_len, sel[g], p)
         kc = np.asarray(k[g, pos], dtype=np.float64)
         vc = np.asarray(v[g, pos], dtype=np.float64)
         kx = np.asarray(k[g, past_len: past_len + nq], dtype=np.float64)
         vx = np.asarray(v[g, past_len: past_len + nq], dtype=np.float64)
+        if remap:
+            # I and the units (everything before L in C) at distance l_L; L and X
+            # at their true positions.
+            n_mem = pos.shape[0] - (past_len - part.local_begin)
+            kc[n_mem:] = rotate(kc[n_mem:], pos[n_mem:], p.rope_inv_freq)
+            kx = rotate(kx, np.arange(past_len, past_len + nq), p.rope_inv_freq)
         for h in range(g * G, (g + 1) * G):
             qh = np.asarray(q_chunk[h], dtype=np.float64)
-            z = np.concatenate([p.sm_scale * (qh @ kc.T),
-                                np.where(causal, p.sm_scale * (qh @ kx.T), -np.inf)], axis=1)
+            if remap:
+                q_mem = rotate(qh, float(p.n_local), p.rope_inv_freq)
+                q_loc = rotate(qh, np.arange(past_len, past_len + nq), p.rope_inv_freq)
+                zc = np.concatenate([q_mem @ kc[:n_mem].T, q_loc @ kc[n_mem:].T], axis=1)
+                zx = q_loc @ kx.T
+            else:
+                zc, zx = qh @ kc.T, qh @ kx.T
+            z = np.concatenate([p.sm_scale * zc, np.where(causal, p.sm_scale * zx, -np.inf)], axis=1)
             zmax = z.max(axis=1, keepdims=True)
             w = np.exp(z - zmax)
             s = w.sum(axis=1, keepdims=True)
@@ -261,7 +315,7 @@ class StreamOracle:
         out = np.zeros((p.n_kv_heads, nu))
         for g in range(p.n_kv_heads):
             qx = self.q[b, g * G:(g + 1) * G, past_len:past_len + n_q]
-            out[g] = unit_relevance(qx, self.k[b, g], self.rep_positions(b, g, nu))
+            out[g] = unit_relevance(qx, self.k[b, g], self.rep_positions(b, g, nu), p)
         return out
 
     def step(self, b: int, past_len: int, n_q: int, sel: Optional[np.ndarray] = None) -> dict:

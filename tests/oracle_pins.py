@@ -374,6 +374,155 @@ def check_lse_merge():
     assert np.allclose(ml, ref_l, rtol=1e-13, atol=1e-13)
 
 
+# --------------------------------------------------------------------------- positional remap
+def _rot_complex(x, pos, freqs):
+    """R(p) x written as complex arithmetic: pair (x_2i, x_2i+1) is the number
+    x_2i + i x_2i+1, multiplied by e^{i p theta_i}.  pos: scalar or one per row."""
+    x = np.asarray(x, float)
+    z = (x[..., 0::2] + 1j * x[..., 1::2]) * np.exp(1j * np.multiply.outer(np.asarray(pos, float), freqs))
+    out = np.empty(x.shape)
+    out[..., 0::2] = z.real
+    out[..., 1::2] = z.imag
+    return out
+
+
+def _rope_params(**kw):
+    rng = np.random.default_rng(kw.pop("seed", 30))
+    p = _params(**kw)
+    freqs = tuple(float(f) for f in rng.uniform(0.05, 1.5, p.head_dim // 2))
+    return O.Params(**{**p.__dict__, "rope_inv_freq": freqs})
+
+
+def check_rotation_is_complex_multiplication():
+    """The rotary map against complex multiplication, at small and at 2^20-scale positions;
+    it preserves norms and composes additively, R(a) R(b) = R(a + b)."""
+    rng = np.random.default_rng(31)
+    freqs = rng.uniform(0.0, 2.0, 5)
+    x = rng.standard_normal((3, 7, 10))
+    for pos in (np.arange(7), np.arange(7) * 149_999 + 3, 12.0):
+        got = O.rotate(x, pos, freqs)
+        ref = _rot_complex(x, pos, freqs)
+        assert np.allclose(got, ref, rtol=1e-12, atol=1e-12), pos
+        assert np.allclose(np.linalg.norm(got, axis=-1), np.linalg.norm(x, axis=-1), rtol=1e-13)
+    ab = O.rotate(O.rotate(x, 5.0, freqs), 9.0, freqs)
+    assert np.allclose(ab, O.rotate(x, 14.0, freqs), rtol=1e-12, atol=1e-12)
+
+
+def check_remap_zero_frequencies_is_identity():
+    """All angles zero: the remap changes nothing (every rotation is the identity)."""
+    rng = np.random.default_rng(32)
+    p0 = _params(n_q_heads=4, n_kv_heads=2, head_dim=8, n_init=3, n_local=8, block_size=4, n_repr=2,
+                 topk=2, sm_scale=0.9)
+    pz = O.Params(**{**p0.__dict__, "rope_inv_freq": (0.0,) * 4})
+    q, k, v = _rand_qkv(rng, p0, 70)
+    a, b = O.StreamOracle(q, k, v, p0), O.StreamOracle(q, k, v, pz)
+    for past, nq in ((30, 5), (61, 9)):
+        ra, rb = a.step(0, past, nq), b.step(0, past, nq)
+        for key in ("scores", "out", "lse"):
+            assert np.allclose(ra[key], rb[key], rtol=1e-14, atol=1e-14), (past, key)
+        assert (ra["idx"] == rb["idx"]).all()
+
+
+def check_remap_attention_effective_positions():
+    """Brute force of the remap as the paper states it: for query i at position P the key of a
+    token in I or in a selected unit is placed at position P - l_L (distance l_L), a key of L or X
+    at its own position; each logit is sm_scale (R(P) q) . (R(e) k) with its own rotation
+    (complex arithmetic, per query and key)."""
+    rng = np.random.default_rng(33)
+    p = _rope_params(seed=34, n_q_heads=4, n_kv_heads=2, head_dim=6, n_init=3, n_local=5,
+                     block_size=3, n_repr=1, topk=2, sm_scale=0.8)
+    f = np.array(p.rope_inv_freq)
+    S, G = 60, 2
+    q, k, v = _rand_qkv(rng, p, S)
+    for past, nq in ((20, 4), (47, 6)):
+        part = O.partition(past, p)
+        sel = np.stack([np.sort(rng.choice(part.n_units, 2, replace=False)) for _ in range(2)])
+        out, lse = O.attend(q[0, :, past:past + nq], k[0], v[0], past, sel, p)
+        for h in range(p.n_q_heads):
+            g = h // G
+            mem = list(range(part.n_init))
+            for b in sel[g]:
+                s0 = p.n_init + int(b) * p.block_size
+                mem += list(range(s0, s0 + p.block_size))
+            for i in range(nq):
+                P = past + i
+                keys = [(t, P - p.n_local) for t in mem] + [(t, t) for t in range(part.local_begin, P + 1)]
+                qr = _rot_complex(q[0, h, P], P, f)
+                z = np.array([p.sm_scale * float(qr @ _rot_complex(k[0, g, t], e, f)) for t, e in keys])
+                w = np.exp(z - z.max())
+                o = sum(w[j] * v[0, g, t] for j, (t, _) in enumerate(keys)) / w.sum()
+                assert np.allclose(out[h, i], o, rtol=1e-11, atol=1e-11), (past, h, i)
+                assert math.isclose(lse[h, i], z.max() + math.log(w.sum()), rel_tol=1e-11, abs_tol=1e-11)
+
+
+def check_remap_relevance_effective_positions():
+    """sim with the remap, literal triple sum: query i at its position P, every representative key
+    at P - l_L, each rotated on its own."""
+    rng = np.random.default_rng(35)
+    f = rng.uniform(0.05, 1.5, 3)
+    p = O.Params(n_q_heads=2, n_kv_heads=1, head_dim=6, n_init=2, n_local=5, block_size=4, n_repr=2,
+                 topk=2, rope_inv_freq=tuple(f))
+    G, nq, S, past = 2, 4, 50, 37
+    q = rng.standard_normal((G, S, 6))
+    k = rng.standard_normal((S, 6))
+    rep = np.stack([np.sort(rng.choice(30, 2, replace=False)) for _ in range(6)])
+    got = O.unit_relevance(q[:, past:past + nq], k, rep, p)
+    ref = []
+    for r in rep:
+        t = 0.0
+        for h in range(G):
+            for i in range(nq):
+                P = past + i
+                for j in r:
+                    t += float(_rot_complex(q[h, P], P, f) @ _rot_complex(k[j], P - p.n_local, f))
+        ref.append(t)
+    assert np.allclose(got, ref, rtol=1e-11, atol=1e-11)
+
+
+def check_remap_repr_scores_bruteforce():
+    """r_m with the remap, literal loops: window query m+j at position m+j, key m at position m."""
+    rng = np.random.default_rng(36)
+    p = _rope_params(seed=37, n_q_heads=4, n_kv_heads=2, head_dim=4, n_init=2, n_local=3, block_size=4)
+    f = np.array(p.rope_inv_freq)
+    q, k, _ = _rand_qkv(rng, p, S=2 + 3 * 4 + 3 + 1)
+    so = O.StreamOracle(q, k, k, p)
+    for g in range(2):
+        for unit in range(3):
+            m0 = p.n_init + unit * p.block_size
+            ref = []
+            for m in range(m0, m0 + p.block_size):
+                km = _rot_complex(k[0, g, m], m, f)
+                tot = 0.0
+                for h in range(2 * g, 2 * g + 2):
+                    for j in range(1, p.n_local + 1):
+                        tot += float(_rot_complex(q[0, h, m + j], m + j, f) @ km)
+                ref.append(tot / (p.n_local * 2))
+            got = O.representative_scores(q[0, 2 * g:2 * g + 2], k[0, g], unit, p)
+            assert np.allclose(got, ref, rtol=1e-12, atol=1e-12), (g, unit)
+            assert np.allclose(so.repr_scores(0, g, unit), ref, rtol=1e-12, atol=1e-12), (g, unit)
+
+
+def check_remap_reduces_to_rotary_attention():
+    """No initial tokens and a window longer than the sequence: nothing is ever beyond the local
+    window, so the remap is plain causal attention over rotary-encoded q and k (PyTorch's
+    scaled_dot_product_attention in float64 on the rotated inputs)."""
+    rng = np.random.default_rng(38)
+    p = _rope_params(seed=39, n_q_heads=4, n_kv_heads=2, head_dim=8, n_init=0, n_local=64,
+                     block_size=4, n_repr=1, topk=3, sm_scale=0.6)
+    f = np.array(p.rope_inv_freq)
+    S = 40
+    q, k, v = _rand_qkv(rng, p, S)
+    pos = np.arange(S)
+    qr, kr = _rot_complex(q[0], pos, f), _rot_complex(k[0], pos, f)
+    mask = np.tril(np.ones((S, S), dtype=bool))[None]
+    ref_o, ref_l = _sdpa(qr, _expand(kr, 2), _expand(v[0], 2), mask, 0.6)
+    so = O.StreamOracle(q, k, v, p)
+    for past in (0, 9, 31):
+        r = so.step(0, past, 9)
+        assert np.allclose(r["out"], ref_o[:, past:past + 9], rtol=1e-12, atol=1e-12), past
+        assert np.allclose(r["lse"], ref_l[:, past:past + 9], rtol=1e-12, atol=1e-12), past
+
+
 # --------------------------------------------------------------------------- golden
 def load_golden():
     with open(os.path.join(GOLDEN, "hand_worked_tiny.yaml")) as f:
@@ -417,4 +566,10 @@ ALL_CHECKS = [
     check_sparse_equals_masked_dense,
     check_lse_merge,
     check_hand_worked_example,
+    check_rotation_is_complex_multiplication,
+    check_remap_zero_frequencies_is_identity,
+    check_remap_attention_effective_positions,
+    check_remap_relevance_effective_positions,
+    check_remap_repr_scores_bruteforce,
+    check_remap_reduces_to_rotary_attention,
 ]

@@ -20,7 +20,7 @@ def test_pin(check):
 # ------------------------------------------------------------------ mutants
 _orig = {name: getattr(O, name) for name in
          ("partition", "representative_scores", "top_indices", "unit_relevance", "attend",
-          "lse_merge", "context_positions", "select_units", "unit_start")}
+          "lse_merge", "context_positions", "select_units", "unit_start", "rotate")}
 
 
 def _mut_partition_drop_remainder(past_len, p):
@@ -65,12 +65,86 @@ def _mut_topk_smallest(values, count):
     return _orig["top_indices"](-np.asarray(values, float), count)
 
 
-def _mut_relevance_sign(q, k, rep):
-    return -_orig["unit_relevance"](q, k, rep)
+def _mut_relevance_sign(q, k, rep, p=None):
+    return -_orig["unit_relevance"](q, k, rep, p)
 
 
-def _mut_relevance_one_rep(q, k, rep):
-    return _orig["unit_relevance"](q, k, rep[:, :1])
+def _mut_relevance_one_rep(q, k, rep, p=None):
+    return _orig["unit_relevance"](q, k, rep[:, :1], p)
+
+
+# ---- positional remap slips
+def _mut_rotate_half_split(x, positions, inv_freq):
+    # pairs (i, i + D/2) instead of (2i, 2i+1)
+    x = np.asarray(x, float)
+    h = x.shape[-1] // 2
+    ang = np.multiply.outer(np.asarray(positions, float), np.asarray(inv_freq, float))
+    c, s = np.cos(ang), np.sin(ang)
+    out = np.empty_like(x)
+    out[..., :h] = x[..., :h] * c - x[..., h:] * s
+    out[..., h:] = x[..., :h] * s + x[..., h:] * c
+    return out
+
+
+def _mut_rotate_backwards(x, positions, inv_freq):
+    return _orig["rotate"](x, -np.asarray(positions, float), inv_freq)
+
+
+def _mut_relevance_true_positions(q, k, rep, p=None):
+    # memory keys scored without the remap (no R(l_L) on the queries)
+    import dataclasses
+    return _orig["unit_relevance"](q, k, rep, None if p is None else dataclasses.replace(p, rope_inv_freq=None))
+
+
+def _mut_repr_unrotated(q_group, k_head, unit, p, q_summed=None):
+    import dataclasses
+    return _orig["representative_scores"](q_group, k_head, unit, dataclasses.replace(p, rope_inv_freq=None),
+                                          q_summed)
+
+
+def _mut_attend_memory_negative_distance(q_chunk, k, v, past_len, sel, p):
+    # memory queries turned by R(-l_L) instead of R(l_L)
+    import dataclasses
+    if p.rope_inv_freq is None:
+        return _orig["attend"](q_chunk, k, v, past_len, sel, p)
+    real_rotate = O.rotate
+
+    def rot(x, positions, f):
+        if np.ndim(positions) == 0 and float(positions) == float(p.n_local):
+            positions = -float(p.n_local)
+        return real_rotate(x, positions, f)
+    O.rotate = rot
+    try:
+        return _orig["attend"](q_chunk, k, v, past_len, sel, p)
+    finally:
+        O.rotate = real_rotate
+
+
+def _mut_attend_init_true_positions(q_chunk, k, v, past_len, sel, p):
+    # initial tokens kept at their true positions (only the units remapped)
+    if p.rope_inv_freq is None:
+        return _orig["attend"](q_chunk, k, v, past_len, sel, p)
+    Hq, nq, D = q_chunk.shape
+    G = p.group
+    f = p.rope_inv_freq
+    part = O.partition(past_len, p)
+    out, lse = np.empty((Hq, nq, D)), np.empty((Hq, nq))
+    for g in range(p.n_kv_heads):
+        pos = O.context_positions(past_len, sel[g], p)
+        for h in range(g * G, (g + 1) * G):
+            for i in range(nq):
+                P = past_len + i
+                keys = np.concatenate([pos, np.arange(past_len, P + 1)])
+                qr = O.rotate(q_chunk[h, i], float(P), f)
+                z = []
+                for t in keys:
+                    e = t if (t < part.n_init or t >= part.local_begin) else P - p.n_local
+                    z.append(p.sm_scale * float(qr @ O.rotate(k[g, t], float(e), f)))
+                z = np.array(z)
+                w = np.exp(z - z.max())
+                out[h, i] = (w[:, None] * v[g, keys]).sum(0) / w.sum()
+                lse[h, i] = z.max() + np.log(w.sum())
+    return out, lse
 
 
 def _mut_attend_no_causal(q_chunk, k, v, past_len, sel, p):
@@ -143,6 +217,12 @@ MUTANTS = [
     ("unit_start", _mut_unit_start_off_by_one),
     ("context_positions", _mut_context_drop_init),
     ("select_units", _mut_select_top_km_minus_1),
+    ("rotate", _mut_rotate_half_split),
+    ("rotate", _mut_rotate_backwards),
+    ("unit_relevance", _mut_relevance_true_positions),
+    ("representative_scores", _mut_repr_unrotated),
+    ("attend", _mut_attend_memory_negative_distance),
+    ("attend", _mut_attend_init_true_positions),
 ]
 
 
