@@ -62,6 +62,20 @@ typedef struct {
   int32_t topk;       /* k_m >= 0: units loaded per step */
   int32_t dtype;      /* infllm_dtype of q, k, v and the attention output */
   float sm_scale;     /* softmax logit scale > 0 (1 when q or k arrive pre-scaled) */
+  /* Positional remap (Section 3.2, "Positional Encoding").  NULL: q and k arrive
+   * with their positions already applied and nothing is rotated.  Otherwise a HOST
+   * array of D/2 finite rotary angular frequencies theta_i >= 0 (radians per
+   * position), read during each call: q and k arrive without positions, dimension
+   * pair i = (2i, 2i+1) turns by p*theta_i, and the library applies the remap:
+   *  - keys of I and of the memory units are met at distance l_L from every current
+   *    token: logit sm_scale * (R(l_L) q) . k, the key unrotated;
+   *  - keys of L and X keep their true positions: sm_scale * (R(p_q) q) . (R(t) k_t);
+   *  - unit relevance uses the memory distance, sim = (R(l_L) Qbar) . Kbar;
+   *  - representative scores are those of the local window, q_{m+j} and k_m at
+   *    their own positions.
+   * Half-split pairs (i, i + D/2) are the same model after one fixed permutation
+   * of the head dimensions of q and k.  Needs memory.k_rot. */
+  const double* rope_inv_freq;
 } infllm_params;
 
 /*
@@ -83,6 +97,10 @@ typedef struct {
  *              t; summed over s it is l_L*G times the representative score r_t of
  *              Section 3.2.  Written by infllm_append once position t + l_L is
  *              appended, read by infllm_build_units.
+ *   k_rot      [batch][Hkv][capacity][D] dtype, only with the positional remap
+ *              (params.rope_inv_freq set; may be NULL otherwise): every key rotated
+ *              to its own position, R(t) k_t, written by infllm_append next to the
+ *              unrotated k; the attention reads L and X from it.
  * Unit b of E covers positions [l_I + b*l_bs, l_I + (b+1)*l_bs).
  * For bf16 the attention entry points need one [capacity][D] slice of k or v to
  * span at most 4 GiB (capacity * D * 2 bytes; 16M tokens at D = 128), else
@@ -99,6 +117,7 @@ typedef struct {
   double* qprefix;
   double* rpart;
   int32_t ring;
+  void* k_rot;
 } infllm_memory;
 
 /* Partition of P at past length l_P (Section 3.1): |I| = min(l_I, l_P);
@@ -118,7 +137,9 @@ size_t infllm_workspace_bytes(const infllm_params* p, int32_t batch, int32_t n_q
  *     q + (b*Hq + h)*q_head_stride elements (q_head_stride >= n_q*D).
  *  k, v: chunk keys/values laid out the same way with kv_head_stride; both NULL
  *     when the caller has already written them into the store.
- * Copies k, v into the store, extends the qprefix ring and, for every appended
+ * Copies k, v into the store (and, with the positional remap, the rotated keys
+ * into k_rot; the ring then sums the group's queries rotated to their positions),
+ * extends the qprefix ring and, for every appended
  * position p with t = p - l_L >= l_I, writes the partial representative scores of
  * token t into rpart (what the representative score r_t of Section 3.2 needs
  * once t is evicted).  Positions must be appended in order: slot (past_len - 1)
@@ -167,7 +188,9 @@ infllm_status infllm_select_topk(int32_t rows, const float* scores, int32_t n_un
  *  out: [batch][Hq] heads of n_q x D dtype rows, head stride out_head_stride.
  *  lse: optional [batch][Hq][n_q] float32 natural-log sum of exp of the logits.
  * The keys are split into parts processed in parallel whose partial softmaxes are
- * merged by their log-sum-exp; the workspace holds the partials. */
+ * merged by their log-sum-exp; the workspace holds the partials.  With the
+ * positional remap, memory keys and local keys always fall in different parts,
+ * so the workspace is required whenever I or a unit is attended (E_WORKSPACE). */
 infllm_status infllm_chunk_attend(const infllm_params* p, const infllm_memory* m, const void* q,
                                   int64_t q_head_stride, int32_t n_q, int64_t past_len,
                                   const int32_t* idx, int32_t k, void* out, int64_t out_head_stride,

@@ -54,14 +54,39 @@ infllm_status check_params(const infllm_params* p) {
   if (p->block_size > 256) return INFLLM_E_UNSUPPORTED;
   if (p->n_repr < 1 || p->n_repr > p->block_size) return INFLLM_E_SHAPE;
   if (!std::isfinite(p->sm_scale) || !(p->sm_scale > 0.f)) return INFLLM_E_SHAPE;
+  if (p->rope_inv_freq != nullptr) {
+    for (int i = 0; i < p->head_dim / 2; ++i)
+      if (!std::isfinite(p->rope_inv_freq[i]) || p->rope_inv_freq[i] < 0.0) return INFLLM_E_SHAPE;
+  }
   return INFLLM_OK;
+}
+
+bool remap(const infllm_params* p) { return p->rope_inv_freq != nullptr; }
+
+// Rotary tables of the positional remap, formed in float64 on the host.
+RopeArgs rope_args(const infllm_params* p) {
+  RopeArgs r;
+  std::memset(&r, 0, sizeof(r));
+  if (!remap(p)) return r;
+  r.on = 1;
+  const double two_pi = 6.283185307179586476925286766559;
+  for (int i = 0; i < p->head_dim / 2; ++i) {
+    const double th = p->rope_inv_freq[i];
+    r.rev[i] = th / two_pi;
+    r.mem_cos[i] = (float)std::cos((double)p->n_local * th);
+    r.mem_sin[i] = (float)std::sin((double)p->n_local * th);
+  }
+  return r;
 }
 
 infllm_status check_store(const infllm_params* p, const infllm_memory* m) {
   if (m == nullptr || m->k == nullptr || m->v == nullptr) return INFLLM_E_NULL;
   if (m->batch < 1 || m->capacity < 1) return INFLLM_E_SHAPE;
   if (!aligned16(m->k) || !aligned16(m->v)) return INFLLM_E_SHAPE;
-  (void)p;
+  if (remap(p)) {
+    if (m->k_rot == nullptr) return INFLLM_E_NULL;
+    if (!aligned16(m->k_rot)) return INFLLM_E_SHAPE;
+  }
   return INFLLM_OK;
 }
 
@@ -156,9 +181,21 @@ infllm_status prepare_attend(const infllm_params* p, const infllm_memory* m, con
   const int64_t rows = (int64_t)m->batch * p->n_q_heads * n_q;
   const size_t per_part = rows > 0 ? (size_t)rows * part_row_bytes(p) : 1;
   const int max_parts = (workspace == nullptr) ? 0 : (int)(workspace_bytes / per_part > 4096 ? 4096 : workspace_bytes / per_part);
-  const int parts = attend_choose_parts(bf16, m->batch, p->n_q_heads, p->n_kv_heads, n_q, n_sel, (int)n_virtual,
-                                        max_parts);
+  int parts = attend_choose_parts(bf16, m->batch, p->n_q_heads, p->n_kv_heads, n_q, n_sel, (int)n_virtual,
+                                  max_parts);
   if (parts < 1) return INFLLM_E_WORKSPACE;
+  // With the remap, memory keys (I and the units) and local keys go to
+  // different parts, in proportion to their counts.
+  const int64_t mem_len = part.n_init + (int64_t)n_sel * p->block_size;
+  int parts_mem = 0;
+  if (remap(p) && mem_len > 0) {
+    if (parts < 2) {
+      if (max_parts < 2) return INFLLM_E_WORKSPACE;
+      parts = 2;
+    }
+    parts_mem = (int)((parts * mem_len + n_virtual / 2) / n_virtual);
+    parts_mem = std::min(std::max(parts_mem, 1), parts - 1);
+  }
   if (parts > 1 && !aligned16(workspace)) return INFLLM_E_SHAPE;
 
   std::memset(a, 0, sizeof(*a));
@@ -183,6 +220,10 @@ infllm_status prepare_attend(const infllm_params* p, const infllm_memory* m, con
   a->q = q;
   a->k_store = m->k;
   a->v_store = m->v;
+  a->k_rot = m->k_rot;
+  a->parts_mem = parts_mem;
+  a->mem_len = (int)mem_len;
+  a->rope = rope_args(p);
   a->idx = idx;
   a->out = out;
   a->lse = lse;
@@ -264,6 +305,8 @@ infllm_status prep_append(const infllm_params* p, const infllm_memory* m, const 
   a->v_store = m->v;
   a->qprefix = m->qprefix;
   a->rpart = m->rpart;
+  a->k_rot = m->k_rot;
+  a->rope = rope_args(p);
   a->bf16 = p->dtype == INFLLM_BF16;
   return INFLLM_OK;
 }
@@ -334,6 +377,7 @@ infllm_status prep_score(const infllm_params* p, const infllm_memory* m, const v
   a->unit_ksum = m->unit_ksum;
   a->scores = scores;
   a->qbar_parts = (float*)workspace;
+  a->rope = rope_args(p);
   a->bf16 = p->dtype == INFLLM_BF16;
   return INFLLM_OK;
 }
@@ -380,7 +424,8 @@ infllm_status infllm_partition(const infllm_params* p, int64_t past_len, int64_t
 size_t infllm_workspace_bytes(const infllm_params* p, int32_t batch, int32_t n_q) {
   if (check_params(p) != INFLLM_OK || batch < 1 || n_q < 0) return 0;
   const int G = p->n_q_heads / p->n_kv_heads;
-  const int parts = attend_max_parts(p->dtype == INFLLM_BF16, G, n_q, max_virtual_keys(p, n_q));
+  int parts = attend_max_parts(p->dtype == INFLLM_BF16, G, n_q, max_virtual_keys(p, n_q));
+  if (remap(p)) parts = std::max(parts, 2);
   size_t a = attend_ws_bytes(p, batch, n_q, parts);
   size_t b = qbar_ws_bytes(p, batch, n_q);
   size_t r = a > b ? a : b;

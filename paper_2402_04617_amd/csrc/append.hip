@@ -73,6 +73,45 @@ __device__ __forceinline__ void raw8_to_float(const Raw8<T>& r, float* out) {
   }
 }
 
+// R(pos) applied to one 16-byte vector of consecutive dimensions starting at the
+// even dimension 2*pair0 (positional remap): 4 bf16 pairs or 2 float32 pairs.
+template <typename T>
+__device__ __forceinline__ uint4 rotate_vec(const uint4 w, int64_t pos, int pair0, const RopeArgs& r) {
+  uint32_t in[4] = {w.x, w.y, w.z, w.w}, out[4];
+  if constexpr (sizeof(T) == 2) {
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      float c, sn;
+      rope_cos_sin(r, pos, pair0 + j, c, sn);
+      const float x0 = __uint_as_float(in[j] << 16), x1 = __uint_as_float(in[j] & 0xFFFF0000u);
+      out[j] = (uint32_t)f32_to_bf16(x0 * c - x1 * sn) | ((uint32_t)f32_to_bf16(x0 * sn + x1 * c) << 16);
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      float c, sn;
+      rope_cos_sin(r, pos, pair0 + j, c, sn);
+      const float x0 = __uint_as_float(in[2 * j]), x1 = __uint_as_float(in[2 * j + 1]);
+      out[2 * j] = __float_as_uint(x0 * c - x1 * sn);
+      out[2 * j + 1] = __float_as_uint(x0 * sn + x1 * c);
+    }
+  }
+  return make_uint4(out[0], out[1], out[2], out[3]);
+}
+
+// R(pos) on 8 consecutive dimensions (4 pairs from pair0) held as float64 or float.
+template <typename V>
+__device__ __forceinline__ void rotate8(V (&x)[8], int64_t pos, int pair0, const RopeArgs& r) {
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    float c, sn;
+    rope_cos_sin(r, pos, pair0 + j, c, sn);
+    const V x0 = x[2 * j], x1 = x[2 * j + 1];
+    x[2 * j] = x0 * (V)c - x1 * (V)sn;
+    x[2 * j + 1] = x0 * (V)sn + x1 * (V)c;
+  }
+}
+
 // Block roles along the 1-D grid: [unit construction | scan | copy].
 struct AppendGrid {
   int n_build;          // unit-construction blocks (n_new * batch * Hkv), 0 when not fused
@@ -120,6 +159,19 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
     if (e1 < vec_per_head) { dst_k[e1] = k1; dst_v[e1] = v1; }
     if (e2 < vec_per_head) { dst_k[e2] = k2; dst_v[e2] = v2; }
     if (e3 < vec_per_head) { dst_k[e3] = k3; dst_v[e3] = v3; }
+    if (a.rope.on) {
+      // positional remap: the keys rotated to their own positions go to k_rot
+      uint4* dst_r = (uint4*)a.k_rot + head * (a.capacity * D / VEC) + a.past_len * D / VEC;
+      const int vpp = D / VEC;  // vectors per position
+      auto rot = [&](int e, const uint4& w) {
+        if (e < vec_per_head)
+          dst_r[e] = rotate_vec<T>(w, a.past_len + e / vpp, (e % vpp) * (VEC / 2), a.rope);
+      };
+      rot(e0, k0);
+      rot(e1, k1);
+      rot(e2, k2);
+      rot(e3, k3);
+    }
     return;
   }
 
@@ -137,6 +189,8 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
     double* col = a.qprefix + (int64_t)bg * a.ring * D + d;
     const int slot0 = (int)(a.past_len % a.ring);
     // every load that does not depend on this launch's writes is issued first
+    // with the positional remap the stored keys of earlier tokens are read rotated
+    const T* kread = (const T*)(a.rope.on ? a.k_rot : a.k_store);
     double x[kThinMaxQ], ht[kThinMaxQ];
     float kt[kThinMaxQ];
 #pragma unroll
@@ -151,16 +205,26 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
           const int sp = slot0 + i - (slot0 + i >= a.ring ? a.ring : 0);
           const int st = sp - a.n_local + (sp < a.n_local ? a.ring : 0);  // n_local < ring
           ht[i] = col[(int64_t)st * D];
-          kt[i] = Elem<T>::load((const T*)a.k_store + ((int64_t)bg * a.capacity + t) * D + d);
+          kt[i] = Elem<T>::load(kread + ((int64_t)bg * a.capacity + t) * D + d);
         }
       }
     }
     double run = 0.0;
     if (a.past_len > 0) run = col[(int64_t)(slot0 == 0 ? a.ring - 1 : slot0 - 1) * D];
     const double base = run;
+    float raw_tot = 0.f;  // the chunk's unrotated query sum (remap: the ring holds rotated sums)
+    // R(pos) on dimension d of a pair split over lanes d, d^1 (uniform branch: pos is per position)
+    auto rot_lane = [&](double v, int64_t pos) -> double {
+      const double w = __shfl_xor(v, 1);
+      float c, sn;
+      rope_cos_sin(a.rope, pos, d >> 1, c, sn);
+      return (d & 1) ? w * (double)sn + v * (double)c : v * (double)c - w * (double)sn;
+    };
 #pragma unroll
     for (int i = 0; i < kThinMaxQ; ++i) {
       if (i >= a.n_q) continue;  // (not break: the loop stays unrolled, the arrays in registers)
+      raw_tot += (float)x[i];
+      if (a.rope.on) x[i] = rot_lane(x[i], a.past_len + i);
       run += x[i];
       const int sp = slot0 + i - (slot0 + i >= a.ring ? a.ring : 0);
       col[(int64_t)sp * D] = run;
@@ -172,6 +236,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
           const int st = sp - a.n_local + (sp < a.n_local ? a.ring : 0);
           h = col[(int64_t)st * D];
           k = Elem<T>::load((const T*)a.k_src + (int64_t)bg * a.kv_head_stride + (t - a.past_len) * D + d);
+          if (a.rope.on) k = rot_lane(k, t);
         }
         double part = k * (run - h);
 #pragma unroll
@@ -179,7 +244,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
         if ((d & 15) == 0) a.rpart[((int64_t)bg * (D / 16) + d / 16) * a.ring + (int)(t % a.ring)] = part;
       }
     }
-    if (qbar != nullptr) qbar[(int64_t)bg * D + d] = (float)(run - base);
+    if (qbar != nullptr) qbar[(int64_t)bg * D + d] = a.rope.on ? raw_tot : (float)(run - base);
     return;
   }
 
@@ -196,6 +261,11 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
   double* ring = a.qprefix + (int64_t)bg * a.ring * D + d0;
 
   __shared__ double wave_tot[kWaves][2][8];
+  __shared__ float wave_raw[kWaves][2][8];
+  const T* kread = (const T*)(a.rope.on ? a.k_rot : a.k_store);  // stored keys, rotated under the remap
+  float raw_acc[8];  // unrotated query sum of this thread's positions (the chunk total feeds scoring)
+#pragma unroll
+  for (int e = 0; e < 8; ++e) raw_acc[e] = 0.f;
   const int slot0 = (int)(a.past_len % a.ring);  // ring > n_q: slot0 + i wraps at most once
   double base[8], carry[8];
   if (a.past_len > 0) {
@@ -240,7 +310,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
         for (int e = 0; e < 4; ++e) ht[s][e] = src[e];
         int64_t tk = a.past_len + ic - a.n_local;
         tk = tk < 0 ? 0 : tk;
-        kr[s] = load_raw8<T>((const T*)a.k_store + ((int64_t)bg * a.capacity + tk) * D + d0);
+        kr[s] = load_raw8<T>(kread + ((int64_t)bg * a.capacity + tk) * D + d0);
       }
     }
     double run[kSeg][8];
@@ -269,6 +339,12 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
 #pragma unroll
           for (int e = 0; e < 8; ++e) x[e] += (double)y[e];
         }
+      }
+      if (a.rope.on) {
+        // the ring sums the queries rotated to their positions; scoring takes the plain sum
+#pragma unroll
+        for (int e = 0; e < 8; ++e) raw_acc[e] += valid ? (float)x[e] : 0.f;
+        rotate8(x, a.past_len + i, d0 / 2, a.rope);
       }
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -365,7 +441,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
         }
         kk[s] = t >= a.past_len
                     ? load_raw8<T>((const T*)a.k_src + (int64_t)bg * a.kv_head_stride + (t - a.past_len) * D + d0)
-                    : load_raw8<T>((const T*)a.k_store + ((int64_t)bg * a.capacity + t) * D + d0);
+                    : load_raw8<T>(kread + ((int64_t)bg * a.capacity + t) * D + d0);
       }
 #pragma unroll
       for (int s = 0; s < kSeg; ++s) {
@@ -374,6 +450,8 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
         const bool act = i < a.n_q && t >= a.n_init;
         float kt[8];
         raw8_to_float<T>(kk[s], kt);
+        // a key of this chunk comes unrotated from k_src
+        if (a.rope.on && t >= a.past_len) rotate8(kt, t, d0 / 2, a.rope);
         double p = 0.0;
 #pragma unroll
         for (int e = 0; e < 4; ++e)
@@ -383,7 +461,29 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
       }
     }
   }
-  if (qbar != nullptr && seg == 0) {
+  if (qbar != nullptr && a.rope.on) {
+    // plain query sum of the chunk: over the 32 segments of this half in the
+    // wave, then over the waves
+#pragma unroll
+    for (int o = 2; o < 64; o <<= 1) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) raw_acc[e] += __shfl_xor(raw_acc[e], o);
+    }
+    if (lane < 2) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) wave_raw[wave][half][e] = raw_acc[e];
+    }
+    __syncthreads();
+    if (seg == 0) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        float t = 0.f;
+#pragma unroll
+        for (int w = 0; w < kWaves; ++w) t += wave_raw[w][half][e];
+        qbar[(int64_t)bg * D + d0 + e] = t;
+      }
+    }
+  } else if (qbar != nullptr && seg == 0) {
 #pragma unroll
     for (int e = 0; e < 8; ++e) qbar[(int64_t)bg * D + d0 + e] = (float)(carry[e] - base[e]);
   }

@@ -2,7 +2,8 @@
 // the bandwidth kernel of attend_decode.hip), plus the float32 kernel:
 //  - attend_f32_kernel: float32 inputs (any n_q), vector ALU, exact-exp online
 //    softmax; the float32 accuracy path.  It reads keys through the same
-//    virtual key axis as the other kernels.
+//    virtual key axis as the other kernels; with the positional remap it holds
+//    both forms of the query and picks one per key (memory or local).
 #include "launch.h"
 
 namespace infllm {
@@ -55,12 +56,31 @@ __global__ void __launch_bounds__(256) attend_f32_kernel(AttendArgs a) {
   const float* kbase = (const float*)a.k_store + (int64_t)bg * a.capacity * D;
   const float* vbase = (const float*)a.v_store + (int64_t)bg * a.capacity * D;
 
-  float qv[DPT], o[DPT];
+  // Query pieces: qv as given; with the positional remap qv is the query at its
+  // own position (for L and X) and qm the query turned by R(l_L) (for I and the
+  // units, whose keys are read unrotated).
+  float qv[DPT], qm[DPT], o[DPT];
   const float* qp = (const float*)a.q + (int64_t)(b * a.n_q_heads + qh) * a.q_head_stride + (int64_t)qi * D;
 #pragma unroll
   for (int e = 0; e < DPT; ++e) {
     qv[e] = row_ok ? qp[sub * DPT + e] : 0.f;
+    qm[e] = qv[e];
     o[e] = 0.f;
+  }
+  const bool remap = a.rope.on != 0;
+  const float* krot = (const float*)a.k_rot + (int64_t)bg * a.capacity * D;
+  if (remap) {
+#pragma unroll
+    for (int j = 0; j < DPT / 2; ++j) {
+      const int pr = sub * DPT / 2 + j;
+      const float x0 = qv[2 * j], x1 = qv[2 * j + 1];
+      float c, sn;
+      rope_cos_sin(a.rope, geo.past_len + qi, pr, c, sn);
+      qv[2 * j] = x0 * c - x1 * sn;
+      qv[2 * j + 1] = x0 * sn + x1 * c;
+      qm[2 * j] = x0 * a.rope.mem_cos[pr] - x1 * a.rope.mem_sin[pr];
+      qm[2 * j + 1] = x0 * a.rope.mem_sin[pr] + x1 * a.rope.mem_cos[pr];
+    }
   }
   float m = -__builtin_inff(), l = 0.f;
 
@@ -71,7 +91,7 @@ __global__ void __launch_bounds__(256) attend_f32_kernel(AttendArgs a) {
       const int64_t pos = v < geo.n_virtual ? virtual_pos(geo, idx_row, v) : -1;
       float4 kk = make_float4(0.f, 0.f, 0.f, 0.f), vv = kk;
       if (pos >= 0) {
-        kk = *(const float4*)(kbase + pos * D + 4 * c);
+        kk = *(const float4*)((remap && v >= a.mem_len ? krot : kbase) + pos * D + 4 * c);
         vv = *(const float4*)(vbase + pos * D + 4 * c);
       }
       *(float4*)&ks[j][4 * c] = kk;
@@ -80,9 +100,10 @@ __global__ void __launch_bounds__(256) attend_f32_kernel(AttendArgs a) {
     }
     __syncthreads();
     for (int j = 0; j < KT; ++j) {
+      const bool mem_key = remap && t * KT + j < a.mem_len;  // uniform over the workgroup
       float part_dot = 0.f;
 #pragma unroll
-      for (int e = 0; e < DPT; ++e) part_dot += qv[e] * ks[j][sub * DPT + e];
+      for (int e = 0; e < DPT; ++e) part_dot += (mem_key ? qm[e] : qv[e]) * ks[j][sub * DPT + e];
 #pragma unroll
       for (int off = TPR / 2; off > 0; off >>= 1) part_dot += __shfl_xor(part_dot, off);
       const bool vis = kval[j] && key_visible(geo, t * KT + j, qi);

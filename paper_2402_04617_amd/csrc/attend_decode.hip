@@ -124,11 +124,24 @@ __global__ void __launch_bounds__(64 * kDecodeWaves) attend_decode_kernel(Attend
   const int c = lane % LPK, r = lane / LPK;  // 16-byte piece of the row, key slot of the load
   for (int j = tid; j < geo.n_sel; j += 64 * kDecodeWaves) sidx[j] = a.idx[(int64_t)bg * geo.idx_stride + j];
 
-  // This wave's keys: the parts split the virtual axis evenly, in whole tiles per wave.
-  const int n_waves_total = a.parts * kDecodeWaves;
-  const int kpw = ((geo.n_virtual + n_waves_total - 1) / n_waves_total + TK - 1) / TK * TK;
-  const int vw0 = (part * kDecodeWaves + wave) * kpw;
-  const int vw1 = min(vw0 + kpw, geo.n_virtual);
+  // This wave's keys: the parts split the virtual axis evenly, in whole tiles per
+  // wave.  With the positional remap parts [0, parts_mem) split the memory keys
+  // [0, mem_len) (I and the units) and the other parts the local keys.
+  const bool remap = a.rope.on != 0;
+  const bool mem_part = part < a.parts_mem;
+  int rv0 = 0, rv1 = geo.n_virtual, rpart = part, rparts = a.parts;
+  if (mem_part) {
+    rv1 = a.mem_len;
+    rparts = a.parts_mem;
+  } else if (a.parts_mem > 0) {
+    rv0 = a.mem_len;
+    rpart = part - a.parts_mem;
+    rparts = a.parts - a.parts_mem;
+  }
+  const int n_waves_total = rparts * kDecodeWaves;
+  const int kpw = ((rv1 - rv0 + n_waves_total - 1) / n_waves_total + TK - 1) / TK * TK;
+  const int vw0 = rv0 + (rpart * kDecodeWaves + wave) * kpw;
+  const int vw1 = min(vw0 + kpw, rv1);
   const int nt = vw1 > vw0 ? (vw1 - vw0 + TK - 1) / TK : 0;
 
   // Query rows of the group: this lane's 8 dims as 4 bf16 pairs; the dot products
@@ -144,10 +157,30 @@ __global__ void __launch_bounds__(64 * kDecodeWaves) attend_decode_kernel(Attend
     qv[h][2] = raw.z;
     qv[h][3] = raw.w;
   }
+  if (remap) {
+    // memory parts: the query turned by R(l_L); local parts: at its own position
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int pr = 4 * c + e;  // the pair held in word e
+      float cs, sn;
+      if (mem_part) {
+        cs = a.rope.mem_cos[pr];
+        sn = a.rope.mem_sin[pr];
+      } else {
+        rope_cos_sin(a.rope, geo.past_len, pr, cs, sn);
+      }
+#pragma unroll
+      for (int h = 0; h < G; ++h) {
+        const float x0 = __uint_as_float(qv[h][e] << 16), x1 = __uint_as_float(qv[h][e] & 0xFFFF0000u);
+        qv[h][e] = (uint32_t)f32_to_bf16(x0 * cs - x1 * sn) | ((uint32_t)f32_to_bf16(x0 * sn + x1 * cs) << 16);
+      }
+    }
+  }
   __syncthreads();
 
-  // uniform slice bases; per-lane 32-bit byte offsets (row offset + this lane's piece)
-  const char* kbase = (const char*)a.k_store + (int64_t)bg * a.capacity * (D * 2);
+  // uniform slice bases; per-lane 32-bit byte offsets (row offset + this lane's piece).
+  // Local keys come rotated from k_rot under the remap.
+  const char* kbase = (const char*)(remap && !mem_part ? a.k_rot : a.k_store) + (int64_t)bg * a.capacity * (D * 2);
   const char* vbase = (const char*)a.v_store + (int64_t)bg * a.capacity * (D * 2);
   const uint32_t piece = c * 16;
 

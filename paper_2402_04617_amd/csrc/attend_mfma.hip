@@ -126,10 +126,27 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
   const int bg = tmp / a.parts;
   const int b = bg / a.n_kv_heads, g = bg - b * a.n_kv_heads;
 
+  // This part's tiles.  Without the positional remap the parts split the tiles
+  // evenly.  With it, parts [0, parts_mem) split the memory tiles [0,
+  // ceil(mem_len/KB)) (I and the units: unrotated keys, queries turned by R(l_L))
+  // and the other parts the local tiles [floor(mem_len/KB), n_tiles) (L and X:
+  // rotated keys, queries at their own positions); a tile holding keys of both
+  // kinds is taken by both sides, each masking the other's keys.
   const int n_tiles = (geo.n_virtual + KB - 1) / KB;
-  const int per_part = (n_tiles + a.parts - 1) / a.parts;
-  const int t_begin = part * per_part;
-  int t_end = min(n_tiles, t_begin + per_part);
+  const bool remap = a.rope.on != 0;
+  const bool mem_part = part < a.parts_mem;
+  int rt0 = 0, rt1 = n_tiles, rpart = part, rparts = a.parts;
+  if (mem_part) {
+    rt1 = (a.mem_len + KB - 1) / KB;
+    rparts = a.parts_mem;
+  } else if (a.parts_mem > 0) {
+    rt0 = a.mem_len / KB;
+    rpart = part - a.parts_mem;
+    rparts = a.parts - a.parts_mem;
+  }
+  const int per_part = (rt1 - rt0 + rparts - 1) / rparts;
+  const int t_begin = rt0 + rpart * per_part;
+  int t_end = min(rt1, t_begin + per_part);
   const int v_x0 = geo.n_virtual - geo.n_q;  // first current-token key
   {
     const int i_max = (min(R, (rt + 1) * ROWS_WG) - 1) / G;
@@ -143,10 +160,13 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
   const int row = rt * ROWS_WG + wave * 32 + n;
   const bool row_ok = row < R;
   const int qi = row_ok ? row / G : 0;
+  // last virtual key this row may see: causal within X (which also excludes the
+  // ragged end), or for a memory part of the remap the last memory key
+  const int vlim = mem_part ? a.mem_len - 1 : v_x0 + qi;
   const int qh = g * G + (row_ok ? row - qi * G : 0);
 
   const int32_t* idx_row = a.idx + (int64_t)bg * geo.idx_stride;
-  const bf16_t* kbase = (const bf16_t*)a.k_store + (int64_t)bg * a.capacity * D;
+  const bf16_t* kbase = (const bf16_t*)(remap && !mem_part ? a.k_rot : a.k_store) + (int64_t)bg * a.capacity * D;
   const bf16_t* vbase = (const bf16_t*)a.v_store + (int64_t)bg * a.capacity * D;
 
   // The lookup row goes to LDS (run starts then read LDS, not global memory) in
@@ -165,7 +185,23 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
     const bf16_t* qp = (const bf16_t*)a.q + (int64_t)(b * a.n_q_heads + qh) * a.q_head_stride + (int64_t)qi * D;
 #pragma unroll
     for (int s = 0; s < KSTEPS; ++s) {
-      const u32x4 raw = row_ok ? *(const u32x4*)(qp + 16 * s + 8 * gsel) : u32x4{0, 0, 0, 0};
+      u32x4 raw = row_ok ? *(const u32x4*)(qp + 16 * s + 8 * gsel) : u32x4{0, 0, 0, 0};
+      if (remap) {
+        // memory parts: the query turned by R(l_L); local parts: at its own position
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          const int pr = 8 * s + 4 * gsel + j;  // the pair held in word j
+          float cs, sn;
+          if (mem_part) {
+            cs = a.rope.mem_cos[pr];
+            sn = a.rope.mem_sin[pr];
+          } else {
+            rope_cos_sin(a.rope, geo.past_len + qi, pr, cs, sn);
+          }
+          const float x0 = __uint_as_float(raw[j] << 16), x1 = __uint_as_float(raw[j] & 0xFFFF0000u);
+          raw[j] = (uint32_t)f32_to_bf16(x0 * cs - x1 * sn) | ((uint32_t)f32_to_bf16(x0 * sn + x1 * cs) << 16);
+        }
+      }
       qreg[s] = __builtin_bit_cast(bf16x8, raw);
     }
   }
@@ -334,10 +370,10 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
     }
   };
   // Mask of tile t: key kl is visible to query qi iff its virtual index is at
-  // most v_x0 + qi (causal within X; also excludes the ragged end) and, with
-  // skipped unit entries present, its kvalid flag (K buffer kbuf) is set.
+  // most vlim and, with skipped unit entries present, its kvalid flag (K buffer
+  // kbuf) is set.
   auto apply_mask = [&](int t, int kbuf, f32x16 (&sacc)[2]) {
-    const int lim = v_x0 + qi - t * KB - 4 * gsel;
+    const int lim = vlim - t * KB - 4 * gsel;
     uint32_t kv[4][2];
     if (has_invalid) {
 #pragma unroll
@@ -432,7 +468,7 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
   // looked up at the end of an iteration, so their scalar loads complete under
   // the barrier.
   // Tiles wholly before X need no mask unless skipped unit entries exist.
-  const int t_plain = has_invalid ? t_begin : max(t_begin, min(t_end, v_x0 / KB));
+  const int t_plain = has_invalid ? t_begin : max(t_begin, min(t_end, (mem_part ? a.mem_len : v_x0) / KB));
   int64_t run_k = -1, run_v = -1;  // run starts of the next K and V loads: tiles t+3, t+2
   // Run starts of the part's tiles, computed once by all lanes into LDS; the
   // per-iteration lookup is then an LDS read (a global read here would wait
@@ -509,7 +545,7 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
       constexpr bool MASK = decltype(mask_next)::value;
       const uint32_t vaddr = vaddr_of(bc);
       auto vfrag = [&](int db, int j) { return vfrag_at(vaddr, db, j); };
-      const int lim = v_x0 + qi - (t + 1) * KB - 4 * gsel;  // mask bound of tile t+1
+      const int lim = vlim - (t + 1) * KB - 4 * gsel;  // mask bound of tile t+1
       uint32_t kv[4][2];
       if (MASK && has_invalid) {
 #pragma unroll
@@ -574,6 +610,15 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
     publish_barrier<4 * NI>();  // K(t0) has landed
     qk(0, sA);
     if (t_begin >= t_plain) apply_mask(t_begin, 0, sA);
+    if (!mem_part && a.parts_mem > 0 && t_begin * KB < a.mem_len) {
+      // the first local tile also holds the last memory keys: hide them here
+      const int lo = a.mem_len - t_begin * KB - 4 * gsel;
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int j = 0; j < 16; ++j)
+          if (32 * kb + 8 * (j >> 2) + (j & 3) < lo) sA[kb][j] = -__builtin_inff();
+    }
     update_max(tile_max(sA));
 
     int t = t_begin;

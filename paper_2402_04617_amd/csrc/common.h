@@ -71,6 +71,30 @@ __device__ __forceinline__ int64_t virtual_pos(const StepGeom& g, const int32_t*
   return g.local_begin + (w - sel_len);
 }
 
+// Positional remap (Section 3.2, "Positional Encoding"): rotary tables for a
+// step whose q and k arrive without positions.  Dimension pair i = (2i, 2i+1)
+// turns by the angle p * theta_i.  Keys of I and of the memory units are kept
+// unrotated and met by queries turned by R(l_L) (distance l_L); keys of L and X
+// are rotated to their own positions and met by queries at theirs.
+constexpr int kMaxPairs = 64;  // D/2 at D = 128
+struct RopeArgs {
+  int32_t on;                // 0: positions pre-applied, nothing is rotated
+  double rev[kMaxPairs];     // theta_i / (2 pi): revolutions per position of pair i
+  float mem_cos[kMaxPairs];  // cos(l_L theta_i)
+  float mem_sin[kMaxPairs];  // sin(l_L theta_i)
+};
+
+// cos and sin of p * theta_i.  The angle is reduced to [0, 1) revolutions in
+// float64 (p * theta_i reaches 10^6 radians at a million positions); the
+// hardware sine and cosine take revolutions.
+__device__ __forceinline__ void rope_cos_sin(const RopeArgs& r, int64_t pos, int i, float& c, float& s) {
+  double t = (double)pos * r.rev[i];
+  t -= floor(t);
+  const float f = (float)t;
+  s = __builtin_amdgcn_sinf(f);
+  c = __builtin_amdgcn_cosf(f);
+}
+
 // XCD-aware workgroup order: consecutive logical ids land on the same XCD (and so
 // share its L2), given round-robin dispatch of linear ids over the XCDs.
 __device__ __forceinline__ int xcd_logical_block(int linear, int total) {

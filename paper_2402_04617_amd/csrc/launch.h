@@ -21,6 +21,8 @@ struct AppendArgs {
   void* v_store;
   double* qprefix;
   double* rpart;  // [B*Hkv][D/16][ring] partial representative scores
+  void* k_rot;    // positional remap: keys rotated to their own positions (same layout as k_store)
+  RopeArgs rope;
   bool bf16;
 };
 struct BuildArgs;
@@ -49,6 +51,7 @@ struct ScoreArgs {
   const float* unit_ksum;
   float* scores;
   float* qbar_parts;  // workspace
+  RopeArgs rope;      // positional remap: the query sum is turned by R(l_L)
   bool bf16;
 };
 int score_qbar_parts(int G, int n_q);
@@ -79,6 +82,15 @@ struct AttendArgs {
   const void* q;
   const void* k_store;
   const void* v_store;
+  // Positional remap: parts [0, parts_mem) cover the memory keys (virtual
+  // indices [0, mem_len): I and the selected units) with unrotated keys from
+  // k_store and queries turned by R(l_L); parts [parts_mem, parts) cover L and X
+  // with keys from k_rot and queries at their own positions.  Without the remap
+  // parts_mem = 0 and every part reads k_store.
+  const void* k_rot;
+  int parts_mem;
+  int mem_len;
+  RopeArgs rope;
   const int32_t* idx;
   void* out;     // final output (one part)
   float* lse;    // nullable

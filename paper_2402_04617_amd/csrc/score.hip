@@ -2,7 +2,8 @@
 //
 // sim(X, B) = sum_i sum_j q_{i+l_P} . k_{b_j} is bilinear, so per kv head it is
 // Qbar . Kbar_B with Qbar the sum of the group's current queries and Kbar_B the
-// sum of the unit's representative keys (kept by unit construction).  Two
+// sum of the unit's representative keys (kept by unit construction).  Qbar is the
+// sum of the queries as given (unrotated when the positional remap is on).  Two
 // kernels: a reduction of the chunk's queries into per-part partial sums
 // (deterministic order), then one streaming pass over the Kbar table (fp32,
 // unit-contiguous 16-byte cells) at HBM rate.
@@ -53,10 +54,14 @@ __global__ void __launch_bounds__(256) qbar_kernel(const T* __restrict__ q, int6
   }
 }
 
-// grid (ceil(n_units/256), batch*Hkv); one unit per thread.
+// grid (ceil(n_units/256), batch*Hkv); one unit per thread.  With the
+// positional remap the memory keys sit at distance l_L from every current token,
+// so the query sum is turned by R(l_L) before the dot products (the keys stay
+// unrotated).
 __global__ void __launch_bounds__(256) score_kernel(const float* __restrict__ qbar_parts, int parts,
                                                     const float4* __restrict__ unit_ksum, int head_dim,
-                                                    int n_units, int max_units, float* __restrict__ scores) {
+                                                    int n_units, int max_units, float* __restrict__ scores,
+                                                    const RopeArgs rope) {
   const int bg = blockIdx.y;
   __shared__ float qbar[256];
   for (int d = threadIdx.x; d < head_dim; d += 256) {
@@ -65,6 +70,22 @@ __global__ void __launch_bounds__(256) score_kernel(const float* __restrict__ qb
     qbar[d] = s;
   }
   __syncthreads();
+  if (rope.on) {
+    const int i = threadIdx.x;
+    float x0 = 0.f, x1 = 0.f, c = 1.f, sn = 0.f;
+    if (i < head_dim / 2) {
+      x0 = qbar[2 * i];
+      x1 = qbar[2 * i + 1];
+      c = rope.mem_cos[i];
+      sn = rope.mem_sin[i];
+    }
+    __syncthreads();
+    if (i < head_dim / 2) {
+      qbar[2 * i] = x0 * c - x1 * sn;
+      qbar[2 * i + 1] = x0 * sn + x1 * c;
+    }
+    __syncthreads();
+  }
   const int u = blockIdx.x * 256 + threadIdx.x;
   if (u >= n_units) return;
   const int nc = head_dim / 4;
@@ -104,7 +125,7 @@ hipError_t launch_score_given_qbar(const ScoreArgs& a, int parts, hipStream_t s)
   if (a.n_units == 0) return hipSuccess;
   dim3 g2((a.n_units + 255) / 256, a.batch * a.n_kv_heads);
   hipLaunchKernelGGL(score_kernel, g2, dim3(256), 0, s, (const float*)a.qbar_parts, parts,
-                     (const float4*)a.unit_ksum, a.head_dim, a.n_units, a.max_units, a.scores);
+                     (const float4*)a.unit_ksum, a.head_dim, a.n_units, a.max_units, a.scores, a.rope);
   return hipGetLastError();
 }
 

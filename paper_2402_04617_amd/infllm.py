@@ -36,14 +36,19 @@ class Params(ctypes.Structure):
     _fields_ = [("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("n_init", ctypes.c_int32), ("n_local", ctypes.c_int32), ("block_size", ctypes.c_int32),
                 ("n_repr", ctypes.c_int32), ("topk", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("sm_scale", ctypes.c_float)]
+                ("sm_scale", ctypes.c_float), ("rope_inv_freq", ctypes.POINTER(ctypes.c_double))]
+
+    @property
+    def remap(self) -> bool:
+        """Positional remap on (rotary frequencies given)."""
+        return bool(self.rope_inv_freq)
 
 
 class Memory(ctypes.Structure):
     _fields_ = [("batch", ctypes.c_int32), ("capacity", ctypes.c_int64), ("k", ctypes.c_void_p),
                 ("v", ctypes.c_void_p), ("max_units", ctypes.c_int32), ("repr_idx", ctypes.c_void_p),
                 ("unit_ksum", ctypes.c_void_p), ("qprefix", ctypes.c_void_p), ("rpart", ctypes.c_void_p),
-                ("ring", ctypes.c_int32)]
+                ("ring", ctypes.c_int32), ("k_rot", ctypes.c_void_p)]
 
 
 _lib = None
@@ -191,12 +196,28 @@ class LayerMemory:
     qprefix: "object"
     rpart: "object"
     struct: Memory
+    k_rot: "object" = None
+
+
+_rope_tables = {}  # keeps each Params' frequency array alive (the struct holds a raw pointer)
 
 
 def params(n_q_heads, n_kv_heads, head_dim, n_init, n_local, block_size, n_repr, topk, dtype="bf16",
-           sm_scale=1.0) -> Params:
-    return Params(n_q_heads, n_kv_heads, head_dim, n_init, n_local, block_size, n_repr, topk,
-                  INFLLM_BF16 if dtype == "bf16" else INFLLM_F32, sm_scale)
+           sm_scale=1.0, rope_inv_freq=None) -> Params:
+    """Method parameters.  rope_inv_freq: None (positions pre-applied) or the D/2 rotary angular
+    frequencies of the positional remap."""
+    p = Params(n_q_heads, n_kv_heads, head_dim, n_init, n_local, block_size, n_repr, topk,
+               INFLLM_BF16 if dtype == "bf16" else INFLLM_F32, sm_scale)
+    if rope_inv_freq is not None:
+        table = (ctypes.c_double * len(rope_inv_freq))(*[float(x) for x in rope_inv_freq])
+        _rope_tables[ctypes.addressof(p)] = table
+        p.rope_inv_freq = ctypes.cast(table, ctypes.POINTER(ctypes.c_double))
+    return p
+
+
+def rope_frequencies(head_dim: int, base: float = 500000.0):
+    """theta_i = base^(-2i/D), i < D/2 (the usual rotary frequencies; base 500000 as in Llama 3)."""
+    return [base ** (-2.0 * i / head_dim) for i in range(head_dim // 2)]
 
 
 def alloc_memory(p: Params, batch: int, capacity: int, max_units: int, ring: int, device="cuda") -> LayerMemory:
@@ -210,9 +231,11 @@ def alloc_memory(p: Params, batch: int, capacity: int, max_units: int, ring: int
     unit_ksum = torch.zeros((batch, p.n_kv_heads, D // 4, mu, 4), dtype=torch.float32, device=device)
     qprefix = torch.zeros((batch, p.n_kv_heads, ring, D), dtype=torch.float64, device=device)
     rpart = torch.zeros((batch, p.n_kv_heads, D // 16, ring), dtype=torch.float64, device=device)
+    k_rot = torch.zeros_like(k) if p.remap else None
     st = Memory(batch, capacity, k.data_ptr(), v.data_ptr(), max_units, repr_idx.data_ptr(),
-                unit_ksum.data_ptr(), qprefix.data_ptr(), rpart.data_ptr(), ring)
-    return LayerMemory(k, v, repr_idx, unit_ksum, qprefix, rpart, st)
+                unit_ksum.data_ptr(), qprefix.data_ptr(), rpart.data_ptr(), ring,
+                k_rot.data_ptr() if k_rot is not None else None)
+    return LayerMemory(k, v, repr_idx, unit_ksum, qprefix, rpart, st, k_rot)
 
 
 def recommended_ring(p: Params, chunk: int) -> int:

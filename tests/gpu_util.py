@@ -33,8 +33,9 @@ def host(t: torch.Tensor) -> np.ndarray:
 
 
 def oparams(p: F.Params) -> O.Params:
+    freqs = tuple(float(p.rope_inv_freq[i]) for i in range(p.head_dim // 2)) if p.remap else None
     return O.Params(p.n_q_heads, p.n_kv_heads, p.head_dim, p.n_init, p.n_local, p.block_size, p.n_repr,
-                    p.topk, float(p.sm_scale))
+                    p.topk, float(p.sm_scale), freqs)
 
 
 class Layer:
@@ -74,7 +75,8 @@ class Layer:
         B, Hq, Hkv = self.batch, self.p.n_q_heads, self.p.n_kv_heads
         return {
             "out": host(self.out[:, :, :n]).astype(np.float64),
-            "lse": host(self.lse[:, :, :n]).astype(np.float64),
+            # lse is written compact, [batch][Hq][n] (no head stride), also for a short last chunk
+            "lse": host(self.lse.reshape(-1)[: B * Hq * n].reshape(B, Hq, n)).astype(np.float64),
             "scores": host(self.scores[: B * Hkv * n_units]).reshape(B, Hkv, n_units).astype(np.float64),
             "idx": host(self.idx).astype(np.int64),
         }

@@ -199,6 +199,40 @@ def test_step_validation(L):
     assert f(bp, bm, FAKE, S, None, None, 0, 512, 8192, 31, None, FAKE, FAKE, S, None, FAKE, 1 << 30, None) == 1
 
 
+def test_remap_validation(L):
+    """Positional remap: frequencies must be finite and non-negative; the rotated-key store is
+    required; memory keys and local keys take separate parts, so attention with I or units
+    present needs a workspace; the workspace size leaves room for two parts."""
+    S = 512 * 128
+    good = F.rope_frequencies(128)
+    m = mem()
+    for bad in (float("nan"), float("inf"), -1e-3):
+        f = list(good)
+        f[7] = bad
+        p = P(rope_inv_freq=f)
+        n0, n1, n2 = ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int64()
+        assert L.infllm_partition(ctypes.byref(p), 100, ctypes.byref(n0), ctypes.byref(n1), ctypes.byref(n2)) == 2
+    p = P(rope_inv_freq=good)
+    bp = ctypes.byref(p)
+    # k_rot missing
+    assert L.infllm_append(bp, ctypes.byref(m), FAKE, S, FAKE, FAKE, S, 512, 0, None) == 1
+    assert L.infllm_chunk_attend(bp, ctypes.byref(m), FAKE, S, 512, 8192, FAKE, 32, FAKE, S, None, FAKE,
+                                 1 << 30, None) == 1
+    mr = mem(k_rot=FAKE + 8)
+    assert L.infllm_append(bp, ctypes.byref(mr), FAKE, S, FAKE, FAKE, S, 512, 0, None) == 2  # misaligned
+    mr = mem(k_rot=FAKE)
+    bm = ctypes.byref(mr)
+    # no workspace while memory keys exist
+    assert L.infllm_chunk_attend(bp, bm, FAKE, S, 512, 8192, FAKE, 32, FAKE, S, None, None, 0, None) == 5
+    # a one-part workspace is not enough either
+    row = 2 * 128 + 8
+    assert L.infllm_chunk_attend(bp, bm, FAKE, S, 512, 8192, FAKE, 32, FAKE, S, None, FAKE,
+                                 32 * 512 * row, None) == 5
+    assert L.infllm_workspace_bytes(bp, 1, 1) >= 2 * 32 * row
+    pd = P(rope_inv_freq=good, n_init=0, n_local=64, block_size=16, topk=2)
+    assert L.infllm_workspace_bytes(ctypes.byref(pd), 1, 1) >= 2 * 32 * row
+
+
 @pytest.mark.skipif(os.path.exists("/dev/kfd") and os.access("/dev/kfd", os.R_OK),
                     reason="a GPU may be present; valid arguments would launch on fake pointers")
 def test_valid_arguments_without_gpu_report_device_error(L):
