@@ -18,6 +18,7 @@ the 128K stream with the positional remap of Section 3.2.
 from __future__ import annotations
 
 import argparse
+import dataclasses
 import hashlib
 import json
 import os
@@ -233,11 +234,15 @@ def time_steps(torch, fn, steps, warmup):
     return t0.elapsed_time(t1) / steps
 
 
-def encode_leg(name, seed, steps, warmup, torch, want_roofline=True, remap=False, inputs=None):
+def encode_leg(name, seed, steps, warmup, torch, want_roofline=True, remap=False, inputs=None, **method):
+    """One encode stream of workload `name`; `method` overrides method parameters (block_size,
+    n_repr, topk, chunk) on the same inputs."""
     from workload import WORKLOADS, Synth
     wl = WORKLOADS[name]
+    if method:
+        wl = dataclasses.replace(wl, **method)
     t = time.time()
-    synth = Synth(wl, seed)
+    synth = Synth(WORKLOADS[name], seed)
     if inputs is None:
         inputs = upload_inputs(synth, torch)
         log(f"{name}: inputs resident in HBM ({time.time() - t:.1f}s)")
@@ -246,6 +251,8 @@ def encode_leg(name, seed, steps, warmup, torch, want_roofline=True, remap=False
     ms = time_steps(torch, lambda: st.run(plan), steps, warmup)
     res = {"workload": name + ("+remap" if remap else ""), "seq_len": wl.seq_len, "ms_per_step": ms,
            "ctx_tok_per_s": wl.seq_len * wl.batch / (ms / 1e3)}
+    if method:
+        res["method"] = {"block_size": wl.block_size, "n_repr": wl.n_repr, "topk": wl.topk, "chunk": wl.chunk}
     if want_roofline:
         # one more (untimed) pass recording the lookup of every chunk, then the attention replay
         idx_hist = torch.zeros((len(plan),) + tuple(st.idx.shape), dtype=torch.int32, device="cuda")
@@ -316,14 +323,38 @@ def cpu_baseline(synth, n_chunk_samples=64):
             "sample_seconds": t_units + t_chunks}
 
 
+# Memory settings of the paper's studies of them: representative tokens r_k, selected units
+# k_m, and unit size l_bs with the total context held at 12K (4K local + 8K selected).
+SWEEP = ([{"n_repr": r} for r in (1, 2, 4, 8)]
+         + [{"topk": k} for k in (2, 4, 8, 16, 32, 64, 96, 128)]
+         + [{"block_size": b, "topk": 8192 // b} for b in (32, 64, 128, 256)])
+
+
+def sweep(seed, steps, warmup, torch):
+    """128K stream under each memory setting of SWEEP (same inputs): one JSON line per setting."""
+    base, _, st = encode_leg("llama3-8b-128k", seed, steps, warmup, torch)
+    inputs = st.inp
+    del st
+    for m in SWEEP:
+        r, _, s2 = encode_leg("llama3-8b-128k", seed, steps, warmup, torch, inputs=inputs, **m)
+        del s2
+        torch.cuda.empty_cache()
+        a = r["attention"]
+        print(json.dumps({"sweep": r["method"], "ms_per_step": r["ms_per_step"], "ctx_tok_per_s": r["ctx_tok_per_s"],
+                          "attention_us_per_launch": a["avg_ms"] * 1e3, "attention_tflops": a["tflops"],
+                          "attention_ms_per_step": a["total_ms"]}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser(description=__doc__)
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--legs", default="1m,decode,remap",
-                    help="extra legs: comma list of 1m, decode, remap (or 'none')")
+    ap.add_argument("--legs", default="1m,1m-paper,decode,remap",
+                    help="extra legs: comma list of 1m, 1m-paper, decode, remap (or 'none')")
+    ap.add_argument("--sweep", action="store_true",
+                    help="only time the 128K stream under the paper's memory settings (r_k, k_m, l_bs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run the plain-copy calibration dispatch of MIB MiB (for the traffic counters)")
@@ -343,6 +374,9 @@ def main():
     from paper_2402_04617_amd import infllm as F
     F.lib()
     torch.cuda.set_device(0)
+    if args.sweep:
+        sweep(args.seed, args.steps, args.warmup, torch)
+        return
 
     main_res, synth, st = encode_leg("llama3-8b-128k", args.seed, args.steps, args.warmup, torch)
     log(f"128K: {main_res['ms_per_step']:.2f} ms/step, {main_res['ctx_tok_per_s'] / 1e6:.2f}M ctx tok/s; "
@@ -359,12 +393,21 @@ def main():
             f"attention {rr['attention']['tflops']:.0f} TFLOP/s")
     del st
     torch.cuda.empty_cache()
-    if "1m" in legs:
+    if "1m" in legs or "1m-paper" in legs:
         r1, _, st1 = encode_leg("llama3-8b-1m", args.seed, max(1, min(args.steps, 2)), 1, torch)
+        if "1m" in legs:
+            extra["encode_1m"] = r1
+            log(f"1M: {r1['ms_per_step']:.1f} ms/step, {r1['ctx_tok_per_s'] / 1e6:.2f}M ctx tok/s")
+        if "1m-paper" in legs:
+            # the paper's settings for its 1,024K run: 2048-token chunks, one representative token
+            rp, _, st2 = encode_leg("llama3-8b-1m", args.seed, max(1, min(args.steps, 2)), 1, torch,
+                                    inputs=st1.inp, chunk=2048, n_repr=1)
+            del st2
+            extra["encode_1m_paper_settings"] = rp
+            log(f"1M (chunk 2048, r_k 1): {rp['ms_per_step']:.1f} ms/step, "
+                f"{rp['ctx_tok_per_s'] / 1e6:.2f}M ctx tok/s")
         del st1
         torch.cuda.empty_cache()
-        extra["encode_1m"] = r1
-        log(f"1M: {r1['ms_per_step']:.1f} ms/step, {r1['ctx_tok_per_s'] / 1e6:.2f}M ctx tok/s")
     if "decode" in legs:
         rd = decode_leg(args.seed, max(1, min(args.steps, 3)), 1, torch)
         torch.cuda.empty_cache()

@@ -232,6 +232,19 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
     const int bu = u < kSelLds ? sm.sidx[u] : idx_row[u];
     return (int64_t)geo.unit_base + (int64_t)bu * geo.block_size + (w - u * geo.block_size);
   };
+  // Store position of virtual key v (-1: skipped unit entry), with the lookup
+  // entry read from LDS: on the per-key path of tiles that span several runs a
+  // global read would wait behind the tile loads in flight.
+  auto vpos = [&](int v) -> int64_t {
+    if (v < geo.n_init) return v;
+    const int w = v - geo.n_init;
+    const int sel_len = geo.n_sel * geo.block_size;
+    if (w >= sel_len) return geo.local_begin + (w - sel_len);
+    const int u = w / geo.block_size;
+    const int bu = u < kSelLds ? sm.sidx[u] : idx_row[u];
+    if (bu < 0 || bu >= geo.n_units) return -1;
+    return (int64_t)geo.unit_base + (int64_t)bu * geo.block_size + (w - u * geo.block_size);
+  };
   auto uniform64 = [](int64_t x) -> int64_t {
     return ((int64_t)__builtin_amdgcn_readfirstlane((int)(x >> 32)) << 32) |
            (uint32_t)__builtin_amdgcn_readfirstlane((int)(uint32_t)x);
@@ -267,7 +280,7 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
       for (int j = 0; j < NI; ++j) {
         const int r = lrow0 + RPI * j;
         const int v = tile * KB + r;
-        int64_t pos = v < geo.n_virtual ? virtual_pos(geo, idx_row, v) : -1;
+        int64_t pos = v < geo.n_virtual ? vpos(v) : -1;
         if (IS_K && lane % CH == 0) sm.kvalid[buf][r] = pos >= 0;
         pos = pos >= 0 ? pos : 0;
         lds_load_lane(ld + j * 1024, base + pos * D + 8 * (lgran0 ^ (XJ * j)));
@@ -290,7 +303,7 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
       for (int j = 0; j < NI; ++j) {
         const int r = lrow0 + RPI * j;
         const int v = tile * KB + r;
-        int64_t pos = v < geo.n_virtual ? virtual_pos(geo, idx_row, v) : -1;
+        int64_t pos = v < geo.n_virtual ? vpos(v) : -1;
         if (is_k && lane % CH == 0) sm.kvalid[buf][r] = pos >= 0;
         pos = pos >= 0 ? pos : 0;
         off[j] = (uint32_t)pos * (2u * D) + 16u * (lgran0 ^ (XJ * j));

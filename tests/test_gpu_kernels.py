@@ -180,6 +180,7 @@ ATTEND_CASES = [
     ("bf16", 4, 2, 128, 128, 512, 128, 4, 3000, 512, 1),
     ("bf16", 4, 2, 128, 128, 512, 128, 4, 3000, 77, 1),     # ragged rows
     ("bf16", 4, 8, 128, 128, 4096, 128, 32, 20000, 512, 1),  # real shape, several key parts
+    ("bf16", 4, 8, 128, 128, 4096, 128, 32, 20000, 2048, 1),  # 2048-token chunk: one key part
     ("bf16", 1, 2, 128, 16, 256, 32, 4, 1500, 64, 2),
     ("bf16", 8, 1, 64, 5, 100, 16, 7, 900, 100, 1),
     ("bf16", 2, 2, 64, 0, 50, 20, 3, 400, 130, 1),          # no initial tokens, l_bs not a power of 2

@@ -91,6 +91,17 @@ def test_stream_mistral32k_sampled_steps(seed):
     run_and_check(wl, seed, {0, 1, 9, 17, 33, n - 2, n - 1}, q, k, v)
 
 
+def test_stream_paper_1m_settings():
+    """The paper's settings for its 1,024K run (2048-token chunks, one representative token) on the
+    Mistral-7B shape: append scans of four tiles, single-part attention over 8,192 rows per kv head."""
+    import dataclasses
+    wl = dataclasses.replace(WORKLOADS["mistral7b-32k"], chunk=2048, n_repr=1)
+    s = Synth(wl, 3)
+    q, k, v = s.full("q"), s.full("k"), s.full("v")
+    n = len(wl.step_starts())
+    run_and_check(wl, 3, {0, 3, 8, n - 1}, q, k, v)
+
+
 def test_stream_deterministic_mistral32k():
     wl = WORKLOADS["mistral7b-32k"]
     s = Synth(wl, 2)
