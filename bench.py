@@ -139,22 +139,24 @@ def attention_bytes(wl, steps, parts):
     return total
 
 
-def params_of(wl, remap=False):
+def params_of(wl, remap=False, mean_repr=False):
     """Method parameters of a workload; remap=True adds the positional remap with Llama-3 rotary
-    frequencies (the synthetic q and k are then read as unrotated)."""
+    frequencies (the synthetic q and k are then read as unrotated); mean_repr=True scores units by
+    their mean key."""
     from paper_2402_04617_amd import infllm as F
     return F.params(wl.n_q_heads, wl.n_kv_heads, wl.head_dim, wl.n_init, wl.n_local, wl.block_size,
                     wl.n_repr, wl.topk, wl.dtype,
-                    rope_inv_freq=F.rope_frequencies(wl.head_dim) if remap else None)
+                    rope_inv_freq=F.rope_frequencies(wl.head_dim) if remap else None,
+                    repr_mode="mean" if mean_repr else "tokens")
 
 
 class Stream:
     """Device state of one layer over a sequence, stepped through infllm_step."""
 
-    def __init__(self, wl, inputs, torch, remap=False):
+    def __init__(self, wl, inputs, torch, remap=False, mean_repr=False):
         from paper_2402_04617_amd import infllm as F
         self.F, self.torch, self.wl = F, torch, wl
-        self.p = params_of(wl, remap)
+        self.p = params_of(wl, remap, mean_repr)
         self.inp = inputs
         S, D = wl.seq_len, wl.head_dim
         self.max_units = max(1, F.infllm_partition(self.p, S)[1])
@@ -234,7 +236,8 @@ def time_steps(torch, fn, steps, warmup):
     return t0.elapsed_time(t1) / steps
 
 
-def encode_leg(name, seed, steps, warmup, torch, want_roofline=True, remap=False, inputs=None, **method):
+def encode_leg(name, seed, steps, warmup, torch, want_roofline=True, remap=False, inputs=None, mean_repr=False,
+               **method):
     """One encode stream of workload `name`; `method` overrides method parameters (block_size,
     n_repr, topk, chunk) on the same inputs."""
     from workload import WORKLOADS, Synth
@@ -246,10 +249,11 @@ def encode_leg(name, seed, steps, warmup, torch, want_roofline=True, remap=False
     if inputs is None:
         inputs = upload_inputs(synth, torch)
         log(f"{name}: inputs resident in HBM ({time.time() - t:.1f}s)")
-    st = Stream(wl, inputs, torch, remap)
+    st = Stream(wl, inputs, torch, remap, mean_repr)
     plan = wl.step_starts()
     ms = time_steps(torch, lambda: st.run(plan), steps, warmup)
-    res = {"workload": name + ("+remap" if remap else ""), "seq_len": wl.seq_len, "ms_per_step": ms,
+    res = {"workload": name + ("+remap" if remap else "") + ("+mean-repr" if mean_repr else ""),
+           "seq_len": wl.seq_len, "ms_per_step": ms,
            "ctx_tok_per_s": wl.seq_len * wl.batch / (ms / 1e3)}
     if method:
         res["method"] = {"block_size": wl.block_size, "n_repr": wl.n_repr, "topk": wl.topk, "chunk": wl.chunk}
@@ -351,8 +355,8 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--legs", default="1m,1m-paper,decode,remap",
-                    help="extra legs: comma list of 1m, 1m-paper, decode, remap (or 'none')")
+    ap.add_argument("--legs", default="1m,1m-paper,decode,remap,mean",
+                    help="extra legs: comma list of 1m, 1m-paper, decode, remap, mean (or 'none')")
     ap.add_argument("--sweep", action="store_true",
                     help="only time the 128K stream under the paper's memory settings (r_k, k_m, l_bs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -391,6 +395,13 @@ def main():
         extra["encode_128k_remap"] = rr
         log(f"128K remap: {rr['ms_per_step']:.2f} ms/step, {rr['ctx_tok_per_s'] / 1e6:.2f}M ctx tok/s; "
             f"attention {rr['attention']['tflops']:.0f} TFLOP/s")
+    if "mean" in legs:
+        # the same 128K stream with units represented by their mean key
+        rm, _, st_m = encode_leg("llama3-8b-128k", args.seed, args.steps, args.warmup, torch, mean_repr=True,
+                                 inputs=st.inp)
+        del st_m
+        extra["encode_128k_mean_repr"] = rm
+        log(f"128K mean repr: {rm['ms_per_step']:.2f} ms/step, {rm['ctx_tok_per_s'] / 1e6:.2f}M ctx tok/s")
     del st
     torch.cuda.empty_cache()
     if "1m" in legs or "1m-paper" in legs:

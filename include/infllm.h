@@ -50,6 +50,11 @@ typedef enum {
 
 typedef enum { INFLLM_F32 = 0, INFLLM_BF16 = 1 } infllm_dtype;
 
+/* Unit representation (Section 3.2): the r_k representative tokens of highest
+ * representative score (the method), or the mean of all l_bs keys of the unit
+ * (the "Mean Repr" alternative the paper evaluates in its ablation, Section 4). */
+typedef enum { INFLLM_REPR_TOKENS = 0, INFLLM_REPR_MEAN = 1 } infllm_repr_mode;
+
 /* Method parameters (Sections 3.1-3.2; the paper's symbols in comments). */
 typedef struct {
   int32_t n_q_heads;  /* Hq: query heads; Hq % Hkv == 0.  Query head h reads kv head h / (Hq/Hkv). */
@@ -76,6 +81,12 @@ typedef struct {
    * Half-split pairs (i, i + D/2) are the same model after one fixed permutation
    * of the head dimensions of q and k.  Needs memory.k_rot. */
   const double* rope_inv_freq;
+  /* infllm_repr_mode.  With INFLLM_REPR_MEAN a unit is scored by the mean of its
+   * keys, sim(X, B) = sum_i q_{i+l_P} . mean_j k_j^B: unit_ksum holds that mean,
+   * repr_idx is neither written nor needed, n_repr is ignored, and no
+   * representative scores are formed, so qprefix and rpart are not used (NULL
+   * allowed) and the append only stores K and V. */
+  int32_t repr_mode;
 } infllm_params;
 
 /*

@@ -43,6 +43,9 @@ class Params:
     # Rotary angular frequencies theta_i (radians per position) of the D/2 dimension
     # pairs (2i, 2i+1) for the positional remap; None: positions pre-applied.
     rope_inv_freq: Optional[Tuple[float, ...]] = None
+    # Units represented by the mean of their keys (the "Mean Repr" alternative of
+    # Section 4) instead of r_k representative tokens.
+    mean_repr: bool = False
 
     @property
     def group(self) -> int:
@@ -174,6 +177,17 @@ def unit_relevance(q_chunk_group: np.ndarray, k_head: np.ndarray, rep_pos: np.nd
     keys = np.asarray(k_head[rep_pos.reshape(-1)], dtype=np.float64)        # every (unit, j)
     dots = qx @ keys.T                                                        # all q_i . k_{b_j}
     return dots.reshape(qx.shape[0], rep_pos.shape[0], rep_pos.shape[1]).sum(axis=(0, 2))
+
+
+def mean_relevance(q_chunk_group: np.ndarray, k_head: np.ndarray, n_units: int, p: Params) -> np.ndarray:
+    """sim(X, B) = sum_{i=1..l_X} q_{i+l_P} . mean_{j=1..l_bs} k^B_j for every unit B: the unit
+    represented by the mean of its keys (the "Mean Repr" alternative evaluated in Section 4),
+    summed over the query heads of the group like unit_relevance, and with the positional
+    remap taken the same way.  Returns float64 [n_units]."""
+    if n_units == 0:
+        return np.zeros(0)
+    pos = np.stack([np.arange(unit_start(u, p), unit_start(u, p) + p.block_size) for u in range(n_units)])
+    return unit_relevance(q_chunk_group, k_head, pos, p) / p.block_size
 
 
 def select_units(sim: np.ndarray, p: Params, k: Optional[int] = None) -> np.ndarray:
@@ -315,7 +329,10 @@ class StreamOracle:
         out = np.zeros((p.n_kv_heads, nu))
         for g in range(p.n_kv_heads):
             qx = self.q[b, g * G:(g + 1) * G, past_len:past_len + n_q]
-            out[g] = unit_relevance(qx, self.k[b, g], self.rep_positions(b, g, nu), p)
+            if p.mean_repr:
+                out[g] = mean_relevance(qx, self.k[b, g], nu, p)
+            else:
+                out[g] = unit_relevance(qx, self.k[b, g], self.rep_positions(b, g, nu), p)
         return out
 
     def step(self, b: int, past_len: int, n_q: int, sel: Optional[np.ndarray] = None) -> dict:

@@ -54,6 +54,7 @@ infllm_status check_params(const infllm_params* p) {
   if (p->block_size > 256) return INFLLM_E_UNSUPPORTED;
   if (p->n_repr < 1 || p->n_repr > p->block_size) return INFLLM_E_SHAPE;
   if (!std::isfinite(p->sm_scale) || !(p->sm_scale > 0.f)) return INFLLM_E_SHAPE;
+  if (p->repr_mode != INFLLM_REPR_TOKENS && p->repr_mode != INFLLM_REPR_MEAN) return INFLLM_E_SHAPE;
   if (p->rope_inv_freq != nullptr) {
     for (int i = 0; i < p->head_dim / 2; ++i)
       if (!std::isfinite(p->rope_inv_freq[i]) || p->rope_inv_freq[i] < 0.0) return INFLLM_E_SHAPE;
@@ -62,6 +63,8 @@ infllm_status check_params(const infllm_params* p) {
 }
 
 bool remap(const infllm_params* p) { return p->rope_inv_freq != nullptr; }
+// Units scored by their mean key: no representative scores, so no query ring.
+bool mean_repr(const infllm_params* p) { return p->repr_mode == INFLLM_REPR_MEAN; }
 
 // Rotary tables of the positional remap, formed in float64 on the host.
 RopeArgs rope_args(const infllm_params* p) {
@@ -90,8 +93,8 @@ infllm_status check_store(const infllm_params* p, const infllm_memory* m) {
   return INFLLM_OK;
 }
 
-infllm_status check_units(const infllm_memory* m) {
-  if (m->repr_idx == nullptr || m->unit_ksum == nullptr) return INFLLM_E_NULL;
+infllm_status check_units(const infllm_params* p, const infllm_memory* m) {
+  if ((m->repr_idx == nullptr && !mean_repr(p)) || m->unit_ksum == nullptr) return INFLLM_E_NULL;
   if (m->max_units < 0) return INFLLM_E_SHAPE;
   if (!aligned16(m->unit_ksum)) return INFLLM_E_SHAPE;
   return INFLLM_OK;
@@ -263,7 +266,8 @@ infllm_status prep_append(const infllm_params* p, const infllm_memory* m, const 
   infllm_status st;
   if ((st = check_params(p)) != INFLLM_OK) return st;
   if ((st = check_store(p, m)) != INFLLM_OK) return st;
-  if (m->qprefix == nullptr) return INFLLM_E_NULL;
+  const bool ring_used = !mean_repr(p);
+  if (ring_used && m->qprefix == nullptr) return INFLLM_E_NULL;
   if (n_q < 0 || past_len < 0) return INFLLM_E_SHAPE;
   if ((k == nullptr) != (v == nullptr)) return INFLLM_E_NULL;
   if (q == nullptr) return INFLLM_E_NULL;
@@ -271,10 +275,10 @@ infllm_status prep_append(const infllm_params* p, const infllm_memory* m, const 
   if (k != nullptr && ((st = check_rows(p, k, kv_head_stride, n_q)) != INFLLM_OK ||
                        (st = check_rows(p, v, kv_head_stride, n_q)) != INFLLM_OK))
     return st;
-  if (m->ring < 1 || m->ring <= n_q) return INFLLM_E_SHAPE;
+  if (ring_used && (m->ring < 1 || m->ring <= n_q)) return INFLLM_E_SHAPE;
   if (past_len + n_q > m->capacity) return INFLLM_E_RANGE;
-  if (m->rpart == nullptr) return INFLLM_E_NULL;
-  {
+  if (ring_used && m->rpart == nullptr) return INFLLM_E_NULL;
+  if (ring_used) {
     // Partial representative scores are formed for tokens t = p - l_L (t >= l_I) of
     // the appended positions p; the running sum at t must still be in the ring
     // after this chunk's slots are written, and the key of a token inside the
@@ -307,6 +311,7 @@ infllm_status prep_append(const infllm_params* p, const infllm_memory* m, const 
   a->rpart = m->rpart;
   a->k_rot = m->k_rot;
   a->rope = rope_args(p);
+  a->mean_repr = mean_repr(p);
   a->bf16 = p->dtype == INFLLM_BF16;
   return INFLLM_OK;
 }
@@ -316,16 +321,17 @@ infllm_status prep_build(const infllm_params* p, const infllm_memory* m, int32_t
   infllm_status st;
   if ((st = check_params(p)) != INFLLM_OK) return st;
   if ((st = check_store(p, m)) != INFLLM_OK) return st;
-  if ((st = check_units(m)) != INFLLM_OK) return st;
-  if (m->rpart == nullptr) return INFLLM_E_NULL;
-  if (first_unit < 0 || n_new < 0 || past_len < 0 || m->ring < 1) return INFLLM_E_SHAPE;
+  if ((st = check_units(p, m)) != INFLLM_OK) return st;
+  const bool ring_used = !mean_repr(p);
+  if (ring_used && m->rpart == nullptr) return INFLLM_E_NULL;
+  if (first_unit < 0 || n_new < 0 || past_len < 0 || (ring_used && m->ring < 1)) return INFLLM_E_SHAPE;
   if ((int64_t)first_unit + n_new > m->max_units) return INFLLM_E_RANGE;
   if (past_len > m->capacity) return INFLLM_E_RANGE;
   if (n_new > 0) {
     const int64_t m0 = (int64_t)p->n_init + (int64_t)first_unit * p->block_size;
     const int64_t m_last = (int64_t)p->n_init + ((int64_t)first_unit + n_new) * p->block_size - 1;
     if (m_last + p->n_local > past_len - 1) return INFLLM_E_RANGE;  // windows not appended yet: not evicted
-    if (m0 < past_len - m->ring) return INFLLM_E_RANGE;              // ring no longer holds the oldest slot
+    if (ring_used && m0 < past_len - m->ring) return INFLLM_E_RANGE;  // ring no longer holds the oldest slot
   }
   a->batch = m->batch;
   a->n_q_heads = p->n_q_heads;
@@ -345,6 +351,7 @@ infllm_status prep_build(const infllm_params* p, const infllm_memory* m, int32_t
   a->repr_idx = m->repr_idx;
   a->unit_ksum = m->unit_ksum;
   a->repr_score = repr_score;
+  a->mean_repr = mean_repr(p);
   a->bf16 = p->dtype == INFLLM_BF16;
   return INFLLM_OK;
 }
@@ -356,7 +363,7 @@ infllm_status prep_score(const infllm_params* p, const infllm_memory* m, const v
   if ((st = check_params(p)) != INFLLM_OK) return st;
   if (m == nullptr) return INFLLM_E_NULL;
   if (m->batch < 1) return INFLLM_E_SHAPE;
-  if ((st = check_units(m)) != INFLLM_OK) return st;
+  if ((st = check_units(p, m)) != INFLLM_OK) return st;
   if (n_q < 0 || n_units < 0) return INFLLM_E_SHAPE;
   if (n_units > m->max_units) return INFLLM_E_RANGE;
   a->n_units = n_units;
@@ -544,17 +551,26 @@ infllm_status infllm_step(const infllm_params* p, const infllm_memory* m, const 
   // Unit construction reads ring slots of positions >= its first token m0; the
   // append writes the slots of [past_len, past_len + n_q).  When the ring is
   // large enough for those never to coincide, both run in one launch.
+  // (The mean representation reads only keys already in the store: always one launch.)
   const int64_t m0 = (int64_t)p->n_init + (int64_t)units_built * p->block_size;
-  const bool fuse = ba.n_new > 0 && n_q > 0 && m0 >= past_len + n_q - m->ring;
+  const bool mean = mean_repr(p);
+  const bool fuse = ba.n_new > 0 && n_q > 0 && (mean || m0 >= past_len + n_q - m->ring);
   if (ba.n_new > 0 && !fuse && (st = launch_status(launch_build_units(ba, s))) != INFLLM_OK) return st;
-  // the append's scan also yields the chunk's group-query sums, which scoring consumes directly
+  // The append also yields the chunk's group-query sums, which scoring consumes
+  // directly: the scan total, or with the mean representation (no scan) the
+  // partial sums of its query-sum blocks.
   float* qbar = (float*)workspace;
+  const int qbar_parts = mean ? score_qbar_parts(p->n_q_heads / p->n_kv_heads, n_q) : 1;
   if ((st = launch_status(launch_append(aa, s, part.n_units > 0 ? qbar : nullptr, fuse ? &ba : nullptr))) !=
       INFLLM_OK)
     return st;
   if (part.n_units > 0) {
     sa.qbar_parts = qbar;
-    if ((st = launch_status(launch_score_given_qbar(sa, 1, s))) != INFLLM_OK) return st;
+    if (n_q == 0) {
+      if ((st = launch_status(launch_score(sa, s))) != INFLLM_OK) return st;
+    } else if ((st = launch_status(launch_score_given_qbar(sa, qbar_parts, s))) != INFLLM_OK) {
+      return st;
+    }
   }
   // with no units yet this still writes the -1 padding of idx
   if (p->topk > 0 && (st = launch_status(launch_select_topk(rows, scores, part.n_units, p->topk, idx, s))) != INFLLM_OK)

@@ -28,6 +28,7 @@
 // dim).  Copy blocks likewise load all their vectors before storing any.
 #include <cstring>
 
+#include "qsum.h"
 #include "unit_build.h"
 
 namespace infllm {
@@ -112,9 +113,11 @@ __device__ __forceinline__ void rotate8(V (&x)[8], int64_t pos, int pair0, const
   }
 }
 
-// Block roles along the 1-D grid: [unit construction | scan | copy].
+// Block roles along the 1-D grid: [unit construction | query sum | scan | copy].
 struct AppendGrid {
   int n_build;          // unit-construction blocks (n_new * batch * Hkv), 0 when not fused
+  int n_qsum;           // query-sum blocks (Mean Repr: parts * batch * Hkv), 0 otherwise
+  int qsum_parts;
   int n_scan;           // scan blocks
   bool thin;            // scan blocks are thin (one thread per (sequence*kv head, dim))
   int n_copy_per_head;  // copy blocks per (sequence, kv head)
@@ -130,10 +133,19 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
   if (blk < grid.n_build) {
     // ---- unit-construction role
     const int bh = ba.batch * ba.n_kv_heads;
-    build_one_unit<T, DT, kThreads>(ba, blk / bh, blk % bh, bsm);
+    construct_unit<T, DT, kThreads>(ba, blk / bh, blk % bh, bsm);
     return;
   }
   blk -= grid.n_build;
+  if (blk < grid.n_qsum) {
+    // ---- query-sum role (Mean Repr, which has no scan): the chunk's group-query
+    // partial sums that unit scoring consumes
+    __shared__ QsumSmem<T> qsm;
+    qsum_block<T>((const T*)a.q, a.q_head_stride, a.n_q_heads, a.n_kv_heads, D, a.n_q, blk % grid.qsum_parts,
+                  grid.qsum_parts, blk / grid.qsum_parts, qbar, qsm);
+    return;
+  }
+  blk -= grid.n_qsum;
   if (blk >= grid.n_scan) {
     // ---- copy role: K and V rows of the chunk into the store; each thread
     // moves kCopyPerThread 16-byte vectors of one (sequence, kv head).
@@ -494,7 +506,9 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
 template <int DT>
 static hipError_t launch_append_d(const AppendArgs& a, const BuildArgs& ba, const AppendGrid& g, hipStream_t s,
                                   float* qbar) {
-  const dim3 grid(g.n_build + g.n_scan + g.n_copy_per_head * a.batch * a.n_kv_heads);
+  const int blocks = g.n_build + g.n_qsum + g.n_scan + g.n_copy_per_head * a.batch * a.n_kv_heads;
+  if (blocks == 0) return hipSuccess;
+  const dim3 grid(blocks);
   const int G = a.n_q_heads / a.n_kv_heads;
 #define INFLLM_APPEND(T, GT) \
   hipLaunchKernelGGL((append_kernel<T, GT, DT>), grid, dim3(kThreads), 0, s, a, ba, g, qbar)
@@ -524,7 +538,11 @@ hipError_t launch_append(const AppendArgs& a, hipStream_t s, float* qbar, const 
   if (a.n_q == 0 && g.n_build == 0) return hipSuccess;
   const int esize = a.bf16 ? 2 : 4;
   g.thin = a.n_q <= kThinMaxQ;
-  g.n_scan = a.n_q <= 0 ? 0
+  // The mean representation needs no query ring: copy (and build) blocks run, and
+  // query-sum blocks when scoring follows (qbar given).
+  g.qsum_parts = score_qbar_parts(a.n_q_heads / a.n_kv_heads, a.n_q);
+  g.n_qsum = (a.mean_repr && qbar != nullptr && a.n_q > 0) ? g.qsum_parts * a.batch * a.n_kv_heads : 0;
+  g.n_scan = (a.n_q <= 0 || a.mean_repr) ? 0
              : g.thin ? (a.batch * a.n_kv_heads * a.head_dim + kThreads - 1) / kThreads
                       : a.batch * a.n_kv_heads * (a.head_dim / 16);
   g.n_copy_per_head = 0;

@@ -7,7 +7,7 @@ namespace {
 template <typename T, int D>
 __global__ void __launch_bounds__(1024) build_units_kernel(BuildArgs a) {
   __shared__ BuildSmem sm;
-  build_one_unit<T, D, 1024>(a, blockIdx.x, blockIdx.y, sm);
+  construct_unit<T, D, 1024>(a, blockIdx.x, blockIdx.y, sm);
 }
 
 }  // namespace

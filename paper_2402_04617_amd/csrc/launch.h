@@ -23,10 +23,14 @@ struct AppendArgs {
   double* rpart;  // [B*Hkv][D/16][ring] partial representative scores
   void* k_rot;    // positional remap: keys rotated to their own positions (same layout as k_store)
   RopeArgs rope;
+  bool mean_repr;  // units scored by their mean key: no query ring, no representative scores
   bool bf16;
 };
 struct BuildArgs;
-// qbar: optional [batch*Hkv][D] float32 output of the chunk's group-query sums.
+int score_qbar_parts(int G, int n_q);
+// qbar: optional float32 output of the chunk's group-query sums: [batch*Hkv][D]
+// (the scan total), or with the mean representation [batch*Hkv][parts][D]
+// partial sums, parts = score_qbar_parts(G, n_q).
 // fused_build: optional unit construction carried by the same launch (its ring
 // reads must not overlap the chunk's new ring slots).
 hipError_t launch_append(const AppendArgs& a, hipStream_t s, float* qbar, const BuildArgs* fused_build);
@@ -40,6 +44,7 @@ struct BuildArgs {
   int32_t* repr_idx;
   float* unit_ksum;
   double* repr_score;  // nullable
+  bool mean_repr;      // unit_ksum = mean of the unit's l_bs keys (no representatives)
   bool bf16;
 };
 hipError_t launch_build_units(const BuildArgs& a, hipStream_t s);

@@ -1,0 +1,55 @@
+// Block-level sum of a chunk's queries over a kv head's query group, shared by
+// the scoring kernels and the append launch (Mean Repr path).  Rows of the
+// group are (head, i) pairs, head-major; part `part` of `parts` sums an equal
+// share of them in a fixed order, so the partial sums are deterministic.
+#pragma once
+
+#include "launch.h"
+
+namespace infllm {
+
+constexpr int kQsumThreads = 256;
+
+template <typename T>
+struct QsumSmem {
+  float red[kQsumThreads * (16 / sizeof(T))];
+};
+
+template <typename T>
+__device__ __forceinline__ void qsum_block(const T* __restrict__ q, int64_t q_head_stride, int n_q_heads,
+                                           int n_kv_heads, int head_dim, int n_q, int part, int parts, int bg,
+                                           float* __restrict__ qbar_parts, QsumSmem<T>& sm) {
+  constexpr int kVec = 16 / sizeof(T);
+  const int b = bg / n_kv_heads, g = bg - b * n_kv_heads;
+  const int G = n_q_heads / n_kv_heads;
+  const int rows = G * n_q;
+  const int per = (rows + parts - 1) / parts;
+  const int r0 = min(rows, part * per), r1 = min(rows, r0 + per);
+  const int lanes_per_row = head_dim / kVec;
+  const int rgroups = kQsumThreads / lanes_per_row;
+  const int c = threadIdx.x % lanes_per_row;
+  const int rg = threadIdx.x / lanes_per_row;
+
+  float acc[kVec];
+#pragma unroll
+  for (int e = 0; e < kVec; ++e) acc[e] = 0.f;
+#pragma unroll 4
+  for (int r = r0 + rg; r < r1; r += rgroups) {
+    const int hl = r / n_q, i = r - hl * n_q;
+    const T* row = q + (int64_t)(b * n_q_heads + g * G + hl) * q_head_stride + (int64_t)i * head_dim;
+    uint4 raw = *(const uint4*)(row + c * kVec);
+    const T* vals = (const T*)&raw;
+#pragma unroll
+    for (int e = 0; e < kVec; ++e) acc[e] += Elem<T>::load(vals + e);
+  }
+#pragma unroll
+  for (int e = 0; e < kVec; ++e) sm.red[rg * head_dim + c * kVec + e] = acc[e];
+  __syncthreads();
+  for (int d = threadIdx.x; d < head_dim; d += kQsumThreads) {
+    float s = 0.f;
+    for (int j = 0; j < rgroups; ++j) s += sm.red[j * head_dim + d];
+    qbar_parts[((int64_t)bg * parts + part) * head_dim + d] = s;
+  }
+}
+
+}  // namespace infllm

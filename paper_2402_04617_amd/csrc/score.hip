@@ -7,51 +7,21 @@
 // kernels: a reduction of the chunk's queries into per-part partial sums
 // (deterministic order), then one streaming pass over the Kbar table (fp32,
 // unit-contiguous 16-byte cells) at HBM rate.
-#include "launch.h"
+#include "qsum.h"
 
 namespace infllm {
 namespace {
 
 constexpr int kMaxQbarParts = 16;
 
-// grid (parts, batch*Hkv); rows of the group are (head, i) pairs, head-major.
+// grid (parts, batch*Hkv)
 template <typename T>
-__global__ void __launch_bounds__(256) qbar_kernel(const T* __restrict__ q, int64_t q_head_stride,
-                                                   int n_q_heads, int n_kv_heads, int head_dim,
-                                                   int n_q, int parts, float* __restrict__ qbar_parts) {
-  constexpr int kVec = 16 / sizeof(T);
-  const int part = blockIdx.x;
-  const int bg = blockIdx.y;
-  const int b = bg / n_kv_heads, g = bg - b * n_kv_heads;
-  const int G = n_q_heads / n_kv_heads;
-  const int rows = G * n_q;
-  const int per = (rows + parts - 1) / parts;
-  const int r0 = min(rows, part * per), r1 = min(rows, r0 + per);
-  const int lanes_per_row = head_dim / kVec;
-  const int rgroups = 256 / lanes_per_row;
-  const int c = threadIdx.x % lanes_per_row;
-  const int rg = threadIdx.x / lanes_per_row;
-
-  float acc[kVec];
-#pragma unroll
-  for (int e = 0; e < kVec; ++e) acc[e] = 0.f;
-  for (int r = r0 + rg; r < r1; r += rgroups) {
-    const int hl = r / n_q, i = r - hl * n_q;
-    const T* row = q + (int64_t)(b * n_q_heads + g * G + hl) * q_head_stride + (int64_t)i * head_dim;
-    uint4 raw = *(const uint4*)(row + c * kVec);
-    const T* vals = (const T*)&raw;
-#pragma unroll
-    for (int e = 0; e < kVec; ++e) acc[e] += Elem<T>::load(vals + e);
-  }
-  __shared__ float red[256 * kVec];
-#pragma unroll
-  for (int e = 0; e < kVec; ++e) red[rg * head_dim + c * kVec + e] = acc[e];
-  __syncthreads();
-  for (int d = threadIdx.x; d < head_dim; d += 256) {
-    float s = 0.f;
-    for (int j = 0; j < rgroups; ++j) s += red[j * head_dim + d];
-    qbar_parts[((int64_t)bg * parts + part) * head_dim + d] = s;
-  }
+__global__ void __launch_bounds__(kQsumThreads) qbar_kernel(const T* __restrict__ q, int64_t q_head_stride,
+                                                            int n_q_heads, int n_kv_heads, int head_dim,
+                                                            int n_q, int parts, float* __restrict__ qbar_parts) {
+  __shared__ QsumSmem<T> sm;
+  qsum_block<T>(q, q_head_stride, n_q_heads, n_kv_heads, head_dim, n_q, blockIdx.x, parts, blockIdx.y, qbar_parts,
+                sm);
 }
 
 // grid (ceil(n_units/256), batch*Hkv); one unit per thread.  With the
@@ -113,10 +83,10 @@ hipError_t launch_score(const ScoreArgs& a, hipStream_t s) {
   const int parts = score_qbar_parts(G, a.n_q);
   dim3 g1(parts, a.batch * a.n_kv_heads);
   if (a.bf16)
-    hipLaunchKernelGGL(qbar_kernel<bf16_t>, g1, dim3(256), 0, s, (const bf16_t*)a.q, a.q_head_stride,
+    hipLaunchKernelGGL(qbar_kernel<bf16_t>, g1, dim3(kQsumThreads), 0, s, (const bf16_t*)a.q, a.q_head_stride,
                        a.n_q_heads, a.n_kv_heads, a.head_dim, a.n_q, parts, a.qbar_parts);
   else
-    hipLaunchKernelGGL(qbar_kernel<float>, g1, dim3(256), 0, s, (const float*)a.q, a.q_head_stride,
+    hipLaunchKernelGGL(qbar_kernel<float>, g1, dim3(kQsumThreads), 0, s, (const float*)a.q, a.q_head_stride,
                        a.n_q_heads, a.n_kv_heads, a.head_dim, a.n_q, parts, a.qbar_parts);
   return launch_score_given_qbar(a, parts, s);
 }

@@ -118,4 +118,48 @@ __device__ __forceinline__ void build_one_unit(const BuildArgs& a, int unit_loca
   }
 }
 
+// Mean representation (the paper's "Mean Repr" alternative, Section 4): the
+// unit is scored by the mean of all its l_bs keys.  Each key row is read as
+// 16-byte pieces by LPK adjacent threads; KG groups of them take interleaved
+// rows, and the groups' partial sums are added in a fixed order.
+template <typename T, int D, int NT>
+__device__ __forceinline__ void mean_one_unit(const BuildArgs& a, int unit_local, int bg, BuildSmem& sm) {
+  constexpr int VEC = 16 / (int)sizeof(T);  // elements per 16-byte piece
+  constexpr int LPK = D / VEC;              // threads per key row
+  constexpr int KG = (NT / LPK) < (kMaxSumElems / D) ? (NT / LPK) : (kMaxSumElems / D);
+  const int unit = a.first_unit + unit_local;
+  const int lbs = a.block_size;
+  const int64_t m0 = (int64_t)a.n_init + (int64_t)unit * lbs;
+  const T* kb = (const T*)a.k_store + ((int64_t)bg * a.capacity + m0) * D;
+  const int c = threadIdx.x % LPK, grp = threadIdx.x / LPK;
+  if (grp < KG) {
+    float acc[VEC];
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) acc[e] = 0.f;
+#pragma unroll 4
+    for (int j = grp; j < lbs; j += KG) {
+      const uint4 raw = *(const uint4*)(kb + (int64_t)j * D + c * VEC);
+      const T* vals = (const T*)&raw;
+#pragma unroll
+      for (int e = 0; e < VEC; ++e) acc[e] += Elem<T>::load(vals + e);
+    }
+#pragma unroll
+    for (int e = 0; e < VEC; ++e) sm.rk[grp * D + c * VEC + e] = acc[e];
+  }
+  __syncthreads();
+  for (int d = threadIdx.x; d < D; d += NT) {
+    float s = 0.f;
+#pragma unroll
+    for (int g = 0; g < KG; ++g) s += sm.rk[g * D + d];
+    a.unit_ksum[(((int64_t)bg * (D / 4) + d / 4) * a.max_units + unit) * 4 + (d & 3)] = s / (float)lbs;
+  }
+}
+
+// One unit of either representation.
+template <typename T, int D, int NT>
+__device__ __forceinline__ void construct_unit(const BuildArgs& a, int unit_local, int bg, BuildSmem& sm) {
+  if (a.mean_repr) mean_one_unit<T, D, NT>(a, unit_local, bg, sm);
+  else build_one_unit<T, D, NT>(a, unit_local, bg, sm);
+}
+
 }  // namespace infllm

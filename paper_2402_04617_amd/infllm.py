@@ -17,6 +17,8 @@ _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libinfllm.
 
 INFLLM_F32 = 0
 INFLLM_BF16 = 1
+INFLLM_REPR_TOKENS = 0
+INFLLM_REPR_MEAN = 1
 
 STATUS = {0: "INFLLM_OK", 1: "INFLLM_E_NULL", 2: "INFLLM_E_SHAPE", 3: "INFLLM_E_RANGE",
           4: "INFLLM_E_UNSUPPORTED", 5: "INFLLM_E_WORKSPACE", 6: "INFLLM_E_LAUNCH", 7: "INFLLM_E_DEVICE"}
@@ -36,12 +38,18 @@ class Params(ctypes.Structure):
     _fields_ = [("n_q_heads", ctypes.c_int32), ("n_kv_heads", ctypes.c_int32), ("head_dim", ctypes.c_int32),
                 ("n_init", ctypes.c_int32), ("n_local", ctypes.c_int32), ("block_size", ctypes.c_int32),
                 ("n_repr", ctypes.c_int32), ("topk", ctypes.c_int32), ("dtype", ctypes.c_int32),
-                ("sm_scale", ctypes.c_float), ("rope_inv_freq", ctypes.POINTER(ctypes.c_double))]
+                ("sm_scale", ctypes.c_float), ("rope_inv_freq", ctypes.POINTER(ctypes.c_double)),
+                ("repr_mode", ctypes.c_int32)]
 
     @property
     def remap(self) -> bool:
         """Positional remap on (rotary frequencies given)."""
         return bool(self.rope_inv_freq)
+
+    @property
+    def mean_repr(self) -> bool:
+        """Units scored by their mean key (no representative tokens, no query ring)."""
+        return self.repr_mode == INFLLM_REPR_MEAN
 
 
 class Memory(ctypes.Structure):
@@ -203,11 +211,13 @@ _rope_tables = {}  # keeps each Params' frequency array alive (the struct holds 
 
 
 def params(n_q_heads, n_kv_heads, head_dim, n_init, n_local, block_size, n_repr, topk, dtype="bf16",
-           sm_scale=1.0, rope_inv_freq=None) -> Params:
+           sm_scale=1.0, rope_inv_freq=None, repr_mode="tokens") -> Params:
     """Method parameters.  rope_inv_freq: None (positions pre-applied) or the D/2 rotary angular
-    frequencies of the positional remap."""
+    frequencies of the positional remap.  repr_mode: "tokens" (r_k representative tokens) or
+    "mean" (units scored by their mean key)."""
     p = Params(n_q_heads, n_kv_heads, head_dim, n_init, n_local, block_size, n_repr, topk,
                INFLLM_BF16 if dtype == "bf16" else INFLLM_F32, sm_scale)
+    p.repr_mode = {"tokens": INFLLM_REPR_TOKENS, "mean": INFLLM_REPR_MEAN}[repr_mode]
     if rope_inv_freq is not None:
         table = (ctypes.c_double * len(rope_inv_freq))(*[float(x) for x in rope_inv_freq])
         _rope_tables[ctypes.addressof(p)] = table
@@ -229,12 +239,14 @@ def alloc_memory(p: Params, batch: int, capacity: int, max_units: int, ring: int
     mu = max(1, max_units)
     repr_idx = torch.zeros((batch, p.n_kv_heads, mu, p.n_repr), dtype=torch.int32, device=device)
     unit_ksum = torch.zeros((batch, p.n_kv_heads, D // 4, mu, 4), dtype=torch.float32, device=device)
-    qprefix = torch.zeros((batch, p.n_kv_heads, ring, D), dtype=torch.float64, device=device)
-    rpart = torch.zeros((batch, p.n_kv_heads, D // 16, ring), dtype=torch.float64, device=device)
+    # the query ring and the partial representative scores exist only for representative tokens
+    ring_used = not p.mean_repr
+    qprefix = torch.zeros((batch, p.n_kv_heads, ring, D), dtype=torch.float64, device=device) if ring_used else None
+    rpart = torch.zeros((batch, p.n_kv_heads, D // 16, ring), dtype=torch.float64, device=device) if ring_used else None
     k_rot = torch.zeros_like(k) if p.remap else None
+    ptr = lambda t: t.data_ptr() if t is not None else None  # noqa: E731
     st = Memory(batch, capacity, k.data_ptr(), v.data_ptr(), max_units, repr_idx.data_ptr(),
-                unit_ksum.data_ptr(), qprefix.data_ptr(), rpart.data_ptr(), ring,
-                k_rot.data_ptr() if k_rot is not None else None)
+                unit_ksum.data_ptr(), ptr(qprefix), ptr(rpart), ring if ring_used else 0, ptr(k_rot))
     return LayerMemory(k, v, repr_idx, unit_ksum, qprefix, rpart, st, k_rot)
 
 

@@ -523,6 +523,39 @@ def check_remap_reduces_to_rotary_attention():
         assert np.allclose(r["lse"], ref_l[:, past:past + 9], rtol=1e-12, atol=1e-12), past
 
 
+# --------------------------------------------------------------------------- Mean Repr
+def check_mean_repr_mode():
+    """Units represented by their mean key: literal loops sum_h sum_i sum_d q[d] * (1/l_bs) sum_j k_j[d];
+    equal to the representative-token scores with r_k = l_bs divided by l_bs; and, with the
+    remap, the literal loops with every query turned by R(l_L) (complex arithmetic)."""
+    rng = np.random.default_rng(40)
+    base = dict(n_q_heads=4, n_kv_heads=2, head_dim=6, n_init=3, n_local=8, block_size=4, n_repr=2, topk=2)
+    pm = _params(**base, mean_repr=True)
+    pt = _params(**{**base, "n_repr": 4})
+    S, past, nq = 60, 40, 5
+    q, k, v = _rand_qkv(rng, pm, S)
+    nu = O.partition(past, pm).n_units
+    sm = O.StreamOracle(q, k, v, pm).scores(0, past, nq)
+    st = O.StreamOracle(q, k, v, pt).scores(0, past, nq)
+    assert np.allclose(sm, st / pm.block_size, rtol=1e-12, atol=1e-12)
+    f = rng.uniform(0.05, 1.5, 3)
+    pr = O.Params(**{**pm.__dict__, "rope_inv_freq": tuple(f)})
+    sr = O.StreamOracle(q, k, v, pr).scores(0, past, nq)
+    for g in range(2):
+        for u in range(nu):
+            s0 = pm.n_init + u * pm.block_size
+            lit = lit_r = 0.0
+            for h in range(2 * g, 2 * g + 2):
+                for i in range(past, past + nq):
+                    qr = _rot_complex(q[0, h, i], pm.n_local, f)
+                    for d in range(pm.head_dim):
+                        kd = sum(float(k[0, g, s0 + j, d]) for j in range(pm.block_size)) / pm.block_size
+                        lit += float(q[0, h, i, d]) * kd
+                        lit_r += float(qr[d]) * kd
+            assert math.isclose(sm[g, u], lit, rel_tol=1e-12, abs_tol=1e-12), (g, u)
+            assert math.isclose(sr[g, u], lit_r, rel_tol=1e-11, abs_tol=1e-11), (g, u)
+
+
 # --------------------------------------------------------------------------- golden
 def load_golden():
     with open(os.path.join(GOLDEN, "hand_worked_tiny.yaml")) as f:
@@ -572,4 +605,5 @@ ALL_CHECKS = [
     check_remap_relevance_effective_positions,
     check_remap_repr_scores_bruteforce,
     check_remap_reduces_to_rotary_attention,
+    check_mean_repr_mode,
 ]

@@ -233,8 +233,33 @@ def test_remap_validation(L):
     assert L.infllm_workspace_bytes(ctypes.byref(pd), 1, 1) >= 2 * 32 * row
 
 
+def test_mean_repr_validation(L):
+    """Mean representation: an unknown mode is a shape error; the query ring, rpart and repr_idx
+    are not needed (their absence is not reported, the call reaches the device check)."""
+    p = P()
+    p.repr_mode = 5
+    n0, n1, n2 = ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int64()
+    assert L.infllm_partition(ctypes.byref(p), 100, ctypes.byref(n0), ctypes.byref(n1), ctypes.byref(n2)) == 2
+    pm = P(repr_mode="mean")
+    m = mem(qprefix=None, rpart=None, repr_idx=None, ring=0)
+    bp, bm = ctypes.byref(pm), ctypes.byref(m)
+    S = 512 * 128
+    # argument errors are still found first
+    assert L.infllm_append(bp, bm, FAKE, 100, None, None, 0, 512, 0, None) == 2
+    assert L.infllm_build_units(bp, bm, 2040, 16, 1 << 17, None, None) == 3
+    # the token representation does need them
+    pt = P()
+    assert L.infllm_append(ctypes.byref(pt), bm, FAKE, S, None, None, 0, 512, 0, None) == 1
+    assert L.infllm_build_units(ctypes.byref(pt), bm, 0, 1, 4352, None, None) == 1
+
+
 @pytest.mark.skipif(os.path.exists("/dev/kfd") and os.access("/dev/kfd", os.R_OK),
                     reason="a GPU may be present; valid arguments would launch on fake pointers")
 def test_valid_arguments_without_gpu_report_device_error(L):
     p, m = P(), mem()
     assert L.infllm_select_topk(8, FAKE, 10, 4, FAKE, None) == 7
+    # mean representation without ring buffers: valid, so only the device check fails
+    pm = P(repr_mode="mean")
+    mm = mem(qprefix=None, rpart=None, repr_idx=None, ring=0)
+    assert L.infllm_append(ctypes.byref(pm), ctypes.byref(mm), FAKE, 512 * 128, None, None, 0, 512, 0, None) == 7
+    assert L.infllm_build_units(ctypes.byref(pm), ctypes.byref(mm), 0, 1, 4352, None, None) == 7

@@ -20,7 +20,7 @@ def test_pin(check):
 # ------------------------------------------------------------------ mutants
 _orig = {name: getattr(O, name) for name in
          ("partition", "representative_scores", "top_indices", "unit_relevance", "attend",
-          "lse_merge", "context_positions", "select_units", "unit_start", "rotate")}
+          "lse_merge", "context_positions", "select_units", "unit_start", "rotate", "mean_relevance")}
 
 
 def _mut_partition_drop_remainder(past_len, p):
@@ -118,6 +118,19 @@ def _mut_attend_memory_negative_distance(q_chunk, k, v, past_len, sel, p):
         return _orig["attend"](q_chunk, k, v, past_len, sel, p)
     finally:
         O.rotate = real_rotate
+
+
+def _mut_mean_sum_not_mean(q, k, n_units, p):
+    # the key sum instead of the mean
+    return _orig["mean_relevance"](q, k, n_units, p) * p.block_size
+
+
+def _mut_mean_skips_last_key(q, k, n_units, p):
+    # l_bs - 1 keys averaged (an off-by-one in the unit's span)
+    if n_units == 0:
+        return np.zeros(0)
+    pos = np.stack([np.arange(O.unit_start(u, p), O.unit_start(u, p) + p.block_size - 1) for u in range(n_units)])
+    return O.unit_relevance(q, k, pos, p) / (p.block_size - 1)
 
 
 def _mut_attend_init_true_positions(q_chunk, k, v, past_len, sel, p):
@@ -223,6 +236,8 @@ MUTANTS = [
     ("representative_scores", _mut_repr_unrotated),
     ("attend", _mut_attend_memory_negative_distance),
     ("attend", _mut_attend_init_true_positions),
+    ("mean_relevance", _mut_mean_sum_not_mean),
+    ("mean_relevance", _mut_mean_skips_last_key),
 ]
 
 
