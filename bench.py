@@ -187,6 +187,29 @@ class Stream:
                 on_step(i)
         return built
 
+    def prefill_view(self, b, upto):
+        """Untimed set-up of one sequence alone: encode sequence b over [0, upto) through a
+        one-sequence view of the memory; returns its units built."""
+        F, wl, S, D = self.F, self.wl, self.wl.seq_len, self.wl.head_dim
+        m, s = self.mem, self.mem.struct
+        ptr = lambda t: None if t is None else t[b].data_ptr()  # noqa: E731
+        view = F.Memory(1, s.capacity, m.k[b].data_ptr(), m.v[b].data_ptr(), s.max_units, ptr(m.repr_idx),
+                        ptr(m.unit_ksum), ptr(m.qprefix), ptr(m.rpart), s.ring, ptr(m.k_rot))
+        off = lambda name, past: self.inp[name][b].data_ptr() + past * D * self.esize  # noqa: E731
+        built = 0
+        for past in range(0, upto, wl.chunk):
+            n = min(wl.chunk, upto - past)
+            nu = F.infllm_partition(self.p, past)[1]
+            if nu > built:
+                F.infllm_build_units(self.p, view, built, nu - built, past)
+                built = nu
+            F.infllm_append(self.p, view, off("q", past), S * D, off("k", past), off("v", past), S * D, n, past)
+        nu = F.infllm_partition(self.p, upto)[1]
+        if nu > built:
+            F.infllm_build_units(self.p, view, built, nu - built, upto)
+            built = nu
+        return built
+
     def prefill_memory(self, upto):
         """Untimed set-up for decode: append positions [0, upto) chunk by chunk and build every unit."""
         F, wl, S, D = self.F, self.wl, self.wl.seq_len, self.wl.head_dim
@@ -285,8 +308,45 @@ def decode_leg(seed, steps, warmup, torch):
     plan = wl.step_starts()[-wl.decode_steps:]
     ms = time_steps(torch, lambda: st.run(plan, built=built), steps, warmup)
     us_tok = ms * 1e3 / len(plan)
-    return {"workload": wl.name, "decode_steps": len(plan), "batch": wl.batch, "us_per_step": us_tok,
-            "tok_per_s": wl.batch * len(plan) / (ms / 1e3)}
+    res = {"workload": wl.name, "decode_steps": len(plan), "batch": wl.batch, "us_per_step": us_tok,
+           "tok_per_s": wl.batch * len(plan) / (ms / 1e3)}
+    return res, st
+
+
+def decode_varlen_leg(st, steps, warmup, torch, spacing=6144):
+    """Serving-style decode: the 16 sequences at different depths (128K, 122K, ..., 38K prior tokens),
+    stepped together by infllm_step_varlen.  Each sequence's memory is first rebuilt alone to its
+    own length (untimed); the step inputs, gathered from each sequence's own position, are made
+    before timing."""
+    F, wl = st.F, st.wl
+    B, S, D = wl.batch, wl.seq_len, wl.head_dim
+    lens = [wl.prefill_len - spacing * b for b in range(B)]
+    built = []
+    for b in range(B):
+        built.append(st.prefill_view(b, lens[b]))
+    torch.cuda.synchronize()
+    T = wl.decode_steps
+    pos = torch.tensor(lens, device="cuda")
+    ar = torch.arange(B, device="cuda")
+
+    def gather(x, t):
+        return x[ar, :, pos + t].unsqueeze(2).contiguous()  # [B][H][1][D]
+    qs = [gather(st.inp["q"], t) for t in range(T)]
+    ks = [gather(st.inp["k"], t) for t in range(T)]
+    vs = [gather(st.inp["v"], t) for t in range(T)]
+    pasts = [[lens[b] + t for b in range(B)] for t in range(T)]
+    builts = [built] + [[F.infllm_partition(st.p, pp)[1] for pp in pasts[t]] for t in range(T - 1)]
+    out = torch.zeros((B, wl.n_q_heads, 1, D), dtype=st.out.dtype, device="cuda")
+    lse = torch.zeros((B, wl.n_q_heads, 1), dtype=torch.float32, device="cuda")
+    scores = torch.zeros((B, wl.n_kv_heads, st.max_units), dtype=torch.float32, device="cuda")
+
+    def run():
+        for t in range(T):
+            F.infllm_step_varlen(st.p, st.mem.struct, qs[t], D, ks[t], vs[t], D, 1, pasts[t], builts[t], scores,
+                                 st.idx, out, D, lse, st.ws)
+    ms = time_steps(torch, run, steps, warmup)
+    return {"workload": wl.name + "+varlen", "decode_steps": T, "batch": B, "prior_tokens": [min(lens), max(lens)],
+            "us_per_step": ms * 1e3 / T, "tok_per_s": B * T / (ms / 1e3)}
 
 
 def cpu_baseline(synth, n_chunk_samples=64):
@@ -420,10 +480,14 @@ def main():
         del st1
         torch.cuda.empty_cache()
     if "decode" in legs:
-        rd = decode_leg(args.seed, max(1, min(args.steps, 3)), 1, torch)
-        torch.cuda.empty_cache()
+        rd, st_d = decode_leg(args.seed, max(1, min(args.steps, 3)), 1, torch)
         extra["decode_16x128k"] = rd
         log(f"decode: {rd['us_per_step']:.1f} us/step (16 seqs)")
+        rv = decode_varlen_leg(st_d, max(1, min(args.steps, 3)), 1, torch)
+        extra["decode_16_varlen"] = rv
+        log(f"decode, lengths {rv['prior_tokens'][0]}..{rv['prior_tokens'][1]}: {rv['us_per_step']:.1f} us/step")
+        del st_d
+        torch.cuda.empty_cache()
 
     att = main_res["attention"]
     achieved = att["tflops"]

@@ -25,7 +25,8 @@
  *    returns INFLLM_E_LAUNCH.  No C++ exception crosses this interface.
  *  - Calls on different streams that write the same buffers race; calls are
  *    otherwise re-entrant.
- *  - All sequences of a batch share one past length.
+ *  - All sequences of a batch share one past length, except in
+ *    infllm_step_varlen.
  */
 #ifndef INFLLM_H
 #define INFLLM_H
@@ -242,6 +243,21 @@ infllm_status infllm_step(const infllm_params* p, const infllm_memory* m, const 
                           const void* k, const void* v, int64_t kv_head_stride, int32_t n_q, int64_t past_len,
                           int32_t units_built, float* scores, int32_t* idx, void* out, int64_t out_head_stride,
                           float* lse, void* workspace, size_t workspace_bytes, void* stream);
+
+/* One step of a batch whose sequences have different past lengths (a serving
+ * batch: each sequence decodes, or encodes a chunk, at its own position).
+ * Sequence b appends its n_q tokens at [past_lens[b], past_lens[b] + n_q) and
+ * runs the five stages of infllm_step against its own partition; past_lens and
+ * units_built are HOST arrays of `batch` entries (units_built[b] as in
+ * infllm_step, per sequence).  scores: [batch][Hkv][max_units] float32 (row
+ * stride memory.max_units; sequence b fills its first n_units(past_lens[b])
+ * entries of each row).  Everything else as in infllm_step.  batch <= 64
+ * (E_UNSUPPORTED beyond); each sequence is validated as its own step first. */
+infllm_status infllm_step_varlen(const infllm_params* p, const infllm_memory* m, const void* q,
+                                 int64_t q_head_stride, const void* k, const void* v, int64_t kv_head_stride,
+                                 int32_t n_q, const int64_t* past_lens, const int32_t* units_built, float* scores,
+                                 int32_t* idx, void* out, int64_t out_head_stride, float* lse, void* workspace,
+                                 size_t workspace_bytes, void* stream);
 
 /* Static description of a status code. */
 const char* infllm_status_string(infllm_status s);

@@ -196,8 +196,7 @@ infllm_status prepare_attend(const infllm_params* p, const infllm_memory* m, con
       if (max_parts < 2) return INFLLM_E_WORKSPACE;
       parts = 2;
     }
-    parts_mem = (int)((parts * mem_len + n_virtual / 2) / n_virtual);
-    parts_mem = std::min(std::max(parts_mem, 1), parts - 1);
+    parts_mem = split_parts_mem(parts, mem_len, n_virtual);
   }
   if (parts > 1 && !aligned16(workspace)) return INFLLM_E_SHAPE;
 
@@ -227,6 +226,7 @@ infllm_status prepare_attend(const infllm_params* p, const infllm_memory* m, con
   a->parts_mem = parts_mem;
   a->mem_len = (int)mem_len;
   a->rope = rope_args(p);
+  a->n_local = p->n_local;
   a->idx = idx;
   a->out = out;
   a->lse = lse;
@@ -311,6 +311,7 @@ infllm_status prep_append(const infllm_params* p, const infllm_memory* m, const 
   a->rpart = m->rpart;
   a->k_rot = m->k_rot;
   a->rope = rope_args(p);
+  a->var.on = 0;
   a->mean_repr = mean_repr(p);
   a->bf16 = p->dtype == INFLLM_BF16;
   return INFLLM_OK;
@@ -352,6 +353,7 @@ infllm_status prep_build(const infllm_params* p, const infllm_memory* m, int32_t
   a->unit_ksum = m->unit_ksum;
   a->repr_score = repr_score;
   a->mean_repr = mean_repr(p);
+  a->var_on = 0;
   a->bf16 = p->dtype == INFLLM_BF16;
   return INFLLM_OK;
 }
@@ -367,6 +369,7 @@ infllm_status prep_score(const infllm_params* p, const infllm_memory* m, const v
   if (n_q < 0 || n_units < 0) return INFLLM_E_SHAPE;
   if (n_units > m->max_units) return INFLLM_E_RANGE;
   a->n_units = n_units;
+  a->var_on = 0;
   if (n_units == 0) return INFLLM_OK;
   if (scores == nullptr) return INFLLM_E_NULL;
   if ((st = check_rows(p, q, q_head_stride, n_q)) != INFLLM_OK) return st;
@@ -579,6 +582,114 @@ infllm_status infllm_step(const infllm_params* p, const infllm_memory* m, const 
   if ((st = launch_status(launch_attend(at, s))) != INFLLM_OK) return st;
   if (at.parts == 1) return INFLLM_OK;
   MergeArgs ma = merge_args(p, m->batch, n_q, at.parts, workspace, out, out_head_stride, lse);
+  return launch_status(launch_merge(ma, s));
+}
+
+infllm_status infllm_step_varlen(const infllm_params* p, const infllm_memory* m, const void* q,
+                                 int64_t q_head_stride, const void* k, const void* v, int64_t kv_head_stride,
+                                 int32_t n_q, const int64_t* past_lens, const int32_t* units_built, float* scores,
+                                 int32_t* idx, void* out, int64_t out_head_stride, float* lse, void* workspace,
+                                 size_t workspace_bytes, void* stream) {
+  infllm_status st;
+  if ((st = check_params(p)) != INFLLM_OK) return st;
+  if (m == nullptr || past_lens == nullptr || units_built == nullptr) return INFLLM_E_NULL;
+  if (m->batch < 1) return INFLLM_E_SHAPE;
+  if (m->batch > kMaxVarBatch) return INFLLM_E_UNSUPPORTED;
+  const int B = m->batch;
+  const bool mean = mean_repr(p);
+  // Every sequence's stages are validated as a step of its own; the launches
+  // then carry all sequences, each kernel deriving a sequence's geometry from
+  // its past length.  The first sequence's arguments supply the shared fields.
+  BuildArgs ba;
+  AppendArgs aa;
+  ScoreArgs sa;
+  std::memset(&sa, 0, sizeof(sa));
+  AttendArgs at;
+  int32_t n_units[kMaxVarBatch];
+  int n_units_max = 0, new_max = 0, parts = 1, n_sel_max = 0, nv_max = 0;
+  bool fuse = n_q > 0;
+  for (int b = 0; b < B; ++b) {
+    const int64_t past = past_lens[b];
+    if (past < 0 || units_built[b] < 0) return INFLLM_E_SHAPE;
+    const Part part = partition(p, past);
+    if (units_built[b] > part.n_units) return INFLLM_E_SHAPE;
+    BuildArgs bb;
+    AppendArgs ab;
+    ScoreArgs sb;
+    AttendArgs tb;
+    if ((st = prep_build(p, m, units_built[b], part.n_units - units_built[b], past, nullptr, &bb)) != INFLLM_OK)
+      return st;
+    if ((st = prep_append(p, m, q, q_head_stride, k, v, kv_head_stride, n_q, past, &ab)) != INFLLM_OK) return st;
+    if ((st = prep_score(p, m, q, q_head_stride, n_q, part.n_units, scores, workspace, workspace_bytes, &sb)) !=
+        INFLLM_OK)
+      return st;
+    if ((st = prepare_attend(p, m, q, q_head_stride, n_q, past, idx, p->topk, out, out_head_stride, lse, workspace,
+                             workspace_bytes, &tb)) != INFLLM_OK)
+      return st;
+    if (b == 0) {
+      ba = bb;
+      aa = ab;
+      at = tb;
+    }
+    // (scoring arguments are complete only where the sequence has units)
+    if (part.n_units > 0 && n_units_max == 0) sa = sb;
+    n_units[b] = part.n_units;
+    n_units_max = std::max(n_units_max, part.n_units);
+    new_max = std::max(new_max, bb.n_new);
+    parts = std::max(parts, tb.parts);
+    n_sel_max = std::max(n_sel_max, tb.geom.n_sel);
+    nv_max = std::max(nv_max, tb.geom.n_virtual);
+    const int64_t m0 = (int64_t)p->n_init + (int64_t)units_built[b] * p->block_size;
+    if (bb.n_new > 0 && !mean && m0 < past + n_q - m->ring) fuse = false;
+    ba.var_first[b] = units_built[b];
+    ba.var_count[b] = bb.n_new;
+    aa.var.past[b] = past;
+    at.var.past[b] = past;
+  }
+  const int32_t rows = B * p->n_kv_heads;
+  if (p->topk > 0 && idx == nullptr) return INFLLM_E_NULL;
+  if (n_units_max > 0 && scores == nullptr) return INFLLM_E_NULL;
+  // every sequence's parts fit the workspace (each was checked for its own count)
+  ba.var_on = 1;
+  ba.n_new = new_max;
+  aa.var.on = 1;
+  sa.var_on = 1;
+  sa.n_units = n_units_max;
+  for (int b = 0; b < B; ++b) sa.var_units[b] = n_units[b];
+  sa.score_stride = m->max_units;
+  at.var.on = 1;
+  at.parts = parts;
+  at.geom.n_sel = n_sel_max;  // bounds only: each kernel derives its sequence's values
+  at.geom.n_virtual = nv_max;
+  partial_layout(p, workspace, parts, (int64_t)B * p->n_q_heads * n_q, &at.part_o, &at.part_lse, &at.part_exp);
+  if ((st = check_device()) != INFLLM_OK) return st;
+  hipStream_t s = (hipStream_t)stream;
+  if (new_max > 0 && !fuse && (st = launch_status(launch_build_units(ba, s))) != INFLLM_OK) return st;
+  float* qbar = (float*)workspace;
+  const int qbar_parts = mean ? score_qbar_parts(p->n_q_heads / p->n_kv_heads, n_q) : 1;
+  if ((st = launch_status(launch_append(aa, s, n_units_max > 0 ? qbar : nullptr,
+                                        (fuse && new_max > 0) ? &ba : nullptr))) != INFLLM_OK)
+    return st;
+  if (n_units_max > 0) {
+    sa.qbar_parts = qbar;
+    if (n_q == 0) {
+      if ((st = launch_status(launch_score(sa, s))) != INFLLM_OK) return st;
+    } else if ((st = launch_status(launch_score_given_qbar(sa, qbar_parts, s))) != INFLLM_OK) {
+      return st;
+    }
+  }
+  if (p->topk > 0) {
+    TopkRows tr;
+    tr.rows_per_seq = p->n_kv_heads;
+    for (int b = 0; b < B; ++b) tr.row_n[b] = n_units[b];
+    if ((st = launch_status(launch_select_topk_var(rows, scores, m->max_units, n_units_max, tr, p->topk, idx, s))) !=
+        INFLLM_OK)
+      return st;
+  }
+  if (n_q == 0) return INFLLM_OK;
+  if ((st = launch_status(launch_attend(at, s))) != INFLLM_OK) return st;
+  if (at.parts == 1) return INFLLM_OK;
+  MergeArgs ma = merge_args(p, B, n_q, at.parts, workspace, out, out_head_stride, lse);
   return launch_status(launch_merge(ma, s));
 }
 

@@ -154,10 +154,11 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
     const int vec_per_head = a.n_q * D / VEC;
     const int64_t head = blk / grid.n_copy_per_head;
     const int cblk = blk % grid.n_copy_per_head;
+    const int64_t past = seq_past(a, (int)(head / a.n_kv_heads));
     const uint4* src_k = (const uint4*)a.k_src + head * (a.kv_head_stride / VEC);
     const uint4* src_v = (const uint4*)a.v_src + head * (a.kv_head_stride / VEC);
-    uint4* dst_k = (uint4*)a.k_store + head * (a.capacity * D / VEC) + a.past_len * D / VEC;
-    uint4* dst_v = (uint4*)a.v_store + head * (a.capacity * D / VEC) + a.past_len * D / VEC;
+    uint4* dst_k = (uint4*)a.k_store + head * (a.capacity * D / VEC) + past * D / VEC;
+    uint4* dst_v = (uint4*)a.v_store + head * (a.capacity * D / VEC) + past * D / VEC;
     const int base = cblk * kThreads * kCopyPerThread + threadIdx.x;
     // all loads first (clamped indices), then the guarded stores
     const int e0 = base, e1 = base + kThreads, e2 = base + 2 * kThreads, e3 = base + 3 * kThreads;
@@ -173,11 +174,11 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
     if (e3 < vec_per_head) { dst_k[e3] = k3; dst_v[e3] = v3; }
     if (a.rope.on) {
       // positional remap: the keys rotated to their own positions go to k_rot
-      uint4* dst_r = (uint4*)a.k_rot + head * (a.capacity * D / VEC) + a.past_len * D / VEC;
+      uint4* dst_r = (uint4*)a.k_rot + head * (a.capacity * D / VEC) + past * D / VEC;
       const int vpp = D / VEC;  // vectors per position
       auto rot = [&](int e, const uint4& w) {
         if (e < vec_per_head)
-          dst_r[e] = rotate_vec<T>(w, a.past_len + e / vpp, (e % vpp) * (VEC / 2), a.rope);
+          dst_r[e] = rotate_vec<T>(w, past + e / vpp, (e % vpp) * (VEC / 2), a.rope);
       };
       rot(e0, k0);
       rot(e1, k1);
@@ -196,10 +197,11 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
     if (gid >= a.batch * a.n_kv_heads * D) return;  // whole waves: the total is a multiple of 64
     const int bg = gid / D, d = gid - bg * D;
     const int b = bg / a.n_kv_heads, g = bg - b * a.n_kv_heads;
+    const int64_t past = seq_past(a, b);
     const int G = GT > 0 ? GT : a.n_q_heads / a.n_kv_heads;
     const T* qb = (const T*)a.q + (int64_t)(b * a.n_q_heads + g * G) * a.q_head_stride + d;
     double* col = a.qprefix + (int64_t)bg * a.ring * D + d;
-    const int slot0 = (int)(a.past_len % a.ring);
+    const int slot0 = (int)(past % a.ring);
     // every load that does not depend on this launch's writes is issued first
     // with the positional remap the stored keys of earlier tokens are read rotated
     const T* kread = (const T*)(a.rope.on ? a.k_rot : a.k_store);
@@ -212,8 +214,8 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
       kt[i] = 0.f;
       if (i < a.n_q) {
         for (int h = 0; h < G; ++h) x[i] += (double)Elem<T>::load(qb + h * a.q_head_stride + (int64_t)i * D);
-        const int64_t t = a.past_len + i - a.n_local;
-        if (t >= a.n_init && t < a.past_len) {
+        const int64_t t = past + i - a.n_local;
+        if (t >= a.n_init && t < past) {
           const int sp = slot0 + i - (slot0 + i >= a.ring ? a.ring : 0);
           const int st = sp - a.n_local + (sp < a.n_local ? a.ring : 0);  // n_local < ring
           ht[i] = col[(int64_t)st * D];
@@ -222,7 +224,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
       }
     }
     double run = 0.0;
-    if (a.past_len > 0) run = col[(int64_t)(slot0 == 0 ? a.ring - 1 : slot0 - 1) * D];
+    if (past > 0) run = col[(int64_t)(slot0 == 0 ? a.ring - 1 : slot0 - 1) * D];
     const double base = run;
     float raw_tot = 0.f;  // the chunk's unrotated query sum (remap: the ring holds rotated sums)
     // R(pos) on dimension d of a pair split over lanes d, d^1 (uniform branch: pos is per position)
@@ -236,18 +238,18 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
     for (int i = 0; i < kThinMaxQ; ++i) {
       if (i >= a.n_q) continue;  // (not break: the loop stays unrolled, the arrays in registers)
       raw_tot += (float)x[i];
-      if (a.rope.on) x[i] = rot_lane(x[i], a.past_len + i);
+      if (a.rope.on) x[i] = rot_lane(x[i], past + i);
       run += x[i];
       const int sp = slot0 + i - (slot0 + i >= a.ring ? a.ring : 0);
       col[(int64_t)sp * D] = run;
-      const int64_t t = a.past_len + i - a.n_local;
+      const int64_t t = past + i - a.n_local;
       if (t >= a.n_init) {
         double h = ht[i], k = kt[i];
-        if (t >= a.past_len) {
+        if (t >= past) {
           // token of this chunk: its running sum was written by this thread above
           const int st = sp - a.n_local + (sp < a.n_local ? a.ring : 0);
           h = col[(int64_t)st * D];
-          k = Elem<T>::load((const T*)a.k_src + (int64_t)bg * a.kv_head_stride + (t - a.past_len) * D + d);
+          k = Elem<T>::load((const T*)a.k_src + (int64_t)bg * a.kv_head_stride + (t - past) * D + d);
           if (a.rope.on) k = rot_lane(k, t);
         }
         double part = k * (run - h);
@@ -264,6 +266,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
   const int slices = D / 16;
   const int bg = blk / slices;
   const int b = bg / a.n_kv_heads, g = bg - b * a.n_kv_heads;
+  const int64_t past = seq_past(a, b);
   const int half = threadIdx.x & 1, seg = threadIdx.x >> 1;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int slice = blk - bg * slices;
@@ -278,9 +281,9 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
   float raw_acc[8];  // unrotated query sum of this thread's positions (the chunk total feeds scoring)
 #pragma unroll
   for (int e = 0; e < 8; ++e) raw_acc[e] = 0.f;
-  const int slot0 = (int)(a.past_len % a.ring);  // ring > n_q: slot0 + i wraps at most once
+  const int slot0 = (int)(past % a.ring);  // ring > n_q: slot0 + i wraps at most once
   double base[8], carry[8];
-  if (a.past_len > 0) {
+  if (past > 0) {
     const double* src = ring + (int64_t)(slot0 == 0 ? a.ring - 1 : slot0 - 1) * D;
 #pragma unroll
     for (int e = 0; e < 8; ++e) base[e] = src[e];
@@ -320,7 +323,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
         const double2* src = (const double2*)(ring + (int64_t)st * D);
 #pragma unroll
         for (int e = 0; e < 4; ++e) ht[s][e] = src[e];
-        int64_t tk = a.past_len + ic - a.n_local;
+        int64_t tk = past + ic - a.n_local;
         tk = tk < 0 ? 0 : tk;
         kr[s] = load_raw8<T>(kread + ((int64_t)bg * a.capacity + tk) * D + d0);
       }
@@ -356,7 +359,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
         // the ring sums the queries rotated to their positions; scoring takes the plain sum
 #pragma unroll
         for (int e = 0; e < 8; ++e) raw_acc[e] += valid ? (float)x[e] : 0.f;
-        rotate8(x, a.past_len + i, d0 / 2, a.rope);
+        rotate8(x, past + i, d0 / 2, a.rope);
       }
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
@@ -421,7 +424,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
 #pragma unroll
       for (int s = 0; s < kSeg; ++s) {
         const int i = i0 + s;
-        const int64_t t = a.past_len + i - a.n_local;
+        const int64_t t = past + i - a.n_local;
         part[s] += __shfl_xor(part[s], 1);  // the two 8-dim halves of the slice
         if (i < a.n_q && t >= a.n_init && half == 0)
           a.rpart[((int64_t)bg * slices + slice) * a.ring + (int)(t % a.ring)] = part[s];
@@ -442,7 +445,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
 #pragma unroll
       for (int s = 0; s < kSeg; ++s) {
         const int ic = min(i0 + s, a.n_q - 1);
-        int64_t t = a.past_len + ic - a.n_local;
+        int64_t t = past + ic - a.n_local;
         t = t < 0 ? 0 : t;
         const int sp = slot0 + ic - (slot0 + ic >= a.ring ? a.ring : 0);
         const int st = sp - a.n_local + (sp < a.n_local ? a.ring : 0);  // n_local < ring
@@ -451,19 +454,19 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
           hp[s][e] = ((const double2*)(ring + (int64_t)sp * D))[e];
           hq[s][e] = ((const double2*)(ring + (int64_t)st * D))[e];
         }
-        kk[s] = t >= a.past_len
-                    ? load_raw8<T>((const T*)a.k_src + (int64_t)bg * a.kv_head_stride + (t - a.past_len) * D + d0)
+        kk[s] = t >= past
+                    ? load_raw8<T>((const T*)a.k_src + (int64_t)bg * a.kv_head_stride + (t - past) * D + d0)
                     : load_raw8<T>(kread + ((int64_t)bg * a.capacity + t) * D + d0);
       }
 #pragma unroll
       for (int s = 0; s < kSeg; ++s) {
         const int i = i0 + s;
-        const int64_t t = a.past_len + i - a.n_local;
+        const int64_t t = past + i - a.n_local;
         const bool act = i < a.n_q && t >= a.n_init;
         float kt[8];
         raw8_to_float<T>(kk[s], kt);
         // a key of this chunk comes unrotated from k_src
-        if (a.rope.on && t >= a.past_len) rotate8(kt, t, d0 / 2, a.rope);
+        if (a.rope.on && t >= past) rotate8(kt, t, d0 / 2, a.rope);
         double p = 0.0;
 #pragma unroll
         for (int e = 0; e < 4; ++e)

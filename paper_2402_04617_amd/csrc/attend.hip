@@ -26,9 +26,8 @@ __global__ void __launch_bounds__(256) attend_f32_kernel(AttendArgs a) {
   __shared__ __attribute__((aligned(16))) float vs[KT][D];
   __shared__ int kval[KT];
 
-  const StepGeom& geo = a.geom;
   const int G = a.n_q_heads / a.n_kv_heads;
-  const int R = G * geo.n_q;
+  const int R = G * a.geom.n_q;
   const int n_row_tiles = (R + RW - 1) / RW;
   const int L = xcd_logical_block(blockIdx.x, gridDim.x);
   const int rt = L % n_row_tiles;
@@ -36,6 +35,10 @@ __global__ void __launch_bounds__(256) attend_f32_kernel(AttendArgs a) {
   const int part = tmp % a.parts;
   const int bg = tmp / a.parts;
   const int b = bg / a.n_kv_heads, g = bg - b * a.n_kv_heads;
+  // this sequence's step (its own past length in a variable-length batch)
+  const SeqStep sq = seq_step(a, b);
+  const StepGeom& geo = sq.geom;
+  const int mem_len = sq.mem_len, parts_mem = sq.parts_mem;
 
   const int n_tiles = (geo.n_virtual + KT - 1) / KT;
   const int per_part = (n_tiles + a.parts - 1) / a.parts;
@@ -91,7 +94,7 @@ __global__ void __launch_bounds__(256) attend_f32_kernel(AttendArgs a) {
       const int64_t pos = v < geo.n_virtual ? virtual_pos(geo, idx_row, v) : -1;
       float4 kk = make_float4(0.f, 0.f, 0.f, 0.f), vv = kk;
       if (pos >= 0) {
-        kk = *(const float4*)((remap && v >= a.mem_len ? krot : kbase) + pos * D + 4 * c);
+        kk = *(const float4*)((remap && v >= mem_len ? krot : kbase) + pos * D + 4 * c);
         vv = *(const float4*)(vbase + pos * D + 4 * c);
       }
       *(float4*)&ks[j][4 * c] = kk;
@@ -100,7 +103,7 @@ __global__ void __launch_bounds__(256) attend_f32_kernel(AttendArgs a) {
     }
     __syncthreads();
     for (int j = 0; j < KT; ++j) {
-      const bool mem_key = remap && t * KT + j < a.mem_len;  // uniform over the workgroup
+      const bool mem_key = remap && t * KT + j < mem_len;  // uniform over the workgroup
       float part_dot = 0.f;
 #pragma unroll
       for (int e = 0; e < DPT; ++e) part_dot += (mem_key ? qm[e] : qv[e]) * ks[j][sub * DPT + e];

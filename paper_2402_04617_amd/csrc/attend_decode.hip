@@ -116,10 +116,13 @@ __global__ void __launch_bounds__(64 * kDecodeWaves) attend_decode_kernel(Attend
   __shared__ int32_t sidx[kDecodeMaxSel];
   __shared__ float fo[G][D];  // this part's output rows before the fp16 write
 
-  const StepGeom& geo = a.geom;
   const int part = blockIdx.x % a.parts;
   const int bg = blockIdx.x / a.parts;
   const int b = bg / a.n_kv_heads, g = bg - b * a.n_kv_heads;
+  // this sequence's step (its own past length in a variable-length batch)
+  const SeqStep sq = seq_step(a, b);
+  const StepGeom& geo = sq.geom;
+  const int mem_len = sq.mem_len, parts_mem = sq.parts_mem;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int c = lane % LPK, r = lane / LPK;  // 16-byte piece of the row, key slot of the load
   for (int j = tid; j < geo.n_sel; j += 64 * kDecodeWaves) sidx[j] = a.idx[(int64_t)bg * geo.idx_stride + j];
@@ -128,15 +131,15 @@ __global__ void __launch_bounds__(64 * kDecodeWaves) attend_decode_kernel(Attend
   // wave.  With the positional remap parts [0, parts_mem) split the memory keys
   // [0, mem_len) (I and the units) and the other parts the local keys.
   const bool remap = a.rope.on != 0;
-  const bool mem_part = part < a.parts_mem;
+  const bool mem_part = part < parts_mem;
   int rv0 = 0, rv1 = geo.n_virtual, rpart = part, rparts = a.parts;
   if (mem_part) {
-    rv1 = a.mem_len;
-    rparts = a.parts_mem;
-  } else if (a.parts_mem > 0) {
-    rv0 = a.mem_len;
-    rpart = part - a.parts_mem;
-    rparts = a.parts - a.parts_mem;
+    rv1 = mem_len;
+    rparts = parts_mem;
+  } else if (parts_mem > 0) {
+    rv0 = mem_len;
+    rpart = part - parts_mem;
+    rparts = a.parts - parts_mem;
   }
   const int n_waves_total = rparts * kDecodeWaves;
   const int kpw = ((rv1 - rv0 + n_waves_total - 1) / n_waves_total + TK - 1) / TK * TK;

@@ -115,9 +115,8 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
   static_assert(2 * NI <= KSTEPS, "one load per chunk of the MFMA phase");
   __shared__ __attribute__((aligned(256))) Smem<D> sm;
 
-  const StepGeom& geo = a.geom;
   const int G = a.n_q_heads / a.n_kv_heads;
-  const int R = G * geo.n_q;
+  const int R = G * a.geom.n_q;
   const int n_row_tiles = (R + ROWS_WG - 1) / ROWS_WG;
   const int L = xcd_logical_block(blockIdx.x, gridDim.x);
   const int rt = L % n_row_tiles;
@@ -125,6 +124,10 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
   const int part = tmp % a.parts;
   const int bg = tmp / a.parts;
   const int b = bg / a.n_kv_heads, g = bg - b * a.n_kv_heads;
+  // this sequence's step (its own past length in a variable-length batch)
+  const SeqStep sq = seq_step(a, b);
+  const StepGeom& geo = sq.geom;
+  const int mem_len = sq.mem_len, parts_mem = sq.parts_mem;
 
   // This part's tiles.  Without the positional remap the parts split the tiles
   // evenly.  With it, parts [0, parts_mem) split the memory tiles [0,
@@ -134,15 +137,15 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
   // kinds is taken by both sides, each masking the other's keys.
   const int n_tiles = (geo.n_virtual + KB - 1) / KB;
   const bool remap = a.rope.on != 0;
-  const bool mem_part = part < a.parts_mem;
+  const bool mem_part = part < parts_mem;
   int rt0 = 0, rt1 = n_tiles, rpart = part, rparts = a.parts;
   if (mem_part) {
-    rt1 = (a.mem_len + KB - 1) / KB;
-    rparts = a.parts_mem;
-  } else if (a.parts_mem > 0) {
-    rt0 = a.mem_len / KB;
-    rpart = part - a.parts_mem;
-    rparts = a.parts - a.parts_mem;
+    rt1 = (mem_len + KB - 1) / KB;
+    rparts = parts_mem;
+  } else if (parts_mem > 0) {
+    rt0 = mem_len / KB;
+    rpart = part - parts_mem;
+    rparts = a.parts - parts_mem;
   }
   const int per_part = (rt1 - rt0 + rparts - 1) / rparts;
   const int t_begin = rt0 + rpart * per_part;
@@ -162,7 +165,7 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
   const int qi = row_ok ? row / G : 0;
   // last virtual key this row may see: causal within X (which also excludes the
   // ragged end), or for a memory part of the remap the last memory key
-  const int vlim = mem_part ? a.mem_len - 1 : v_x0 + qi;
+  const int vlim = mem_part ? mem_len - 1 : v_x0 + qi;
   const int qh = g * G + (row_ok ? row - qi * G : 0);
 
   const int32_t* idx_row = a.idx + (int64_t)bg * geo.idx_stride;
@@ -481,7 +484,7 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
   // looked up at the end of an iteration, so their scalar loads complete under
   // the barrier.
   // Tiles wholly before X need no mask unless skipped unit entries exist.
-  const int t_plain = has_invalid ? t_begin : max(t_begin, min(t_end, (mem_part ? a.mem_len : v_x0) / KB));
+  const int t_plain = has_invalid ? t_begin : max(t_begin, min(t_end, (mem_part ? mem_len : v_x0) / KB));
   int64_t run_k = -1, run_v = -1;  // run starts of the next K and V loads: tiles t+3, t+2
   // Run starts of the part's tiles, computed once by all lanes into LDS; the
   // per-iteration lookup is then an LDS read (a global read here would wait
@@ -623,9 +626,9 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
     publish_barrier<4 * NI>();  // K(t0) has landed
     qk(0, sA);
     if (t_begin >= t_plain) apply_mask(t_begin, 0, sA);
-    if (!mem_part && a.parts_mem > 0 && t_begin * KB < a.mem_len) {
+    if (!mem_part && parts_mem > 0 && t_begin * KB < mem_len) {
       // the first local tile also holds the last memory keys: hide them here
-      const int lo = a.mem_len - t_begin * KB - 4 * gsel;
+      const int lo = mem_len - t_begin * KB - 4 * gsel;
 #pragma unroll
       for (int kb = 0; kb < 2; ++kb)
 #pragma unroll

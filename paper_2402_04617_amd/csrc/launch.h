@@ -11,6 +11,38 @@
 
 namespace infllm {
 
+// Variable-length batches: sequence b has its own past length past[b] (all
+// sequences append the same number of tokens).  Kernels derive each sequence's
+// step geometry from it with the host's partition arithmetic.
+constexpr int kMaxVarBatch = 64;
+struct VarLen {
+  int32_t on;
+  int64_t past[kMaxVarBatch];
+};
+
+// Memory parts of a step split by the positional remap: the memory keys' share
+// of `parts`, at least one part per non-empty region.
+__host__ __device__ inline int split_parts_mem(int parts, int64_t mem_len, int64_t n_virtual) {
+  if (mem_len <= 0 || parts < 2) return 0;
+  int pm = (int)((parts * mem_len + n_virtual / 2) / n_virtual);
+  return pm < 1 ? 1 : (pm > parts - 1 ? parts - 1 : pm);
+}
+
+// Step geometry of a sequence with past length `past` (the partition of
+// Section 3.1): `base` supplies the shared fields (l_bs, l_I, k_m, l_X).
+__host__ __device__ inline StepGeom seq_geom(const StepGeom& base, int n_local, int64_t past) {
+  StepGeom g = base;
+  g.n_init = (int32_t)(past < base.unit_base ? past : base.unit_base);
+  const int64_t evicted = past - base.unit_base - n_local;
+  const int64_t nu = evicted > 0 ? evicted / base.block_size : 0;
+  g.n_units = (int32_t)nu;
+  g.n_sel = (int32_t)(base.idx_stride < nu ? base.idx_stride : nu);
+  g.local_begin = g.n_init + nu * base.block_size;
+  g.past_len = past;
+  g.n_virtual = (int32_t)(g.n_init + (int64_t)g.n_sel * base.block_size + (past - g.local_begin) + base.n_q);
+  return g;
+}
+
 struct AppendArgs {
   int batch, n_q_heads, n_kv_heads, head_dim, n_q, ring, n_init, n_local;
   int64_t past_len, capacity, q_head_stride, kv_head_stride;
@@ -23,9 +55,12 @@ struct AppendArgs {
   double* rpart;  // [B*Hkv][D/16][ring] partial representative scores
   void* k_rot;    // positional remap: keys rotated to their own positions (same layout as k_store)
   RopeArgs rope;
+  VarLen var;      // per-sequence past lengths (var.on), else past_len for all
   bool mean_repr;  // units scored by their mean key: no query ring, no representative scores
   bool bf16;
 };
+// Past length of sequence b of an append.
+__host__ __device__ inline int64_t seq_past(const AppendArgs& a, int b) { return a.var.on ? a.var.past[b] : a.past_len; }
 struct BuildArgs;
 int score_qbar_parts(int G, int n_q);
 // qbar: optional float32 output of the chunk's group-query sums: [batch*Hkv][D]
@@ -45,6 +80,11 @@ struct BuildArgs {
   float* unit_ksum;
   double* repr_score;  // nullable
   bool mean_repr;      // unit_ksum = mean of the unit's l_bs keys (no representatives)
+  // Variable-length batches: sequence b builds units [first[b], first[b] + count[b])
+  // (var_on); otherwise every sequence builds [first_unit, first_unit + n_new).
+  int32_t var_on;
+  int32_t var_first[kMaxVarBatch];
+  int32_t var_count[kMaxVarBatch];
   bool bf16;
 };
 hipError_t launch_build_units(const BuildArgs& a, hipStream_t s);
@@ -57,6 +97,11 @@ struct ScoreArgs {
   float* scores;
   float* qbar_parts;  // workspace
   RopeArgs rope;      // positional remap: the query sum is turned by R(l_L)
+  // Variable-length batches: sequence b scores var_units[b] units, rows of
+  // `scores` strided by score_stride (var_on); otherwise n_units each, stride n_units.
+  int32_t var_on;
+  int32_t var_units[kMaxVarBatch];
+  int32_t score_stride;
   bool bf16;
 };
 int score_qbar_parts(int G, int n_q);
@@ -66,6 +111,14 @@ hipError_t launch_score_given_qbar(const ScoreArgs& a, int parts, hipStream_t s)
 
 hipError_t launch_select_topk(int rows, const float* scores, int n_units, int k, int32_t* idx,
                               hipStream_t s);
+// Rows of different lengths: row r holds row_n[r / rows_per_seq] scores at stride
+// `stride`; n_max bounds them.
+struct TopkRows {
+  int32_t rows_per_seq;
+  int32_t row_n[kMaxVarBatch];
+};
+hipError_t launch_select_topk_var(int rows, const float* scores, int stride, int n_max, const TopkRows& tr, int k,
+                                  int32_t* idx, hipStream_t s);
 
 // Query rows per workgroup of the bf16 matrix-core attention kernel, and the
 // workgroup count the part chooser aims for (one per compute unit).
@@ -96,6 +149,11 @@ struct AttendArgs {
   int parts_mem;
   int mem_len;
   RopeArgs rope;
+  // Variable-length batches (var.on): each sequence's geometry, memory length and
+  // memory parts are derived from var.past[b] (n_local is l_L); geom, mem_len and
+  // parts_mem then only carry the shared fields.
+  VarLen var;
+  int n_local;
   const int32_t* idx;
   void* out;     // final output (one part)
   float* lse;    // nullable
@@ -107,6 +165,25 @@ struct AttendArgs {
   int parts;
   bool bf16;
 };
+// The step of sequence b as a kernel sees it.
+struct SeqStep {
+  StepGeom geom;
+  int mem_len;
+  int parts_mem;
+};
+__host__ __device__ inline SeqStep seq_step(const AttendArgs& a, int b) {
+  SeqStep r;
+  if (!a.var.on) {
+    r.geom = a.geom;
+    r.mem_len = a.mem_len;
+    r.parts_mem = a.parts_mem;
+    return r;
+  }
+  r.geom = seq_geom(a.geom, a.n_local, a.var.past[b]);
+  r.mem_len = r.geom.n_init + r.geom.n_sel * r.geom.block_size;
+  r.parts_mem = a.rope.on ? split_parts_mem(a.parts, r.mem_len, r.geom.n_virtual) : 0;
+  return r;
+}
 // Number of key parts the attention uses for this shape, limited by max_parts.
 int attend_choose_parts(bool bf16, int batch, int n_q_heads, int n_kv_heads, int n_q, int n_sel, int n_virtual,
                         int max_parts);

@@ -27,16 +27,16 @@ __global__ void __launch_bounds__(kQsumThreads) qbar_kernel(const T* __restrict_
 // grid (ceil(n_units/256), batch*Hkv); one unit per thread.  With the
 // positional remap the memory keys sit at distance l_L from every current token,
 // so the query sum is turned by R(l_L) before the dot products (the keys stay
-// unrotated).
-__global__ void __launch_bounds__(256) score_kernel(const float* __restrict__ qbar_parts, int parts,
-                                                    const float4* __restrict__ unit_ksum, int head_dim,
-                                                    int n_units, int max_units, float* __restrict__ scores,
-                                                    const RopeArgs rope) {
+// unrotated).  In a variable-length batch sequence b scores its own unit count
+// (units past it are left alone) into rows of stride score_stride.
+__global__ void __launch_bounds__(256) score_kernel(const ScoreArgs a, int parts) {
   const int bg = blockIdx.y;
+  const int head_dim = a.head_dim;
+  const RopeArgs& rope = a.rope;
   __shared__ float qbar[256];
   for (int d = threadIdx.x; d < head_dim; d += 256) {
     float s = 0.f;
-    for (int p = 0; p < parts; ++p) s += qbar_parts[((int64_t)bg * parts + p) * head_dim + d];
+    for (int p = 0; p < parts; ++p) s += a.qbar_parts[((int64_t)bg * parts + p) * head_dim + d];
     qbar[d] = s;
   }
   __syncthreads();
@@ -56,17 +56,18 @@ __global__ void __launch_bounds__(256) score_kernel(const float* __restrict__ qb
     }
     __syncthreads();
   }
+  const int n_units = a.var_on ? a.var_units[bg / a.n_kv_heads] : a.n_units;
   const int u = blockIdx.x * 256 + threadIdx.x;
   if (u >= n_units) return;
   const int nc = head_dim / 4;
-  const float4* ks = unit_ksum + (int64_t)bg * nc * max_units + u;
+  const float4* ks = (const float4*)a.unit_ksum + (int64_t)bg * nc * a.max_units + u;
   float acc = 0.f;
 #pragma unroll 8
   for (int c = 0; c < nc; ++c) {
-    const float4 k4 = ks[(int64_t)c * max_units];
+    const float4 k4 = ks[(int64_t)c * a.max_units];
     acc += qbar[4 * c] * k4.x + qbar[4 * c + 1] * k4.y + qbar[4 * c + 2] * k4.z + qbar[4 * c + 3] * k4.w;
   }
-  scores[(int64_t)bg * n_units + u] = acc;
+  a.scores[(int64_t)bg * (a.var_on ? a.score_stride : n_units) + u] = acc;
 }
 
 }  // namespace
@@ -93,9 +94,8 @@ hipError_t launch_score(const ScoreArgs& a, hipStream_t s) {
 
 hipError_t launch_score_given_qbar(const ScoreArgs& a, int parts, hipStream_t s) {
   if (a.n_units == 0) return hipSuccess;
-  dim3 g2((a.n_units + 255) / 256, a.batch * a.n_kv_heads);
-  hipLaunchKernelGGL(score_kernel, g2, dim3(256), 0, s, (const float*)a.qbar_parts, parts,
-                     (const float4*)a.unit_ksum, a.head_dim, a.n_units, a.max_units, a.scores, a.rope);
+  dim3 g2((a.n_units + 255) / 256, a.batch * a.n_kv_heads);  // n_units: the largest count of the batch
+  hipLaunchKernelGGL(score_kernel, g2, dim3(256), 0, s, a, parts);
   return hipGetLastError();
 }
 

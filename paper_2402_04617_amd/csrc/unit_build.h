@@ -29,10 +29,10 @@ struct BuildSmem {
 };
 
 template <typename T, int D, int NT>
-__device__ __forceinline__ void build_one_unit(const BuildArgs& a, int unit_local, int bg, BuildSmem& sm) {
+__device__ __forceinline__ void build_one_unit(const BuildArgs& a, int unit, int unit_local, int bg,
+                                               BuildSmem& sm) {
   static_assert(NT % 64 == 0 && NT >= 256 && NT <= 1024, "block size");
   constexpr int SLICES = D / 16;
-  const int unit = a.first_unit + unit_local;
   const int lbs = a.block_size;
   const int tid = threadIdx.x;
   const int64_t m0 = (int64_t)a.n_init + (int64_t)unit * lbs;
@@ -123,11 +123,10 @@ __device__ __forceinline__ void build_one_unit(const BuildArgs& a, int unit_loca
 // 16-byte pieces by LPK adjacent threads; KG groups of them take interleaved
 // rows, and the groups' partial sums are added in a fixed order.
 template <typename T, int D, int NT>
-__device__ __forceinline__ void mean_one_unit(const BuildArgs& a, int unit_local, int bg, BuildSmem& sm) {
+__device__ __forceinline__ void mean_one_unit(const BuildArgs& a, int unit, int bg, BuildSmem& sm) {
   constexpr int VEC = 16 / (int)sizeof(T);  // elements per 16-byte piece
   constexpr int LPK = D / VEC;              // threads per key row
   constexpr int KG = (NT / LPK) < (kMaxSumElems / D) ? (NT / LPK) : (kMaxSumElems / D);
-  const int unit = a.first_unit + unit_local;
   const int lbs = a.block_size;
   const int64_t m0 = (int64_t)a.n_init + (int64_t)unit * lbs;
   const T* kb = (const T*)a.k_store + ((int64_t)bg * a.capacity + m0) * D;
@@ -155,11 +154,20 @@ __device__ __forceinline__ void mean_one_unit(const BuildArgs& a, int unit_local
   }
 }
 
-// One unit of either representation.
+// Unit `unit_local` of the units this (sequence, kv head) builds, in either
+// representation.  In a variable-length batch each sequence has its own range;
+// blocks past a sequence's count return at once (before any barrier).
 template <typename T, int D, int NT>
 __device__ __forceinline__ void construct_unit(const BuildArgs& a, int unit_local, int bg, BuildSmem& sm) {
-  if (a.mean_repr) mean_one_unit<T, D, NT>(a, unit_local, bg, sm);
-  else build_one_unit<T, D, NT>(a, unit_local, bg, sm);
+  int first = a.first_unit, count = a.n_new;
+  if (a.var_on) {
+    const int b = bg / a.n_kv_heads;
+    first = a.var_first[b];
+    count = a.var_count[b];
+  }
+  if (unit_local >= count) return;
+  if (a.mean_repr) mean_one_unit<T, D, NT>(a, first + unit_local, bg, sm);
+  else build_one_unit<T, D, NT>(a, first + unit_local, unit_local, bg, sm);
 }
 
 }  // namespace infllm

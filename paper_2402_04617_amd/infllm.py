@@ -25,7 +25,7 @@ STATUS = {0: "INFLLM_OK", 1: "INFLLM_E_NULL", 2: "INFLLM_E_SHAPE", 3: "INFLLM_E_
 
 EXPORTS = ["infllm_partition", "infllm_workspace_bytes", "infllm_append", "infllm_build_units",
            "infllm_score_units", "infllm_select_topk", "infllm_chunk_attend", "infllm_attend_partial",
-           "infllm_lse_merge", "infllm_step", "infllm_status_string"]
+           "infllm_lse_merge", "infllm_step", "infllm_step_varlen", "infllm_status_string"]
 
 
 class InfllmError(RuntimeError):
@@ -84,6 +84,8 @@ def lib() -> ctypes.CDLL:
                                   ctypes.POINTER(i32), vp],
         "infllm_lse_merge": [P, i32, i32, i32, vp, sz, vp, i64, vp, vp],
         "infllm_step": [P, M, vp, i64, vp, vp, i64, i32, i64, i32, vp, vp, vp, i64, vp, vp, sz, vp],
+        "infllm_step_varlen": [P, M, vp, i64, vp, vp, i64, i32, ctypes.POINTER(i64), ctypes.POINTER(i32), vp, vp,
+                               vp, i64, vp, vp, sz, vp],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -189,6 +191,18 @@ def infllm_step(p, m, q, q_head_stride, k, v, kv_head_stride, n_q, past_len, uni
         ctypes.byref(p), ctypes.byref(m), _ptr(q), q_head_stride, _ptr(k), _ptr(v), kv_head_stride, n_q, past_len,
         units_built, _ptr(scores), _ptr(idx), _ptr(out), out_head_stride, _ptr(lse), _ptr(workspace), wb,
         _stream(stream)))
+
+
+def infllm_step_varlen(p, m, q, q_head_stride, k, v, kv_head_stride, n_q, past_lens, units_built, scores, idx, out,
+                       out_head_stride, lse=None, workspace=None, workspace_bytes=None, stream=None):
+    """past_lens, units_built: sequences of `batch` ints (host)."""
+    wb = (0 if workspace is None else workspace.numel() * workspace.element_size()) \
+        if workspace_bytes is None else workspace_bytes
+    pl = (ctypes.c_int64 * len(past_lens))(*[int(x) for x in past_lens])
+    ub = (ctypes.c_int32 * len(units_built))(*[int(x) for x in units_built])
+    _check("infllm_step_varlen", lib().infllm_step_varlen(
+        ctypes.byref(p), ctypes.byref(m), _ptr(q), q_head_stride, _ptr(k), _ptr(v), kv_head_stride, n_q, pl, ub,
+        _ptr(scores), _ptr(idx), _ptr(out), out_head_stride, _ptr(lse), _ptr(workspace), wb, _stream(stream)))
 
 
 # ------------------------------------------------------------------ allocation plumbing

@@ -233,6 +233,31 @@ def test_remap_validation(L):
     assert L.infllm_workspace_bytes(ctypes.byref(pd), 1, 1) >= 2 * 32 * row
 
 
+def test_step_varlen_validation(L):
+    """Variable-length steps: host arrays required, at most 64 sequences, every sequence validated
+    as its own step (its own capacity and unit checks) before anything runs."""
+    p = P()
+    S = 512 * 128
+    m = mem(batch=3)
+    f = L.infllm_step_varlen
+    pl = (ctypes.c_int64 * 3)(8192, 100, 20000)
+    ub = (ctypes.c_int32 * 3)(31, 0, 100)
+    bp, bm = ctypes.byref(p), ctypes.byref(m)
+    args = lambda pl_, ub_: (bp, bm, FAKE, S, None, None, 0, 1, pl_, ub_, FAKE, FAKE, FAKE, 128, None, FAKE,  # noqa
+                            1 << 30, None)
+    assert f(*args(None, ub)) == 1
+    assert f(*args(pl, None)) == 1
+    big = mem(batch=65)
+    assert f(bp, ctypes.byref(big), FAKE, S, None, None, 0, 1, pl, ub, FAKE, FAKE, FAKE, 128, None, FAKE, 1 << 30,
+             None) == 4
+    bad = (ctypes.c_int32 * 3)(31, 1, 100)      # sequence 1 has no unit to have built
+    assert f(*args(pl, bad)) == 2
+    far = (ctypes.c_int64 * 3)(8192, 100, (1 << 17))  # sequence 2 past the capacity
+    assert f(*args(far, ub)) == 3
+    neg = (ctypes.c_int64 * 3)(8192, -1, 20000)
+    assert f(*args(neg, ub)) == 2
+
+
 def test_mean_repr_validation(L):
     """Mean representation: an unknown mode is a shape error; the query ring, rpart and repr_idx
     are not needed (their absence is not reported, the call reaches the device check)."""
