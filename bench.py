@@ -313,6 +313,27 @@ def decode_leg(seed, steps, warmup, torch):
     return res, st
 
 
+def multilayer_leg(st1, layers, steps, warmup, torch):
+    """Streaming encode of a whole model's attention memory: `layers` layers of the 1M workload,
+    each with its own context memory resident in HBM (no offload), chunk-major (every layer's
+    step for a chunk before the next chunk).  All layers read the same synthetic inputs, which
+    changes nothing in the work done."""
+    wl = st1.wl
+    streams = [st1] + [Stream(wl, st1.inp, torch) for _ in range(layers - 1)]
+    plan = wl.step_starts()
+
+    def run():
+        built = [0] * layers
+        for past, n in plan:
+            for li, st in enumerate(streams):
+                built[li] = st.step(past, n, built[li])
+    ms = time_steps(torch, run, steps, warmup)
+    hbm = sum(sum(t.numel() * t.element_size() for t in (s_.mem.k, s_.mem.v, s_.mem.unit_ksum, s_.mem.repr_idx,
+                                                           s_.mem.qprefix, s_.mem.rpart)) for s_ in streams)
+    return {"workload": f"{wl.name} x {layers} layers", "layers": layers, "seq_len": wl.seq_len, "ms_per_step": ms,
+            "ctx_tok_per_s": wl.seq_len / (ms / 1e3), "memory_resident_gb": hbm / 1e9}
+
+
 def decode_varlen_leg(st, steps, warmup, torch, spacing=6144):
     """Serving-style decode: the 16 sequences at different depths (128K, 122K, ..., 38K prior tokens),
     stepped together by infllm_step_varlen.  Each sequence's memory is first rebuilt alone to its
@@ -415,8 +436,8 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--legs", default="1m,1m-paper,decode,remap,mean",
-                    help="extra legs: comma list of 1m, 1m-paper, decode, remap, mean (or 'none')")
+    ap.add_argument("--legs", default="1m,1m-paper,32l-1m,decode,remap,mean",
+                    help="extra legs: comma list of 1m, 1m-paper, 32l-1m, decode, remap, mean (or 'none')")
     ap.add_argument("--sweep", action="store_true",
                     help="only time the 128K stream under the paper's memory settings (r_k, k_m, l_bs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -464,7 +485,7 @@ def main():
         log(f"128K mean repr: {rm['ms_per_step']:.2f} ms/step, {rm['ctx_tok_per_s'] / 1e6:.2f}M ctx tok/s")
     del st
     torch.cuda.empty_cache()
-    if "1m" in legs or "1m-paper" in legs:
+    if "1m" in legs or "1m-paper" in legs or "32l-1m" in legs:
         r1, _, st1 = encode_leg("llama3-8b-1m", args.seed, max(1, min(args.steps, 2)), 1, torch)
         if "1m" in legs:
             extra["encode_1m"] = r1
@@ -477,6 +498,15 @@ def main():
             extra["encode_1m_paper_settings"] = rp
             log(f"1M (chunk 2048, r_k 1): {rp['ms_per_step']:.1f} ms/step, "
                 f"{rp['ctx_tok_per_s'] / 1e6:.2f}M ctx tok/s")
+        if "32l-1m" in legs:
+            try:
+                rl = multilayer_leg(st1, 32, 1, 1, torch)
+                extra["encode_1m_32_layers"] = rl
+                log(f"1M x 32 layers: {rl['ms_per_step'] / 1e3:.2f} s/pass, {rl['ctx_tok_per_s'] / 1e3:.0f}K ctx tok/s "
+                    f"through all layers, {rl['memory_resident_gb']:.0f} GB of memory resident")
+            except torch.cuda.OutOfMemoryError as e:  # report, keep the rest of the line
+                extra["encode_1m_32_layers"] = {"error": f"out of device memory: {e}"[:200]}
+            torch.cuda.empty_cache()
         del st1
         torch.cuda.empty_cache()
     if "decode" in legs:
