@@ -124,7 +124,9 @@ struct AppendGrid {
 };
 
 // GT: the query group size G when known at compile time (0: read it at run time).
-template <typename T, int GT, int DT>
+// ROPE: the positional remap is on (a.rope.on), fixed at compile time so that
+// the plain path carries none of its code.
+template <typename T, int GT, int DT, bool ROPE>
 __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArgs ba, AppendGrid grid,
                                                           float* __restrict__ qbar) {
   const int D = a.head_dim;
@@ -172,7 +174,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
     if (e1 < vec_per_head) { dst_k[e1] = k1; dst_v[e1] = v1; }
     if (e2 < vec_per_head) { dst_k[e2] = k2; dst_v[e2] = v2; }
     if (e3 < vec_per_head) { dst_k[e3] = k3; dst_v[e3] = v3; }
-    if (a.rope.on) {
+    if (ROPE) {
       // positional remap: the keys rotated to their own positions go to k_rot
       uint4* dst_r = (uint4*)a.k_rot + head * (a.capacity * D / VEC) + past * D / VEC;
       const int vpp = D / VEC;  // vectors per position
@@ -204,7 +206,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
     const int slot0 = (int)(past % a.ring);
     // every load that does not depend on this launch's writes is issued first
     // with the positional remap the stored keys of earlier tokens are read rotated
-    const T* kread = (const T*)(a.rope.on ? a.k_rot : a.k_store);
+    const T* kread = (const T*)(ROPE ? a.k_rot : a.k_store);
     double x[kThinMaxQ], ht[kThinMaxQ];
     float kt[kThinMaxQ];
 #pragma unroll
@@ -238,7 +240,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
     for (int i = 0; i < kThinMaxQ; ++i) {
       if (i >= a.n_q) continue;  // (not break: the loop stays unrolled, the arrays in registers)
       raw_tot += (float)x[i];
-      if (a.rope.on) x[i] = rot_lane(x[i], past + i);
+      if (ROPE) x[i] = rot_lane(x[i], past + i);
       run += x[i];
       const int sp = slot0 + i - (slot0 + i >= a.ring ? a.ring : 0);
       col[(int64_t)sp * D] = run;
@@ -250,7 +252,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
           const int st = sp - a.n_local + (sp < a.n_local ? a.ring : 0);
           h = col[(int64_t)st * D];
           k = Elem<T>::load((const T*)a.k_src + (int64_t)bg * a.kv_head_stride + (t - past) * D + d);
-          if (a.rope.on) k = rot_lane(k, t);
+          if (ROPE) k = rot_lane(k, t);
         }
         double part = k * (run - h);
 #pragma unroll
@@ -258,7 +260,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
         if ((d & 15) == 0) a.rpart[((int64_t)bg * (D / 16) + d / 16) * a.ring + (int)(t % a.ring)] = part;
       }
     }
-    if (qbar != nullptr) qbar[(int64_t)bg * D + d] = a.rope.on ? raw_tot : (float)(run - base);
+    if (qbar != nullptr) qbar[(int64_t)bg * D + d] = ROPE ? raw_tot : (float)(run - base);
     return;
   }
 
@@ -277,7 +279,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
 
   __shared__ double wave_tot[kWaves][2][8];
   __shared__ float wave_raw[kWaves][2][8];
-  const T* kread = (const T*)(a.rope.on ? a.k_rot : a.k_store);  // stored keys, rotated under the remap
+  const T* kread = (const T*)(ROPE ? a.k_rot : a.k_store);  // stored keys, rotated under the remap
   float raw_acc[8];  // unrotated query sum of this thread's positions (the chunk total feeds scoring)
 #pragma unroll
   for (int e = 0; e < 8; ++e) raw_acc[e] = 0.f;
@@ -355,7 +357,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
           for (int e = 0; e < 8; ++e) x[e] += (double)y[e];
         }
       }
-      if (a.rope.on) {
+      if (ROPE) {
         // the ring sums the queries rotated to their positions; scoring takes the plain sum
 #pragma unroll
         for (int e = 0; e < 8; ++e) raw_acc[e] += valid ? (float)x[e] : 0.f;
@@ -466,7 +468,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
         float kt[8];
         raw8_to_float<T>(kk[s], kt);
         // a key of this chunk comes unrotated from k_src
-        if (a.rope.on && t >= past) rotate8(kt, t, d0 / 2, a.rope);
+        if (ROPE && t >= past) rotate8(kt, t, d0 / 2, a.rope);
         double p = 0.0;
 #pragma unroll
         for (int e = 0; e < 4; ++e)
@@ -476,7 +478,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
       }
     }
   }
-  if (qbar != nullptr && a.rope.on) {
+  if (qbar != nullptr && ROPE) {
     // plain query sum of the chunk: over the 32 segments of this half in the
     // wave, then over the waves
 #pragma unroll
@@ -513,8 +515,13 @@ static hipError_t launch_append_d(const AppendArgs& a, const BuildArgs& ba, cons
   if (blocks == 0) return hipSuccess;
   const dim3 grid(blocks);
   const int G = a.n_q_heads / a.n_kv_heads;
-#define INFLLM_APPEND(T, GT) \
-  hipLaunchKernelGGL((append_kernel<T, GT, DT>), grid, dim3(kThreads), 0, s, a, ba, g, qbar)
+#define INFLLM_APPEND(T, GT)                                                                        \
+  do {                                                                                             \
+    if (a.rope.on)                                                                                 \
+      hipLaunchKernelGGL((append_kernel<T, GT, DT, true>), grid, dim3(kThreads), 0, s, a, ba, g, qbar);  \
+    else                                                                                           \
+      hipLaunchKernelGGL((append_kernel<T, GT, DT, false>), grid, dim3(kThreads), 0, s, a, ba, g, qbar); \
+  } while (0)
   if (a.bf16) {
     switch (G) {
       case 1: INFLLM_APPEND(bf16_t, 1); break;
