@@ -252,7 +252,10 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
           const int st = sp - a.n_local + (sp < a.n_local ? a.ring : 0);
           h = col[(int64_t)st * D];
           k = Elem<T>::load((const T*)a.k_src + (int64_t)bg * a.kv_head_stride + (t - past) * D + d);
-          if (ROPE) k = rot_lane(k, t);
+          if (ROPE) {
+            k = rot_lane(k, t);  // as the copy blocks store it in k_rot
+            if constexpr (sizeof(T) == 2) k = (double)bf16_to_f32(f32_to_bf16((float)k));
+          }
         }
         double part = k * (run - h);
 #pragma unroll
@@ -467,8 +470,15 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
         const bool act = i < a.n_q && t >= a.n_init;
         float kt[8];
         raw8_to_float<T>(kk[s], kt);
-        // a key of this chunk comes unrotated from k_src
-        if (ROPE && t >= past) rotate8(kt, t, d0 / 2, a.rope);
+        // a key of this chunk comes unrotated from k_src; rotated here and rounded to
+        // the store's dtype, it equals what the copy blocks write to k_rot
+        if (ROPE && t >= past) {
+          rotate8(kt, t, d0 / 2, a.rope);
+          if constexpr (sizeof(T) == 2) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) kt[e] = bf16_to_f32(f32_to_bf16(kt[e]));
+          }
+        }
         double p = 0.0;
 #pragma unroll
         for (int e = 0; e < 4; ++e)

@@ -35,7 +35,8 @@ def host(t: torch.Tensor) -> np.ndarray:
 def oparams(p: F.Params) -> O.Params:
     freqs = tuple(float(p.rope_inv_freq[i]) for i in range(p.head_dim // 2)) if p.remap else None
     return O.Params(p.n_q_heads, p.n_kv_heads, p.head_dim, p.n_init, p.n_local, p.block_size, p.n_repr,
-                    p.topk, float(p.sm_scale), freqs, p.mean_repr)
+                    p.topk, float(p.sm_scale), rope_inv_freq=freqs, mean_repr=p.mean_repr,
+                    rope_keys_bf16=p.remap and p.dtype == F.INFLLM_BF16)
 
 
 class Layer:
@@ -111,3 +112,40 @@ def check_selection(gpu_row: np.ndarray, oracle_row: np.ndarray, oracle_scores: 
     band = rel * max(abs(s_sorted[k_eff - 1]), float(np.sqrt(np.mean(oracle_scores ** 2))))
     assert np.all(oracle_scores[g] >= s_sorted[k_eff - 1] - band)
     return False
+
+
+def conditioned_step(so: "O.StreamOracle", b: int, past: int, n: int, gpu_repr_idx: np.ndarray) -> dict:
+    """The oracle's step for sequence b, conditioned on the device's unit representatives.
+
+    Representative sets are an integer decision on r_m; where the device's set differs from the
+    oracle's, it must lie inside the r_m near-tie band (the same 1e-3 rule as the lookup), and the
+    oracle then scores that unit with the device's set (a conditioned oracle: scores, lookup and
+    attention all follow from it).  gpu_repr_idx: [Hkv][>= n_units][r_k] offsets of sequence b.
+    Returns the step dict with the conditioned scores and lookup, plus "rep_ties": units that
+    differed."""
+    p = so.p
+    G = p.group
+    nu = O.partition(past, p).n_units
+    if p.mean_repr or nu == 0:
+        r = so.step(b, past, n)
+        r["rep_ties"] = 0
+        return r
+    scores = np.zeros((p.n_kv_heads, nu))
+    ties = 0
+    for g in range(p.n_kv_heads):
+        reps = []
+        for u in range(nu):
+            mine = so.repr_offsets(b, g, u)
+            dev_off = np.sort(np.asarray(gpu_repr_idx[g, u], dtype=np.int64))
+            if not np.array_equal(mine, dev_off):
+                check_selection(np.asarray(gpu_repr_idx[g, u], dtype=np.int64), mine, so.repr_scores(b, g, u),
+                                p.n_repr)
+                ties += 1
+            reps.append(O.unit_start(u, p) + dev_off)
+        qx = so.q[b, g * G:(g + 1) * G, past:past + n]
+        scores[g] = O.unit_relevance(qx, so.k[b, g], np.stack(reps), p)
+    sel = np.stack([O.select_units(scores[g], p) for g in range(p.n_kv_heads)])
+    r = so.step(b, past, n, sel=sel)
+    r["scores"] = scores
+    r["rep_ties"] = ties
+    return r

@@ -18,7 +18,7 @@ import torch
 
 from oracle import infllm_oracle as O
 from paper_2402_04617_amd import infllm as F
-from tests.gpu_util import Layer, check_selection, dev, host, log, oparams
+from tests.gpu_util import Layer, check_selection, conditioned_step, dev, host, log, oparams
 from tests.test_gpu_kernels import TOL, rand_inputs
 
 pytestmark = pytest.mark.gpu
@@ -148,8 +148,9 @@ def _stream(p, q, k, v, steps, check, chunk, dtype, score_rel):
         log(f"[remap stream] step={si} past={past} n={n}")
         nu = O.partition(past, op).n_units
         got = L.capture(n, nu)
+        ridx = host(L.mem.repr_idx)
         for b in range(B):
-            r = so.step(b, past, n)
+            r = conditioned_step(so, b, past, n, ridx[b])
             for g in range(Hkv):
                 es = r["scores"][g]
                 if nu:

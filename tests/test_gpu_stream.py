@@ -13,7 +13,7 @@ import torch
 
 from oracle import infllm_oracle as O
 from paper_2402_04617_amd import infllm as F
-from tests.gpu_util import Layer, check_selection, dev, log, oparams
+from tests.gpu_util import Layer, check_selection, conditioned_step, dev, host, log, oparams
 from workload import WORKLOADS, Synth
 
 pytestmark = pytest.mark.gpu
@@ -43,8 +43,9 @@ def run_and_check(wl, seed, check_steps, q, k, v, score_rel=None, ring=None):
         log(f"[stream] {wl.name} seed={seed} step={si} past={past} n={n}")
         nu = O.partition(past, op).n_units
         got = L.capture(n, nu)
+        ridx = host(L.mem.repr_idx)
         for b in range(wl.batch):
-            r = so.step(b, past, n)
+            r = conditioned_step(so, b, past, n, ridx[b])
             for g in range(wl.n_kv_heads):
                 es = r["scores"][g]
                 if nu:

@@ -12,7 +12,7 @@ import torch
 
 from oracle import infllm_oracle as O
 from paper_2402_04617_amd import infllm as F
-from tests.gpu_util import check_selection, dev, host, log, oparams
+from tests.gpu_util import check_selection, conditioned_step, dev, host, log, oparams
 from tests.test_gpu_kernels import TOL, rand_inputs
 
 pytestmark = pytest.mark.gpu
@@ -80,8 +80,9 @@ def _run(dtype, G, Hkv, D, lI, lL, lbs, km, starts, n_q, n_steps, remap=False, m
         torch.cuda.synchronize()
         go, gl, gs, gi = (host(out).astype(np.float64), host(lse).astype(np.float64),
                           host(scores).astype(np.float64), host(idx).astype(np.int64))
+        ridx = host(mem.repr_idx)
         for b in range(B):
-            r = so.step(b, pasts[b], n_q)
+            r = conditioned_step(so, b, pasts[b], n_q, ridx[b])
             nu = r["n_units"]
             for g in range(Hkv):
                 es = r["scores"][g]
