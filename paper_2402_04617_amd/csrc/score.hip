@@ -24,49 +24,55 @@ __global__ void __launch_bounds__(kQsumThreads) qbar_kernel(const T* __restrict_
                 sm);
 }
 
-// grid (ceil(n_units/256), batch*Hkv); one unit per thread.  With the
-// positional remap the memory keys sit at distance l_L from every current token,
-// so the query sum is turned by R(l_L) before the dot products (the keys stay
-// unrotated).  In a variable-length batch sequence b scores its own unit count
-// (units past it are left alone) into rows of stride score_stride.
+// grid (ceil(n_units/256), batch*Hkv); one unit per thread.  Every thread
+// issues all D/4 16-byte loads of its unit's key sum first, so that they are in
+// flight while the block forms Qbar (the sum of the query-sum partials, turned
+// by R(l_L) under the positional remap: the memory keys sit at distance l_L from
+// every current token and stay unrotated).  In a variable-length batch sequence
+// b scores its own unit count (units past it are left alone) into rows of stride
+// score_stride.
+template <int D>
 __global__ void __launch_bounds__(256) score_kernel(const ScoreArgs a, int parts) {
+  constexpr int NC = D / 4;
   const int bg = blockIdx.y;
-  const int head_dim = a.head_dim;
+  const int n_units = a.var_on ? a.var_units[bg / a.n_kv_heads] : a.n_units;
+  const int u = blockIdx.x * 256 + threadIdx.x;
+  const bool live = u < n_units;
+  // a thread past the last unit reads unit 0 (always present) and stores nothing
+  const float4* ks = (const float4*)a.unit_ksum + (int64_t)bg * NC * a.max_units + (live ? u : 0);
+  float4 k4[NC];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) k4[c] = ks[(int64_t)c * a.max_units];
+
   const RopeArgs& rope = a.rope;
-  __shared__ float qbar[256];
-  for (int d = threadIdx.x; d < head_dim; d += 256) {
+  __shared__ float qbar[D];
+  if (threadIdx.x < D) {
     float s = 0.f;
-    for (int p = 0; p < parts; ++p) s += a.qbar_parts[((int64_t)bg * parts + p) * head_dim + d];
-    qbar[d] = s;
+    for (int p = 0; p < parts; ++p) s += a.qbar_parts[((int64_t)bg * parts + p) * D + threadIdx.x];
+    qbar[threadIdx.x] = s;
   }
   __syncthreads();
   if (rope.on) {
     const int i = threadIdx.x;
     float x0 = 0.f, x1 = 0.f, c = 1.f, sn = 0.f;
-    if (i < head_dim / 2) {
+    if (i < D / 2) {
       x0 = qbar[2 * i];
       x1 = qbar[2 * i + 1];
       c = rope.mem_cos[i];
       sn = rope.mem_sin[i];
     }
     __syncthreads();
-    if (i < head_dim / 2) {
+    if (i < D / 2) {
       qbar[2 * i] = x0 * c - x1 * sn;
       qbar[2 * i + 1] = x0 * sn + x1 * c;
     }
     __syncthreads();
   }
-  const int n_units = a.var_on ? a.var_units[bg / a.n_kv_heads] : a.n_units;
-  const int u = blockIdx.x * 256 + threadIdx.x;
-  if (u >= n_units) return;
-  const int nc = head_dim / 4;
-  const float4* ks = (const float4*)a.unit_ksum + (int64_t)bg * nc * a.max_units + u;
+  if (!live) return;
   float acc = 0.f;
-#pragma unroll 8
-  for (int c = 0; c < nc; ++c) {
-    const float4 k4 = ks[(int64_t)c * a.max_units];
-    acc += qbar[4 * c] * k4.x + qbar[4 * c + 1] * k4.y + qbar[4 * c + 2] * k4.z + qbar[4 * c + 3] * k4.w;
-  }
+#pragma unroll
+  for (int c = 0; c < NC; ++c)
+    acc += qbar[4 * c] * k4[c].x + qbar[4 * c + 1] * k4[c].y + qbar[4 * c + 2] * k4[c].z + qbar[4 * c + 3] * k4[c].w;
   a.scores[(int64_t)bg * (a.var_on ? a.score_stride : n_units) + u] = acc;
 }
 
@@ -95,7 +101,8 @@ hipError_t launch_score(const ScoreArgs& a, hipStream_t s) {
 hipError_t launch_score_given_qbar(const ScoreArgs& a, int parts, hipStream_t s) {
   if (a.n_units == 0) return hipSuccess;
   dim3 g2((a.n_units + 255) / 256, a.batch * a.n_kv_heads);  // n_units: the largest count of the batch
-  hipLaunchKernelGGL(score_kernel, g2, dim3(256), 0, s, a, parts);
+  if (a.head_dim == 128) hipLaunchKernelGGL(score_kernel<128>, g2, dim3(256), 0, s, a, parts);
+  else hipLaunchKernelGGL(score_kernel<64>, g2, dim3(256), 0, s, a, parts);
   return hipGetLastError();
 }
 
