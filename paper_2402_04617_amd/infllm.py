@@ -221,9 +221,6 @@ class LayerMemory:
     k_rot: "object" = None
 
 
-_rope_tables = {}  # keeps each Params' frequency array alive (the struct holds a raw pointer)
-
-
 def params(n_q_heads, n_kv_heads, head_dim, n_init, n_local, block_size, n_repr, topk, dtype="bf16",
            sm_scale=1.0, rope_inv_freq=None, repr_mode="tokens") -> Params:
     """Method parameters.  rope_inv_freq: None (positions pre-applied) or the D/2 rotary angular
@@ -233,8 +230,10 @@ def params(n_q_heads, n_kv_heads, head_dim, n_init, n_local, block_size, n_repr,
                INFLLM_BF16 if dtype == "bf16" else INFLLM_F32, sm_scale)
     p.repr_mode = {"tokens": INFLLM_REPR_TOKENS, "mean": INFLLM_REPR_MEAN}[repr_mode]
     if rope_inv_freq is not None:
+        if len(rope_inv_freq) != head_dim // 2:
+            raise ValueError(f"rope_inv_freq needs head_dim/2 = {head_dim // 2} entries, got {len(rope_inv_freq)}")
         table = (ctypes.c_double * len(rope_inv_freq))(*[float(x) for x in rope_inv_freq])
-        _rope_tables[ctypes.addressof(p)] = table
+        p._rope_table = table  # the struct holds a raw pointer: keep the array alive with it
         p.rope_inv_freq = ctypes.cast(table, ctypes.POINTER(ctypes.c_double))
     return p
 
