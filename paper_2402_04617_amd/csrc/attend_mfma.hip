@@ -435,20 +435,17 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
       m_run = m_new;
     }
   };
-  // P = exp2(S*c2 - m) as the bf16 P^T operand, and its fp32 row sum.
-  auto softmax_p = [&](const f32x16 (&sacc)[2], bf16x8 (&pb)[2][2]) {
+  // The keys [0, 32) half of P = exp2(S*c2 - m): bf16 operand pair and its row sum.
+  auto half0_p = [&](const f32x16& s0, bf16x8 (&ph)[2]) {
     const float neg_m = (m_run == -__builtin_inff()) ? 0.f : -m_run;
-    float psum[2] = {0.f, 0.f};
+    float ps[2] = {0.f, 0.f};
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const float p = fast_exp2(__builtin_fmaf(sacc[kb][j], c2, neg_m));
-        psum[j & 1] += p;
-        pb[kb][j >> 3][j & 7] = (__bf16)p;
-      }
+    for (int j = 0; j < 16; ++j) {
+      const float p = fast_exp2(__builtin_fmaf(s0[j], c2, neg_m));
+      ps[j & 1] += p;
+      ph[j >> 3][j & 7] = (__bf16)p;
     }
-    return psum[0] + psum[1];
+    return ps[0] + ps[1];
   };
   // O^T += V^T P^T over the four 16-key steps (V buffer vbuf); DBLK independent
   // accumulator chains, each V^T fragment two transposed 8-byte reads.
@@ -471,7 +468,10 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
   // ---- software pipeline over the part's tiles ---------------------------------
   // Tile x lives in K buffer and V buffer (x - t_begin) % 3.  Iteration t runs
   // PV(t) and QK(t+1): the matrix cores work on QK(t+1) while the vector ALUs
-  // form P(t), and on PV(t) while they take the max of tile t+1.  Loads are
+  // form the keys [32, 64) half of P(t), and on PV(t) while they take the mask
+  // and max of tile t+1 and form the keys [0, 32) half of P(t+1) with the
+  // running max (redone in the rare iteration whose tile raises the max past the
+  // lazy-rescale threshold), which balances the vector work over both phases.  Loads are
   // issued two iterations ahead, K three tiles ahead and V two tiles ahead, so
   // each buffer is refilled only after the barrier that retires its last readers:
   //   top of iteration t: wait for K(t+1), V(t) (issued two iterations ago; the
@@ -498,6 +498,9 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
   };
   auto run_finish = [&](int tile, int64_t r) -> int64_t { return uniform64(r != -2 ? r : tile_run_start(tile)); };
   f32x16 sA[2], sB[2];
+  // p0: the keys [0, 32) half of P(t), formed in the previous iteration's phase 2
+  // (or the prologue); replaced here by that half of P(t+1).
+  bf16x8 p0[2];
   auto iteration = [&](int t, f32x16 (&cur)[2], f32x16 (&nxt)[2], auto mask_next) {
     const int bc = (t - t_begin) % NBUF;
     const int bn = bc == NBUF - 1 ? 0 : bc + 1, bp = bc == 0 ? NBUF - 1 : bc - 1;
@@ -513,9 +516,9 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
     // wins the issue slots of its SIMD over a wave doing bookkeeping (measured a
     // few percent faster than uniform priority).
     __builtin_amdgcn_s_setprio(1);
-    // Phase 1: QK(t+1) on the matrix cores, P(t) on the vector ALUs.  Chunk s
+    // Phase 1: QK(t+1) on the matrix cores, half of P(t) on the vector ALUs.  Chunk s
     // issues the K fragment reads of k-step s+1, the two MFMAs of k-step s and
-    // four elements of P(t); scheduling fences keep that interleave.
+    // EPC elements of that half of P(t); scheduling fences keep that interleave.
     const float neg_m = (m_run == -__builtin_inff()) ? 0.f : -m_run;
     bf16x8 pb[2][2];
     float psum[2] = {0.f, 0.f};  // two partial row sums (shorter dependency chains)
@@ -525,7 +528,7 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
       bf16x8 a0[2], a1[2];
       a0[0] = kfrag(0, 0);
       a1[0] = kfrag(1, 0);
-      constexpr int EPC = 32 / KSTEPS;  // P elements per chunk
+      constexpr int EPC = 16 / KSTEPS;  // elements of P(t)'s keys [32, 64) half per chunk
 #pragma unroll
       for (int s = 0; s < KSTEPS; ++s) {
         if (s + 1 < KSTEPS) {
@@ -545,18 +548,21 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
         else if (s < 2 * NI) lds_load_run(ld_v + (s - NI) * 1024, vbase, off_v[s - NI]);
 #pragma unroll
         for (int i = 0; i < EPC; ++i) {
-          const int e = EPC * s + i, kb = e >> 4, j = e & 15;
-          const float p = fast_exp2(__builtin_fmaf(cur[kb][j], c2, neg_m));
+          const int j = EPC * s + i;
+          const float p = fast_exp2(__builtin_fmaf(cur[1][j], c2, neg_m));
           psum[i & 1] += p;
-          pb[kb][j >> 3][j & 7] = (__bf16)p;
+          pb[1][j >> 3][j & 7] = (__bf16)p;
         }
         __builtin_amdgcn_sched_barrier(0);
       }
     }
 
     // Phase 2: PV(t) on the matrix cores; mask and row max of tile t+1 on the
-    // vector ALUs, one 16-key group (of the 32 accumulator elements) per step.
+    // vector ALUs, one 16-key group (of the 32 accumulator elements) per step,
+    // and in the last two steps the keys [0, 32) half of P(t+1).
     float mx = -__builtin_inff();
+    bf16x8 q0[2];
+    float ps0[2] = {0.f, 0.f};
     {
       constexpr bool MASK = decltype(mask_next)::value;
       const uint32_t vaddr = vaddr_of(bc);
@@ -577,8 +583,20 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
       for (int j = 0; j < 4; ++j) {
 #pragma unroll
         for (int db = 0; db < DBLK; ++db) {
-          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[db], pb[j >> 1][j & 1], oacc[db], 0, 0, 0);
+          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[db], j < 2 ? p0[j & 1] : pb[1][j & 1], oacc[db], 0,
+                                                            0, 0);
           if (j + 1 < 4) va[db] = vfrag(db, j + 1);
+        }
+        if (j >= 2) {
+          // speculative P(t+1), keys [0, 32): 8 elements with the current max
+          // (redone below in the rare case the max of tile t+1 raises it)
+#pragma unroll
+          for (int i = 0; i < 8; ++i) {
+            const int jj = 8 * (j - 2) + i;
+            const float p = fast_exp2(__builtin_fmaf(nxt[0][jj], c2, neg_m));
+            ps0[i & 1] += p;
+            q0[jj >> 3][jj & 7] = (__bf16)p;
+          }
         }
         // 8 of the 32 scores of tile t+1: elements [8j, 8j+8)
 #pragma unroll
@@ -601,7 +619,14 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
     }
     __builtin_amdgcn_s_setprio(0);
     l_run += psum[0] + psum[1];
-    update_max(mx);
+    p0[0] = q0[0];
+    p0[1] = q0[1];
+    float l_add = ps0[0] + ps0[1];
+    if (__ballot(mx > m_run + 8.f)) {
+      update_max(mx);
+      l_add = half0_p(nxt[0], p0);  // redo the half with the raised max
+    }
+    l_run += l_add;
     run_v = run_k;
     run_k = run_finish(t + 4, run_next);
   };
@@ -636,6 +661,7 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
           if (32 * kb + 8 * (j >> 2) + (j & 3) < lo) sA[kb][j] = -__builtin_inff();
     }
     update_max(tile_max(sA));
+    l_run += half0_p(sA[0], p0);
 
     int t = t_begin;
     // next tile unmasked
@@ -661,7 +687,19 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
     // drain: P and PV of the last tile (then no load is left in flight)
     publish_barrier<0>();
     bf16x8 pb[2][2];
-    l_run += softmax_p(sA, pb);
+    {
+      const float neg_m = (m_run == -__builtin_inff()) ? 0.f : -m_run;
+      float ps[2] = {0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < 16; ++j) {
+        const float p = fast_exp2(__builtin_fmaf(sA[1][j], c2, neg_m));
+        ps[j & 1] += p;
+        pb[1][j >> 3][j & 7] = (__bf16)p;
+      }
+      l_run += ps[0] + ps[1];
+      pb[0][0] = p0[0];
+      pb[0][1] = p0[1];
+    }
     pv((t - t_begin) % NBUF, pb);
   }
 
