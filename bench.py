@@ -40,9 +40,9 @@ PEAK_HBM_GBS = 8000.0
 # --copy-calibration 1024`.  Valid only for the attention source it was taken on (sha256 below);
 # reported as null once that file changes.
 ATTN_SRC = os.path.join(ROOT, "paper_2402_04617_amd", "csrc", "attend_mfma.hip")
-ATTN_TRAFFIC = {"src_sha256": "213d288af4fcf63c435941c98de2af350faf32dbcf82cc8a220b524cdc6e2a47",
-                "fetch_kib": 20000.25, "write_kib": 16896.0,  # per attention dispatch (768 dispatches)
-                "copy_fetch": 524300.21 / 1048576.0,  # FETCH_SIZE KiB per KiB read by the copy
+ATTN_TRAFFIC = {"src_sha256": "ca0b21819ced1ced360e29015d9124ae273f0ec880f50dc0dfa4e3137856ece0",
+                "fetch_kib": 20024.35, "write_kib": 16896.0,  # per attention dispatch (768 dispatches)
+                "copy_fetch": 524300.0 / 1048576.0,  # FETCH_SIZE KiB per KiB read by the copy
                 "copy_write": 1048576.0 / 1048576.0}  # WRITE_SIZE KiB per KiB written by the copy
 
 
