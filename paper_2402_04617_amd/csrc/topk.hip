@@ -147,7 +147,8 @@ __device__ __forceinline__ void tiled_scan(const bool (&pred)[PER], int (&rank)[
 // built with one atomic per wave where the wave's live digits agree (typical of
 // the leading digits), double-buffered histograms (two barriers per pass), and
 // a final pass whose index-order ranks come from one tiled ballot scan (two
-// when only some keys equal to T are kept).
+// when only some keys equal to T are kept).  The passes stop early once every
+// key sharing the resolved prefix is kept.
 template <int PER>
 __device__ void radix_select_reg(const float* __restrict__ s, int n, int k_eff, int32_t* __restrict__ out) {
   __shared__ uint32_t hist[2][256];
@@ -204,6 +205,9 @@ __device__ void radix_select_reg(const float* __restrict__ s, int n, int k_eff, 
     mask |= 255u << shift;
     remaining = (int)sh_remaining;
     eq_total = sh_eq_total;
+    // Every key with this prefix is kept: the prefix (low bits zero) is already a
+    // threshold that keeps exactly k_eff keys, so the remaining passes are skipped.
+    if ((uint32_t)remaining == eq_total) break;
   }
   const uint32_t thr = prefix;
   // Final pass: ranks in index order (tile j = indices [j*kThreads, (j+1)*kThreads))
