@@ -228,6 +228,30 @@ infllm_status infllm_lse_merge(const infllm_params* p, int32_t batch, int32_t n_
                                const void* workspace, size_t workspace_bytes, void* out,
                                int64_t out_head_stride, float* lse, void* stream);
 
+/* Attention mass of the looked-up units and the frequency score of the cache
+ * policy (Section 3.2, "Cache Management", and the appendix on the cache
+ * management strategy: s_b = s_b * d + sum_{j<l_X} sum_{i in b} attention score).
+ * For the step at past_len with current tokens X (n_q of them, queries q as given
+ * to the attention) and its lookup idx [batch][Hkv][k] (as infllm_select_topk
+ * writes it: distinct entries, -1 padding):
+ *   mass [batch][Hkv][k] float32 (required when k > 0): for slot j with unit
+ *        b = idx[..][j] in [0, n_units(past_len)), the softmax probability the step's
+ *        attention gave b's l_bs keys, summed over the n_q queries and the G query
+ *        heads of the kv group: sum_h sum_i sum_{t in b} exp(z - lse) with z the
+ *        attention logit (under the positional remap the query turned by R(l_L)),
+ *        so it lies in [0, G*n_q]; 0 for a -1 or out-of-range entry;
+ *   lse  [batch][Hq][n_q] float32: the step's natural-log normaliser, as
+ *        infllm_chunk_attend / infllm_step write it (required when n_q, k > 0);
+ *   freq [batch][Hkv][max_units] float32, nullable, read and written: the
+ *        frequency score of every built unit b < n_units(past_len) becomes
+ *        freq * decay + mass(b), with mass 0 for units not looked up (all units
+ *        stay resident here, so all of them decay).  Zero it before the first step.
+ * decay: finite, >= 0 (the paper uses 0.1).  Run it after the step's attention on
+ * the same stream.  E_UNSUPPORTED for k > 1024. */
+infllm_status infllm_unit_mass(const infllm_params* p, const infllm_memory* m, const void* q,
+                               int64_t q_head_stride, int32_t n_q, int64_t past_len, const int32_t* idx, int32_t k,
+                               const float* lse, float decay, float* mass, float* freq, void* stream);
+
 /* One whole step of the layer (Sections 3.1-3.2) for the current tokens X at
  * positions [past_len, past_len + n_q), in this order on `stream`:
  *   1. unit construction for units [units_built, n_units(past_len)), the units

@@ -230,6 +230,43 @@ def context_positions(past_len: int, sel: np.ndarray, p: Params) -> np.ndarray:
     return np.concatenate(pos).astype(np.int64)
 
 
+def attention_logits(q_chunk: np.ndarray, k: np.ndarray, past_len: int, sel_g: np.ndarray, p: Params,
+                     g: int) -> Tuple[np.ndarray, np.ndarray]:
+    """Logits of kv group g's G query heads over Concat(C, X) (Section 3.1).
+
+    z[hh][i][t] = sm_scale * q . k for key t of C (I, the looked-up units in the
+    order of sel_g, L) followed by the current tokens X, -inf where X is causally
+    hidden (query i sees X positions up to its own).  Under the positional remap
+    (Section 3.2) I and the units are met by the query turned by R(l_L) with the
+    key unrotated, L and X at their true positions.
+    Returns z float64 [G][l_X][|C| + l_X] and the keys' positions [|C| + l_X].
+    """
+    nq = q_chunk.shape[1]
+    G = p.group
+    causal = np.tril(np.ones((nq, nq), dtype=bool))
+    remap = p.rope_inv_freq is not None
+    part = partition(past_len, p)
+    pos = context_positions(past_len, sel_g, p)
+    kc = np.asarray(k[g, pos], dtype=np.float64)
+    kx = np.asarray(k[g, past_len: past_len + nq], dtype=np.float64)
+    n_mem = pos.shape[0] - (past_len - part.local_begin)
+    if remap:
+        kc[n_mem:] = rotate_keys(kc[n_mem:], pos[n_mem:], p)
+        kx = rotate_keys(kx, np.arange(past_len, past_len + nq), p)
+    z = np.empty((G, nq, pos.shape[0] + nq))
+    for hh in range(G):
+        qh = np.asarray(q_chunk[g * G + hh], dtype=np.float64)
+        if remap:
+            q_mem = rotate(qh, float(p.n_local), p.rope_inv_freq)
+            q_loc = rotate(qh, np.arange(past_len, past_len + nq), p.rope_inv_freq)
+            zc = np.concatenate([q_mem @ kc[:n_mem].T, q_loc @ kc[n_mem:].T], axis=1)
+            zx = q_loc @ kx.T
+        else:
+            zc, zx = qh @ kc.T, qh @ kx.T
+        z[hh] = np.concatenate([p.sm_scale * zc, np.where(causal, p.sm_scale * zx, -np.inf)], axis=1)
+    return z, np.concatenate([pos, np.arange(past_len, past_len + nq)])
+
+
 def attend(q_chunk: np.ndarray, k: np.ndarray, v: np.ndarray, past_len: int,
            sel: np.ndarray, p: Params) -> Tuple[np.ndarray, np.ndarray]:
     """O = Attn[Q X, Concat(C_k, K X), Concat(C_v, V X)] (Section 3.1).
@@ -244,37 +281,53 @@ def attend(q_chunk: np.ndarray, k: np.ndarray, v: np.ndarray, past_len: int,
     G = p.group
     O = np.empty((Hq, nq, D))
     lse = np.empty((Hq, nq))
-    causal = np.tril(np.ones((nq, nq), dtype=bool))
-    remap = p.rope_inv_freq is not None
-    part = partition(past_len, p)
     for g in range(p.n_kv_heads):
-        pos = context_positions(past_len, sel[g], p)
-        kc = np.asarray(k[g, pos], dtype=np.float64)
-        vc = np.asarray(v[g, pos], dtype=np.float64)
-        kx = np.asarray(k[g, past_len: past_len + nq], dtype=np.float64)
-        vx = np.asarray(v[g, past_len: past_len + nq], dtype=np.float64)
-        if remap:
-            # I and the units (everything before L in C) at distance l_L; L and X
-            # at their true positions.
-            n_mem = pos.shape[0] - (past_len - part.local_begin)
-            kc[n_mem:] = rotate_keys(kc[n_mem:], pos[n_mem:], p)
-            kx = rotate_keys(kx, np.arange(past_len, past_len + nq), p)
-        for h in range(g * G, (g + 1) * G):
-            qh = np.asarray(q_chunk[h], dtype=np.float64)
-            if remap:
-                q_mem = rotate(qh, float(p.n_local), p.rope_inv_freq)
-                q_loc = rotate(qh, np.arange(past_len, past_len + nq), p.rope_inv_freq)
-                zc = np.concatenate([q_mem @ kc[:n_mem].T, q_loc @ kc[n_mem:].T], axis=1)
-                zx = q_loc @ kx.T
-            else:
-                zc, zx = qh @ kc.T, qh @ kx.T
-            z = np.concatenate([p.sm_scale * zc, np.where(causal, p.sm_scale * zx, -np.inf)], axis=1)
-            zmax = z.max(axis=1, keepdims=True)
-            w = np.exp(z - zmax)
+        z, keys = attention_logits(q_chunk, k, past_len, sel[g], p, g)
+        vk = np.asarray(v[g, keys], dtype=np.float64)
+        for hh in range(G):
+            zmax = z[hh].max(axis=1, keepdims=True)
+            w = np.exp(z[hh] - zmax)
             s = w.sum(axis=1, keepdims=True)
-            O[h] = (w / s) @ np.concatenate([vc, vx], axis=0)
-            lse[h] = (zmax + np.log(s))[:, 0]
+            O[g * G + hh] = (w / s) @ vk
+            lse[g * G + hh] = (zmax + np.log(s))[:, 0]
     return O, lse
+
+
+def unit_mass(q_chunk: np.ndarray, k: np.ndarray, past_len: int, sel: np.ndarray, p: Params) -> np.ndarray:
+    """Attention mass of each looked-up unit (Section 3.2, "Cache Management"; the
+    appendix's frequency score adds it up).
+
+    The attention score of a key for a query is its softmax probability in the
+    step's attention (the logits and key set of `attend`); a unit's mass sums it
+    over the unit's l_bs keys, the chunk's queries and the G query heads of the
+    kv group.  sel: [Hkv][k] unit ids (-1 = none, mass 0).  Returns float64 [Hkv][k].
+    """
+    n_units = partition(past_len, p).n_units
+    mass = np.zeros(np.shape(sel), dtype=np.float64)
+    for g in range(p.n_kv_heads):
+        z, keys = attention_logits(q_chunk, k, past_len, sel[g], p, g)
+        prob = np.exp(z - z.max(axis=2, keepdims=True))
+        prob /= prob.sum(axis=2, keepdims=True)
+        for j, b in enumerate(sel[g]):
+            if 0 <= b < n_units:
+                s0 = unit_start(int(b), p)
+                in_unit = (keys >= s0) & (keys < s0 + p.block_size)
+                mass[g, j] = prob[:, :, in_unit].sum()
+    return mass
+
+
+def frequency_update(freq: np.ndarray, sel: np.ndarray, mass: np.ndarray, n_units: int,
+                     decay: float) -> np.ndarray:
+    """The frequency score after one step (appendix on cache management):
+    s_b <- s_b * d + (mass of b this step), for every built unit b < n_units, the
+    mass being 0 for a unit that was not looked up.  freq: [Hkv][>= n_units]."""
+    f = np.array(freq, dtype=np.float64, copy=True)
+    f[:, :n_units] *= decay
+    for g in range(f.shape[0]):
+        for j, b in enumerate(sel[g]):
+            if 0 <= b < n_units:
+                f[g, b] += mass[g, j]
+    return f
 
 
 def lse_merge(outs: Sequence[np.ndarray], lses: Sequence[np.ndarray]) -> Tuple[np.ndarray, np.ndarray]:

@@ -18,7 +18,7 @@ LIB = os.path.join(PKG, "libinfllm.so")
 PEAKS = os.path.join(PKG, "infllm_peaks")
 
 SOURCES = ["abi.cpp", "append.hip", "build_units.hip", "score.hip", "topk.hip", "attend_mfma.hip",
-           "attend.hip", "attend_decode.hip", "merge.hip"]
+           "attend.hip", "attend_decode.hip", "merge.hip", "mass.hip"]
 
 # Packed fp32 ops are disabled for all device code (the host pass warns that it
 # does not know the feature; that is harmless).

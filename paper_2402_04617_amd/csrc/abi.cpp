@@ -525,6 +525,56 @@ infllm_status infllm_chunk_attend(const infllm_params* p, const infllm_memory* m
   return launch_status(launch_merge(ma, (hipStream_t)stream));
 }
 
+infllm_status infllm_unit_mass(const infllm_params* p, const infllm_memory* m, const void* q,
+                               int64_t q_head_stride, int32_t n_q, int64_t past_len, const int32_t* idx, int32_t k,
+                               const float* lse, float decay, float* mass, float* freq, void* stream) {
+  infllm_status st;
+  if ((st = check_params(p)) != INFLLM_OK) return st;
+  if ((st = check_store(p, m)) != INFLLM_OK) return st;
+  if (n_q < 0 || past_len < 0 || k < 0) return INFLLM_E_SHAPE;
+  if (!std::isfinite(decay) || decay < 0.f) return INFLLM_E_SHAPE;
+  if (past_len + n_q > m->capacity) return INFLLM_E_RANGE;
+  if (k > kMassMaxK) return INFLLM_E_UNSUPPORTED;
+  if (p->dtype == INFLLM_BF16 && (uint64_t)m->capacity * (uint64_t)p->head_dim * 2u > 0xFFFFFFFFull)
+    return INFLLM_E_UNSUPPORTED;
+  const Part part = partition(p, past_len);
+  if (freq != nullptr && part.n_units > m->max_units) return INFLLM_E_RANGE;
+  if (k > 0) {
+    if (idx == nullptr || mass == nullptr) return INFLLM_E_NULL;
+    if (n_q > 0) {
+      if (lse == nullptr) return INFLLM_E_NULL;
+      if ((st = check_rows(p, q, q_head_stride, n_q)) != INFLLM_OK) return st;
+    }
+  }
+  if (k == 0 && (freq == nullptr || part.n_units == 0)) return INFLLM_OK;
+  MassArgs a;
+  std::memset(&a, 0, sizeof(a));
+  a.rows = m->batch * p->n_kv_heads;
+  a.n_q_heads = p->n_q_heads;
+  a.n_kv_heads = p->n_kv_heads;
+  a.head_dim = p->head_dim;
+  a.n_q = n_q;
+  a.k = k;
+  a.n_units = part.n_units;
+  a.max_units = m->max_units;
+  a.block_size = p->block_size;
+  a.n_init = p->n_init;
+  a.capacity = m->capacity;
+  a.q_head_stride = q_head_stride;
+  a.sm_scale = p->sm_scale;
+  a.decay = decay;
+  a.q = q;
+  a.k_store = m->k;
+  a.idx = idx;
+  a.lse = lse;
+  a.mass = mass;
+  a.freq = part.n_units > 0 ? freq : nullptr;
+  a.rope = rope_args(p);
+  a.bf16 = p->dtype == INFLLM_BF16;
+  if ((st = check_device()) != INFLLM_OK) return st;
+  return launch_status(launch_unit_mass(a, (hipStream_t)stream));
+}
+
 infllm_status infllm_step(const infllm_params* p, const infllm_memory* m, const void* q, int64_t q_head_stride,
                           const void* k, const void* v, int64_t kv_head_stride, int32_t n_q, int64_t past_len,
                           int32_t units_built, float* scores, int32_t* idx, void* out, int64_t out_head_stride,

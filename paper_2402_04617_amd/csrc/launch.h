@@ -201,4 +201,24 @@ struct MergeArgs {
 };
 hipError_t launch_merge(const MergeArgs& a, hipStream_t s);
 
+// Attention mass of the looked-up units and the frequency-score update.
+constexpr int kMassMaxK = 1024;  // most lookup slots per row
+struct MassArgs {
+  int rows;  // batch * n_kv_heads
+  int n_q_heads, n_kv_heads, head_dim;
+  int n_q, k, n_units, max_units, block_size;
+  int64_t n_init;  // l_I: first position of unit 0
+  int64_t capacity, q_head_stride;
+  float sm_scale, decay;
+  const void* q;
+  const void* k_store;
+  const int32_t* idx;  // [rows][k]
+  const float* lse;    // [batch][Hq][n_q] natural log
+  float* mass;         // [rows][k]
+  float* freq;         // [rows][max_units] or null
+  RopeArgs rope;
+  bool bf16;
+};
+hipError_t launch_unit_mass(const MassArgs& a, hipStream_t s);
+
 }  // namespace infllm

@@ -25,7 +25,7 @@ STATUS = {0: "INFLLM_OK", 1: "INFLLM_E_NULL", 2: "INFLLM_E_SHAPE", 3: "INFLLM_E_
 
 EXPORTS = ["infllm_partition", "infllm_workspace_bytes", "infllm_append", "infllm_build_units",
            "infllm_score_units", "infllm_select_topk", "infllm_chunk_attend", "infllm_attend_partial",
-           "infllm_lse_merge", "infllm_step", "infllm_step_varlen", "infllm_status_string"]
+           "infllm_lse_merge", "infllm_step", "infllm_step_varlen", "infllm_unit_mass", "infllm_status_string"]
 
 
 class InfllmError(RuntimeError):
@@ -86,6 +86,7 @@ def lib() -> ctypes.CDLL:
         "infllm_step": [P, M, vp, i64, vp, vp, i64, i32, i64, i32, vp, vp, vp, i64, vp, vp, sz, vp],
         "infllm_step_varlen": [P, M, vp, i64, vp, vp, i64, i32, ctypes.POINTER(i64), ctypes.POINTER(i32), vp, vp,
                                vp, i64, vp, vp, sz, vp],
+        "infllm_unit_mass": [P, M, vp, i64, i32, i64, vp, i32, vp, ctypes.c_float, vp, vp, vp],
     }
     for name, args in sig.items():
         f = getattr(L, name)
@@ -191,6 +192,12 @@ def infllm_step(p, m, q, q_head_stride, k, v, kv_head_stride, n_q, past_len, uni
         ctypes.byref(p), ctypes.byref(m), _ptr(q), q_head_stride, _ptr(k), _ptr(v), kv_head_stride, n_q, past_len,
         units_built, _ptr(scores), _ptr(idx), _ptr(out), out_head_stride, _ptr(lse), _ptr(workspace), wb,
         _stream(stream)))
+
+
+def infllm_unit_mass(p, m, q, q_head_stride, n_q, past_len, idx, k, lse, decay, mass, freq=None, stream=None):
+    _check("infllm_unit_mass", lib().infllm_unit_mass(
+        ctypes.byref(p), ctypes.byref(m), _ptr(q), q_head_stride, n_q, past_len, _ptr(idx), k, _ptr(lse),
+        float(decay), _ptr(mass), _ptr(freq), _stream(stream)))
 
 
 def infllm_step_varlen(p, m, q, q_head_stride, k, v, kv_head_stride, n_q, past_lens, units_built, scores, idx, out,

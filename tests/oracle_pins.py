@@ -598,6 +598,81 @@ def check_hand_worked_example():
         assert np.allclose(r["lse"], st["lse"], rtol=1e-13, atol=1e-13)
 
 
+def check_unit_mass_uniform_closed_form():
+    """q = 0 makes every logit 0: query i spreads its attention evenly over its |T_i| keys, so a
+    looked-up unit's mass is G * sum_i l_bs / |T_i| with |T_i| = l_I + k_eff*l_bs + |L| + i + 1."""
+    rng = np.random.default_rng(61)
+    p = _params(n_q_heads=6, n_kv_heads=2, head_dim=4, n_init=3, n_local=7, block_size=5, topk=3)
+    S, G = 80, 3
+    _, k, v = _rand_qkv(rng, p, S)
+    for past, nq in ((40, 5), (63, 1), (71, 9)):
+        q = np.zeros((p.n_q_heads, nq, p.head_dim))
+        part = O.partition(past, p)
+        sel = np.stack([np.sort(rng.choice(part.n_units, 3, replace=False)) for _ in range(2)])
+        sel[1, 2] = -1  # an empty slot: mass 0, and one unit fewer in the key set
+        m = O.unit_mass(q, k[0], past, sel, p)
+        for g in range(2):
+            k_eff = int((sel[g] >= 0).sum())
+            n_t = part.n_init + k_eff * p.block_size + (past - part.local_begin) + np.arange(1, nq + 1)
+            want = G * float(np.sum(p.block_size / n_t))
+            for j in range(3):
+                assert math.isclose(m[g, j], want if sel[g, j] >= 0 else 0.0, rel_tol=1e-12), (past, g, j)
+
+
+def check_unit_mass_bruteforce():
+    """Softmax probabilities formed key by key (explicit attended-position list, per-key logits,
+    math.exp), summed over each looked-up unit, every query and every head of the group; with and
+    without the positional remap (complex-number rotations, memory keys at distance l_L)."""
+    rng = np.random.default_rng(62)
+    for remap in (False, True):
+        p = _rope_params(seed=63, n_q_heads=4, n_kv_heads=2, head_dim=6, n_init=2, n_local=5,
+                         block_size=3, n_repr=1, topk=2, sm_scale=0.7)
+        if not remap:
+            import dataclasses
+            p = dataclasses.replace(p, rope_inv_freq=None)
+        f = None if p.rope_inv_freq is None else np.array(p.rope_inv_freq)
+        S, G = 50, 2
+        q, k, _ = _rand_qkv(rng, p, S)
+        for past, nq in ((22, 4), (38, 1)):
+            part = O.partition(past, p)
+            sel = np.stack([np.sort(rng.choice(part.n_units, 2, replace=False)) for _ in range(2)])
+            m = O.unit_mass(q[0, :, past:past + nq], k[0], past, sel, p)
+            for g in range(2):
+                units = {int(b): set(range(p.n_init + int(b) * p.block_size,
+                                           p.n_init + (int(b) + 1) * p.block_size)) for b in sel[g]}
+                mem = list(range(part.n_init)) + sorted(t for u in units.values() for t in u)
+                want = {b: 0.0 for b in units}
+                for h in range(g * G, (g + 1) * G):
+                    for i in range(nq):
+                        P = past + i
+                        keys = [(t, P - p.n_local if f is not None else t) for t in mem] + \
+                               [(t, t) for t in range(part.local_begin, P + 1)]
+                        qr = q[0, h, P] if f is None else _rot_complex(q[0, h, P], P, f)
+                        z = [p.sm_scale * float(qr @ (k[0, g, t] if f is None else _rot_complex(k[0, g, t], e, f)))
+                             for t, e in keys]
+                        zm = max(z)
+                        tot = sum(math.exp(x - zm) for x in z)
+                        for (t, _), x in zip(keys, z):
+                            for b, pos in units.items():
+                                if t in pos and t < past:
+                                    want[b] += math.exp(x - zm) / tot
+                for j, b in enumerate(sel[g]):
+                    assert math.isclose(m[g, j], want[int(b)], rel_tol=1e-11, abs_tol=1e-14), (remap, past, g, j)
+
+
+def check_frequency_update_recurrence():
+    """The decayed sum in closed form: a unit looked up every step with mass c reaches
+    c (1 - d^n) / (1 - d) after n steps; one never looked up keeps s_0 d^n; units not yet
+    built stay untouched."""
+    d, c, n = 0.1, 2.5, 7
+    freq = np.array([[4.0, 1.0, 9.0]])
+    for _ in range(n):
+        freq = O.frequency_update(freq, np.array([[0, -1]]), np.array([[c, 0.0]]), 2, d)
+    assert math.isclose(freq[0, 0], 4.0 * d ** n + c * (1 - d ** n) / (1 - d), rel_tol=1e-13)
+    assert math.isclose(freq[0, 1], 1.0 * d ** n, rel_tol=1e-13)
+    assert freq[0, 2] == 9.0
+
+
 ALL_CHECKS = [
     check_partition,
     check_repr_scores_bruteforce,
@@ -622,4 +697,7 @@ ALL_CHECKS = [
     check_remap_repr_scores_bruteforce,
     check_remap_reduces_to_rotary_attention,
     check_mean_repr_mode,
+    check_unit_mass_uniform_closed_form,
+    check_unit_mass_bruteforce,
+    check_frequency_update_recurrence,
 ]

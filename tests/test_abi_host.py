@@ -278,6 +278,36 @@ def test_mean_repr_validation(L):
     assert L.infllm_build_units(ctypes.byref(pt), bm, 0, 1, 4352, None, None) == 1
 
 
+def test_unit_mass_validation(L):
+    p, m = P(), mem()
+    f = L.infllm_unit_mass
+    bp, bm = ctypes.byref(p), ctypes.byref(m)
+    past = 1 << 16
+    ok = (bp, bm, FAKE, 512 * 128, 512, past, FAKE, 32, FAKE, 0.1, FAKE, FAKE, None)
+
+    def call(**kw):
+        a = list(ok)
+        names = ["p", "m", "q", "qs", "n_q", "past", "idx", "k", "lse", "decay", "mass", "freq", "stream"]
+        for key, val in kw.items():
+            a[names.index(key)] = val
+        return f(*a)
+    assert call(p=None) == 1
+    assert call(m=None) == 1
+    assert call(idx=None) == 1
+    assert call(mass=None) == 1
+    assert call(lse=None) == 1
+    assert call(q=None) == 1
+    assert call(qs=100) == 2                   # head stride < n_q*D
+    assert call(n_q=-1) == 2
+    assert call(k=-1) == 2
+    assert call(decay=-0.5) == 2
+    assert call(decay=float("nan")) == 2
+    assert call(past=(1 << 17) - 100) == 3     # past + n_q beyond capacity
+    assert call(k=1025) == 4                   # more lookup slots than the kernel stages
+    few = mem(max_units=10)
+    assert call(m=ctypes.byref(few)) == 3      # freq rows shorter than the built units
+
+
 @pytest.mark.skipif(os.path.exists("/dev/kfd") and os.access("/dev/kfd", os.R_OK),
                     reason="a GPU may be present; valid arguments would launch on fake pointers")
 def test_valid_arguments_without_gpu_report_device_error(L):

@@ -1,0 +1,122 @@
+"""Attention mass of the looked-up units and the decayed frequency score (GPU).
+
+Each step of a stream runs through infllm_step, then infllm_unit_mass takes the
+step's lookup and lse; the masses and the running frequency scores are compared
+with the oracle's unit_mass / frequency_update on the same inputs (decay 0.1,
+the paper's setting).  Where a lookup legitimately differs inside a near-tie,
+the oracle takes the device's valid set for that kv head (the conditioned
+oracle), since that set is what the attention used.
+
+Tolerance: a probability exp(z - lse) inherits the error of z - lse, and the
+attention's lse is held to 1e-3 (bf16), 1e-2 (bf16 with the remap, whose rotated
+queries and keys are rounded to bf16) and 1e-4 (float32) of the oracle's; the
+mass is compared to that relative bound, doubled, plus 1e-6 * G * n_q.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import infllm_oracle as O
+from paper_2402_04617_amd import infllm as F
+from tests.gpu_util import Layer, check_selection, conditioned_step, dev, host, log, oparams
+from tests.test_gpu_kernels import rand_inputs
+
+pytestmark = pytest.mark.gpu
+
+DECAY = 0.1
+
+
+def _rel_tol(p):
+    if p.dtype == F.INFLLM_F32:
+        return 2e-4
+    return 2e-2 if p.remap else 2e-3
+
+
+def _run(p, dtype, q, k, v, steps, chunk):
+    op = oparams(p)
+    B, G, Hkv = q.shape[0], p.n_q_heads // p.n_kv_heads, p.n_kv_heads
+    L = Layer(p, B, q.shape[2], chunk=chunk)
+    qd, kd, vd = dev(q, dtype), dev(k, dtype), dev(v, dtype)
+    so = O.StreamOracle(q, k, v, op)
+    kk = max(1, p.topk)
+    mass = torch.zeros((B, Hkv, kk), dtype=torch.float32, device="cuda")
+    freq = torch.zeros((B, Hkv, L.max_units), dtype=torch.float32, device="cuda")
+    ofreq = np.zeros((B, Hkv, L.max_units))
+    esz = 2 if dtype == "bf16" else 4
+    S, D = q.shape[2], q.shape[3]
+    rel = _rel_tol(p)
+    n_checked = 0
+    for si, (past, n) in enumerate(steps):
+        L.step(qd, kd, vd, past, n)
+        F.infllm_unit_mass(p, L.mem.struct, qd.data_ptr() + past * D * esz, S * D, n, past, L.idx, p.topk,
+                           L.lse, DECAY, mass, freq)
+        log(f"[mass] step={si} past={past} n={n}")
+        nu = O.partition(past, op).n_units
+        got = L.capture(n, nu)
+        gm, gf = host(mass), host(freq)
+        ridx = host(L.mem.repr_idx)
+        for b in range(B):
+            r = conditioned_step(so, b, past, n, ridx[b])
+            sel = np.array(r["idx"])
+            for g in range(Hkv):
+                if not check_selection(got["idx"][b, g], r["idx"][g], r["scores"][g], p.topk):
+                    sel[g] = got["idx"][b, g]  # a valid set inside the tie band: what the attention used
+            om = O.unit_mass(q[b, :, past:past + n], k[b], past, sel, op)
+            ofreq[b] = O.frequency_update(ofreq[b], sel, om, nu, DECAY)
+            floor = 1e-6 * G * n
+            for g in range(Hkv):
+                if p.topk:
+                    err = np.abs(gm[b, g, :p.topk] - om[g])
+                    assert np.all(err <= rel * om[g] + floor), (si, b, g, gm[b, g], om[g])
+                    n_checked += int((sel[g] >= 0).sum())
+                if nu:
+                    ferr = np.abs(gf[b, g, :nu] - ofreq[b, g, :nu])
+                    assert np.all(ferr <= rel * np.abs(ofreq[b, g, :nu]) + floor), (si, b, g)
+                assert np.all(gf[b, g, nu:] == 0.0), (si, b, g)  # units not built yet are untouched
+    assert n_checked > 0
+
+
+def _steps(S, chunk):
+    return [(s, min(chunk, S - s)) for s in range(0, S, chunk)]
+
+
+# (dtype, G, Hkv, D, l_I, l_L, l_bs, r_k, k_m, S, chunk, remap)
+CASES = [
+    ("bf16", 4, 2, 128, 5, 300, 24, 4, 7, 1500, 128, False),
+    ("bf16", 4, 2, 128, 5, 300, 24, 4, 7, 1500, 128, True),
+    ("bf16", 2, 1, 64, 0, 256, 256, 2, 3, 1800, 300, False),
+    ("bf16", 8, 1, 128, 64, 512, 64, 4, 8, 2600, 256, False),
+    ("f32", 2, 2, 64, 3, 200, 40, 2, 5, 1100, 100, False),
+    ("f32", 2, 1, 64, 16, 256, 32, 4, 4, 1000, 64, True),
+]
+
+
+@pytest.mark.parametrize("case", CASES)
+def test_unit_mass_stream(case):
+    dtype, G, Hkv, D, n_init, n_local, lbs, nrep, topk, S, chunk, remap = case
+    rng = np.random.default_rng(sum(case[1:11]))
+    freqs = F.rope_frequencies(D, 10000.0) if remap else None
+    p = F.params(G * Hkv, Hkv, D, n_init, n_local, lbs, nrep, topk, dtype, rope_inv_freq=freqs)
+    q, k, v = rand_inputs(rng, G * Hkv, Hkv, S, D, dtype)
+    _run(p, dtype, q, k, v, _steps(S, chunk), chunk)
+
+
+def test_unit_mass_decode():
+    # prefill in chunks, then token-by-token decode of two sequences
+    rng = np.random.default_rng(8)
+    G, Hkv, D, S0, n_dec = 4, 2, 128, 1100, 12
+    p = F.params(G * Hkv, Hkv, D, 4, 256, 32, 4, 6, "bf16")
+    q, k, v = rand_inputs(rng, G * Hkv, Hkv, S0 + n_dec, D, "bf16", B=2)
+    steps = _steps(S0, 220) + [(S0 + i, 1) for i in range(n_dec)]
+    _run(p, "bf16", q, k, v, steps, 220)
+
+
+def test_unit_mass_every_unit_looked_up():
+    # l_I = 0, a one-token local window and k_m above the unit count: every built unit is
+    # looked up each step (most of the attention lands on units) and the padded slots are 0
+    rng = np.random.default_rng(12)
+    G, Hkv, D = 2, 1, 64
+    p = F.params(G * Hkv, Hkv, D, 0, 1, 16, 2, 64, "bf16")
+    S, chunk = 16 * 40 + 1 + 32, 32
+    q, k, v = rand_inputs(rng, G * Hkv, Hkv, S, D, "bf16")
+    _run(p, "bf16", q, k, v, _steps(S, chunk), chunk)

@@ -20,7 +20,8 @@ def test_pin(check):
 # ------------------------------------------------------------------ mutants
 _orig = {name: getattr(O, name) for name in
          ("partition", "representative_scores", "top_indices", "unit_relevance", "attend",
-          "lse_merge", "context_positions", "select_units", "unit_start", "rotate", "mean_relevance", "round_bf16")}
+          "lse_merge", "context_positions", "select_units", "unit_start", "rotate", "mean_relevance", "round_bf16",
+          "unit_mass", "frequency_update")}
 
 
 def _mut_partition_drop_remainder(past_len, p):
@@ -220,6 +221,66 @@ def _mut_select_top_km_minus_1(sim, p, k=None):
     return out
 
 
+# ---- attention mass and frequency score slips
+def _mut_mass_unnormalised(q_chunk, k, past_len, sel, p):
+    # exp(z - max) summed without dividing by the row's total
+    n_units = O.partition(past_len, p).n_units
+    mass = np.zeros(np.shape(sel))
+    for g in range(p.n_kv_heads):
+        z, keys = O.attention_logits(q_chunk, k, past_len, sel[g], p, g)
+        w = np.exp(z - z.max(axis=2, keepdims=True))
+        for j, b in enumerate(sel[g]):
+            if 0 <= b < n_units:
+                s0 = O.unit_start(int(b), p)
+                mass[g, j] = w[:, :, (keys >= s0) & (keys < s0 + p.block_size)].sum()
+    return mass
+
+
+def _mut_mass_first_head_only(q_chunk, k, past_len, sel, p):
+    G = p.group
+    return _orig["unit_mass"](q_chunk, k, past_len, sel, p) / G
+
+
+def _mut_mass_span_short(q_chunk, k, past_len, sel, p):
+    # the unit's last key left out
+    n_units = O.partition(past_len, p).n_units
+    mass = np.zeros(np.shape(sel))
+    for g in range(p.n_kv_heads):
+        z, keys = O.attention_logits(q_chunk, k, past_len, sel[g], p, g)
+        prob = np.exp(z - z.max(axis=2, keepdims=True))
+        prob /= prob.sum(axis=2, keepdims=True)
+        for j, b in enumerate(sel[g]):
+            if 0 <= b < n_units:
+                s0 = O.unit_start(int(b), p)
+                mass[g, j] = prob[:, :, (keys >= s0) & (keys < s0 + p.block_size - 1)].sum()
+    return mass
+
+
+def _mut_mass_no_remap(q_chunk, k, past_len, sel, p):
+    import dataclasses
+    return _orig["unit_mass"](q_chunk, k, past_len, sel, dataclasses.replace(p, rope_inv_freq=None))
+
+
+def _mut_freq_add_then_decay(freq, sel, mass, n_units, decay):
+    f = np.array(freq, dtype=np.float64, copy=True)
+    for g in range(f.shape[0]):
+        for j, b in enumerate(sel[g]):
+            if 0 <= b < n_units:
+                f[g, b] += mass[g, j]
+    f[:, :n_units] *= decay
+    return f
+
+
+def _mut_freq_idle_units_kept(freq, sel, mass, n_units, decay):
+    # only looked-up units decay
+    f = np.array(freq, dtype=np.float64, copy=True)
+    for g in range(f.shape[0]):
+        for j, b in enumerate(sel[g]):
+            if 0 <= b < n_units:
+                f[g, b] = f[g, b] * decay + mass[g, j]
+    return f
+
+
 MUTANTS = [
     ("partition", _mut_partition_drop_remainder),
     ("partition", _mut_partition_ceil_units),
@@ -237,6 +298,12 @@ MUTANTS = [
     ("unit_start", _mut_unit_start_off_by_one),
     ("context_positions", _mut_context_drop_init),
     ("select_units", _mut_select_top_km_minus_1),
+    ("unit_mass", _mut_mass_unnormalised),
+    ("unit_mass", _mut_mass_first_head_only),
+    ("unit_mass", _mut_mass_span_short),
+    ("unit_mass", _mut_mass_no_remap),
+    ("frequency_update", _mut_freq_add_then_decay),
+    ("frequency_update", _mut_freq_idle_units_kept),
     ("rotate", _mut_rotate_half_split),
     ("rotate", _mut_rotate_backwards),
     ("unit_relevance", _mut_relevance_true_positions),
