@@ -46,6 +46,9 @@ ATTN_TRAFFIC = {"src_sha256": "ca0b21819ced1ced360e29015d9124ae273f0ec880f50dc0d
                 "copy_write": 1048576.0 / 1048576.0}  # WRITE_SIZE KiB per KiB written by the copy
 
 
+MASS_DECAY = 0.1  # the frequency score's decay coefficient in the paper's experiments
+
+
 def attention_traffic_bytes():
     t = ATTN_TRAFFIC
     if t is None:
@@ -153,7 +156,7 @@ def params_of(wl, remap=False, mean_repr=False):
 class Stream:
     """Device state of one layer over a sequence, stepped through infllm_step."""
 
-    def __init__(self, wl, inputs, torch, remap=False, mean_repr=False):
+    def __init__(self, wl, inputs, torch, remap=False, mean_repr=False, mass=False):
         from paper_2402_04617_amd import infllm as F
         self.F, self.torch, self.wl = F, torch, wl
         self.p = params_of(wl, remap, mean_repr)
@@ -169,6 +172,11 @@ class Stream:
         self.scores = torch.zeros(wl.batch * wl.n_kv_heads * self.max_units, dtype=torch.float32, device="cuda")
         self.idx = torch.zeros((wl.batch, wl.n_kv_heads, max(1, wl.topk)), dtype=torch.int32, device="cuda")
         self.esize = 2 if dt == torch.bfloat16 else 4
+        # after each step: the looked-up units' attention mass and the decayed frequency score
+        self.mass = None
+        if mass:
+            self.mass = torch.zeros((wl.batch, wl.n_kv_heads, max(1, wl.topk)), dtype=torch.float32, device="cuda")
+            self.freq = torch.zeros((wl.batch, wl.n_kv_heads, self.max_units), dtype=torch.float32, device="cuda")
 
     def ptr(self, name, past):
         return self.inp[name].data_ptr() + past * self.wl.head_dim * self.esize
@@ -178,6 +186,9 @@ class Stream:
         self.F.infllm_step(self.p, self.mem.struct, self.ptr("q", past), S * D, self.ptr("k", past),
                            self.ptr("v", past), S * D, n, past, units_built, self.scores, self.idx, self.out,
                            wl.chunk * D, self.lse, self.ws)
+        if self.mass is not None:
+            self.F.infllm_unit_mass(self.p, self.mem.struct, self.ptr("q", past), S * D, n, past, self.idx, wl.topk,
+                                    self.lse, MASS_DECAY, self.mass, self.freq)
         return self.F.infllm_partition(self.p, past)[1]
 
     def run(self, steps, built=0, on_step=None):
@@ -260,7 +271,7 @@ def time_steps(torch, fn, steps, warmup):
 
 
 def encode_leg(name, seed, steps, warmup, torch, want_roofline=True, remap=False, inputs=None, mean_repr=False,
-               **method):
+               mass=False, **method):
     """One encode stream of workload `name`; `method` overrides method parameters (block_size,
     n_repr, topk, chunk) on the same inputs."""
     from workload import WORKLOADS, Synth
@@ -272,10 +283,11 @@ def encode_leg(name, seed, steps, warmup, torch, want_roofline=True, remap=False
     if inputs is None:
         inputs = upload_inputs(synth, torch)
         log(f"{name}: inputs resident in HBM ({time.time() - t:.1f}s)")
-    st = Stream(wl, inputs, torch, remap, mean_repr)
+    st = Stream(wl, inputs, torch, remap, mean_repr, mass)
     plan = wl.step_starts()
     ms = time_steps(torch, lambda: st.run(plan), steps, warmup)
-    res = {"workload": name + ("+remap" if remap else "") + ("+mean-repr" if mean_repr else ""),
+    res = {"workload": name + ("+remap" if remap else "") + ("+mean-repr" if mean_repr else "") +
+           ("+unit-mass" if mass else ""),
            "seq_len": wl.seq_len, "ms_per_step": ms,
            "ctx_tok_per_s": wl.seq_len * wl.batch / (ms / 1e3)}
     if method:
@@ -436,8 +448,8 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--legs", default="1m,1m-paper,32l-1m,decode,remap,mean",
-                    help="extra legs: comma list of 1m, 1m-paper, 32l-1m, decode, remap, mean (or 'none')")
+    ap.add_argument("--legs", default="1m,1m-paper,32l-1m,decode,remap,mean,mass",
+                    help="extra legs: comma list of 1m, 1m-paper, 32l-1m, decode, remap, mean, mass (or 'none')")
     ap.add_argument("--sweep", action="store_true",
                     help="only time the 128K stream under the paper's memory settings (r_k, k_m, l_bs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -483,6 +495,15 @@ def main():
         del st_m
         extra["encode_128k_mean_repr"] = rm
         log(f"128K mean repr: {rm['ms_per_step']:.2f} ms/step, {rm['ctx_tok_per_s'] / 1e6:.2f}M ctx tok/s")
+    if "mass" in legs:
+        # the same 128K stream with the attention mass / frequency score after every step
+        rs, _, st_s = encode_leg("llama3-8b-128k", args.seed, args.steps, args.warmup, torch, want_roofline=False,
+                                 inputs=st.inp, mass=True)
+        del st_s
+        rs["added_us_per_step"] = (rs["ms_per_step"] - main_res["ms_per_step"]) * 1e3 / len(st.wl.step_starts())
+        rs["decay"] = MASS_DECAY
+        extra["encode_128k_unit_mass"] = rs
+        log(f"128K with unit mass: {rs['ms_per_step']:.2f} ms/step (+{rs['added_us_per_step']:.1f} us per chunk)")
     del st
     torch.cuda.empty_cache()
     if "1m" in legs or "1m-paper" in legs or "32l-1m" in legs:

@@ -9,20 +9,21 @@
 // natural-log normaliser.  The frequency score of every built unit then decays,
 // s_b <- s_b * d, and a looked-up unit adds its mass.
 //
-// One workgroup per (sequence*kv head, lookup slot).  bf16: the unit's keys are
-// staged in LDS once (rows padded by 16 bytes so the fragment reads of 32 rows
-// spread over the banks), each wave takes 32-row blocks of the group's queries
-// as the B operand of v_mfma_f32_32x32x16_bf16 against 32-key blocks of the
-// unit, exponentiates against the row's lse and accumulates; one float per lane,
-// then a wave and a workgroup sum.  float32: plain dot products per (row, key).
-// Extra workgroups, one per (sequence*kv head), decay the scores of the units
-// not looked up, so every score is written by exactly one thread.
+// One workgroup (16 waves) per (sequence*kv head, lookup slot).  bf16: the unit's
+// keys are staged in LDS once (rows padded by 16 bytes so the fragment reads of
+// 32 rows spread over the banks); each wave takes two 32-row blocks of the
+// group's queries at a time as B operands of v_mfma_f32_32x32x16_bf16, so every
+// K fragment read from LDS (one k-step ahead) feeds two independent accumulator
+// chains; each score is exponentiated against its row's lse and summed, one
+// float per lane, then a wave and a workgroup sum.  float32: plain dot products
+// per (row, key).  Extra workgroups, one per (sequence*kv head), decay the scores
+// of the units not looked up, so every score is written by exactly one thread.
 #include "launch.h"
 
 namespace infllm {
 namespace {
 
-constexpr int kMassThreads = 512;
+constexpr int kMassThreads = 1024;
 constexpr int kMassWaves = kMassThreads / 64;
 constexpr int kMassMaxBlock = 256;  // largest l_bs
 
@@ -59,51 +60,81 @@ __device__ void unit_mass_bf16(const MassArgs& a, int bg, int slot, int unit, fl
 
   const float c2 = a.sm_scale * 1.4426950408889634f;
   const int R = G * a.n_q;  // rows: head-major (hh * n_q + i)
-  float acc = 0.f;
   const int nn = lane & 31, gs = lane >> 5;
   const int n_kblk = (lbs + 31) / 32;
-  for (int rb = wave; rb * 32 < R; rb += kMassWaves) {
+  const int n_rblk = (R + 31) / 32;
+  // This lane's query pieces of row block rb (the B operand: row 32*rb + nn, dims
+  // 16s + 8*gs .. +8; under the remap turned by R(l_L) and rounded to bf16, as the
+  // attention does for memory keys) and the row's lse in the exp2 domain.
+  auto load_rows = [&](int rb, bf16x8 (&qf)[KSTEPS], float& lse2, bool& ok) {
     const int row = rb * 32 + nn;
-    const bool row_ok = row < R;
-    const int hh = row_ok ? row / a.n_q : 0, qi = row_ok ? row - hh * a.n_q : 0;
+    ok = rb < n_rblk && row < R;
+    const int hh = ok ? row / a.n_q : 0, qi = ok ? row - hh * a.n_q : 0;
     const int qh = g * G + hh;
-    // this lane's query pieces (B operand): row `row`, dims 16s + 8*gs .. +8
     const bf16_t* qp = (const bf16_t*)a.q + (int64_t)(b * a.n_q_heads + qh) * a.q_head_stride + (int64_t)qi * D;
-    bf16x8 qf[KSTEPS];
+    u32x4 raw[KSTEPS];
+#pragma unroll
+    for (int s = 0; s < KSTEPS; ++s) raw[s] = ok ? *(const u32x4*)(qp + 16 * s + 8 * gs) : u32x4{0, 0, 0, 0};
+    lse2 = ok ? a.lse[(int64_t)(b * a.n_q_heads + qh) * a.n_q + qi] * 1.4426950408889634f : __builtin_inff();
 #pragma unroll
     for (int s = 0; s < KSTEPS; ++s) {
-      u32x4 raw = row_ok ? *(const u32x4*)(qp + 16 * s + 8 * gs) : u32x4{0, 0, 0, 0};
       if (a.rope.on) {
-        // memory keys meet the query turned by R(l_L), rounded to bf16 as the attention does
 #pragma unroll
         for (int j = 0; j < 4; ++j) {
           const int pr = 8 * s + 4 * gs + j;
           const float cs = a.rope.mem_cos[pr], sn = a.rope.mem_sin[pr];
-          const float x0 = __uint_as_float(raw[j] << 16), x1 = __uint_as_float(raw[j] & 0xFFFF0000u);
-          raw[j] = (uint32_t)f32_to_bf16(x0 * cs - x1 * sn) | ((uint32_t)f32_to_bf16(x0 * sn + x1 * cs) << 16);
+          const float x0 = __uint_as_float(raw[s][j] << 16), x1 = __uint_as_float(raw[s][j] & 0xFFFF0000u);
+          raw[s][j] = (uint32_t)f32_to_bf16(x0 * cs - x1 * sn) | ((uint32_t)f32_to_bf16(x0 * sn + x1 * cs) << 16);
         }
       }
-      qf[s] = __builtin_bit_cast(bf16x8, raw);
+      qf[s] = __builtin_bit_cast(bf16x8, raw[s]);
     }
-    const float lse2 = row_ok ? a.lse[(int64_t)(b * a.n_q_heads + qh) * a.n_q + qi] * 1.4426950408889634f : 0.f;
-    for (int kbk = 0; kbk < n_kblk; ++kbk) {
-      f32x16 sacc = {};
+  };
+  // p = exp2(S*c2 - lse2) over a 32x32 block (lane: row nn, keys 32*kbk + 8*(j/4)
+  // + 4*gs + j%4).  A row past R carries lse2 = +inf (p = 0); keys past l_bs are
+  // left out in the last, partial key block only.
+  auto add_block = [&](const f32x16& sacc, int kbk, float lse2, float& acc) {
+    if (32 * kbk + 32 <= lbs) {
 #pragma unroll
-      for (int s = 0; s < KSTEPS; ++s) {
-        // A operand: key row 32*kbk + nn (clamped; masked below), dims 16s + 8*gs
-        const int kr = min(32 * kbk + nn, lbs - 1);
-        const bf16x8 kf = *(const bf16x8*)(ks + kr * ROW_BYTES + (16 * s + 8 * gs) * 2);
-        sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sacc, 0, 0, 0);
-      }
-      // lane holds column nn (this row) and keys 8*(j/4) + 4*gs + j%4 of the block
+      for (int j = 0; j < 16; ++j) acc += __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[j], c2, -lse2));
+    } else {
 #pragma unroll
       for (int j = 0; j < 16; ++j) {
         const int key = 32 * kbk + 8 * (j >> 2) + 4 * gs + (j & 3);
         const float p = __builtin_amdgcn_exp2f(__builtin_fmaf(sacc[j], c2, -lse2));
-        acc += (row_ok && key < lbs) ? p : 0.f;
+        acc += key < lbs ? p : 0.f;
       }
     }
+  };
+  auto kfrag = [&](int kbk, int s) {
+    const int kr = min(32 * kbk + nn, lbs - 1);  // clamped; masked in add_block
+    return *(const bf16x8*)(ks + kr * ROW_BYTES + (16 * s + 8 * gs) * 2);
+  };
+  // Each wave takes two row blocks at a time: every K fragment read from LDS feeds
+  // two independent accumulator chains, and the next fragment is read one k-step
+  // ahead.
+  float acc0 = 0.f, acc1 = 0.f;
+  for (int rb = 2 * wave; rb < n_rblk; rb += 2 * kMassWaves) {
+    bf16x8 qa[KSTEPS], qb[KSTEPS];
+    float la, lb;
+    bool oka, okb;
+    load_rows(rb, qa, la, oka);
+    load_rows(rb + 1, qb, lb, okb);
+    for (int kbk = 0; kbk < n_kblk; ++kbk) {
+      f32x16 sa = {}, sb = {};
+      bf16x8 kf[2];
+      kf[0] = kfrag(kbk, 0);
+#pragma unroll
+      for (int s = 0; s < KSTEPS; ++s) {
+        if (s + 1 < KSTEPS) kf[(s + 1) & 1] = kfrag(kbk, s + 1);
+        sa = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s & 1], qa[s], sa, 0, 0, 0);
+        sb = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf[s & 1], qb[s], sb, 0, 0, 0);
+      }
+      add_block(sa, kbk, la, acc0);
+      add_block(sb, kbk, lb, acc1);
+    }
   }
+  const float acc = acc0 + acc1;
   const float tot = block_sum(acc, red);
   if (tid == 0) {
     a.mass[(int64_t)bg * a.k + slot] = tot;
