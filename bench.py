@@ -382,9 +382,9 @@ def decode_varlen_leg(st, steps, warmup, torch, spacing=6144):
             "us_per_step": ms * 1e3 / T, "tok_per_s": B * T / (ms / 1e3)}
 
 
-def cpu_baseline(synth, n_chunk_samples=64):
+def cpu_baseline(synth, n_chunk_samples=128):
     """The oracle on a bounded sample of the 128K encode: kv head 0 (of 8) with its 4 query heads;
-    all of that head's units are built, and every 4th chunk is scored, looked up and attended.
+    all of that head's units are built, and every 2nd chunk is scored, looked up and attended.
     Extrapolated linearly to all chunks and all kv heads."""
     from oracle import infllm_oracle as O
     try:
