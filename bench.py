@@ -415,7 +415,8 @@ def cpu_baseline(synth, n_chunk_samples=128):
     t_full = wl.n_kv_heads * (t_units + t_chunks * len(plan) / len(sample))
     return {"value": S / t_full, "unit": "ctx tok/s", "cores": threads, "kind": "oracle",
             "sample": f"kv head 0 of {wl.n_kv_heads}: all {last_units} units built, {len(sample)} of {len(plan)} "
-                      f"chunks (every {stride}th) scored/selected/attended; extrapolated x{len(plan) / len(sample):g} "
+                      f"chunks (every {stride}{'nd' if stride == 2 else 'rd' if stride == 3 else 'th'}) scored/selected/attended; "
+                      f"extrapolated x{len(plan) / len(sample):g} "
                       f"over chunks and x{wl.n_kv_heads} over kv heads",
             "sample_seconds": t_units + t_chunks}
 
