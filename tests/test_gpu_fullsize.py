@@ -91,14 +91,25 @@ def test_encode_128k_sampled_steps(mode):
     lse_tol = 1e-2 if mode == "remap" else 1e-3  # rotated q and k enter the MFMA rounded to bf16
     G = wl.group
     n_checked = 0
+    mass = torch.zeros((1, wl.n_kv_heads, wl.topk), dtype=torch.float32, device="cuda")
+    mass_rel = 2e-2 if mode == "remap" else 2e-3  # twice the lse tolerance (p = exp(z - lse))
     for si, (past, n) in enumerate(steps):
         L.step(qd, kd, vd, past, n)
         if si not in check:
             continue
         log(f"[128k] checking step {si} past={past}")
+        # the looked-up units' attention mass at the benchmark's shape (its unit-mass leg)
+        F.infllm_unit_mass(p, L.mem.struct, qd.data_ptr() + past * wl.head_dim * 2, wl.seq_len * wl.head_dim, n,
+                           past, L.idx, wl.topk, L.lse, 0.1, mass)
         nu = O.partition(past, op).n_units
         got = L.capture(n, nu)
+        gm = host(mass)
         r = conditioned_step(so, 0, past, n, host(L.mem.repr_idx)[0])
+        same = [check_selection(got["idx"][0, g], r["idx"][g], r["scores"][g], wl.topk) for g in range(wl.n_kv_heads)]
+        om = O.unit_mass(q[0, :, past:past + n], k[0], past, np.array(r["idx"]), op)
+        for g in range(wl.n_kv_heads):
+            if same[g]:
+                assert np.all(np.abs(gm[0, g] - om[g]) <= mass_rel * om[g] + 1e-6 * G * n), (si, g)
         for g in range(wl.n_kv_heads):
             es = r["scores"][g]
             scale = max(np.abs(es).max(), np.sqrt(np.mean(es ** 2)))
