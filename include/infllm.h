@@ -247,7 +247,9 @@ infllm_status infllm_lse_merge(const infllm_params* p, int32_t batch, int32_t n_
  *        freq * decay + mass(b), with mass 0 for units not looked up (all units
  *        stay resident here, so all of them decay).  Zero it before the first step.
  * decay: finite, >= 0 (the paper uses 0.1).  Run it after the step's attention on
- * the same stream.  E_UNSUPPORTED for k > 1024. */
+ * the same stream.  All sequences share past_len (for a batch stepped with
+ * infllm_step_varlen, call it per sequence on a one-sequence view of the memory).
+ * E_UNSUPPORTED for k > 1024. */
 infllm_status infllm_unit_mass(const infllm_params* p, const infllm_memory* m, const void* q,
                                int64_t q_head_stride, int32_t n_q, int64_t past_len, const int32_t* idx, int32_t k,
                                const float* lse, float decay, float* mass, float* freq, void* stream);
