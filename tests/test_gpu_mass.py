@@ -120,3 +120,32 @@ def test_unit_mass_every_unit_looked_up():
     S, chunk = 16 * 40 + 1 + 32, 32
     q, k, v = rand_inputs(rng, G * Hkv, Hkv, S, D, "bf16")
     _run(p, "bf16", q, k, v, _steps(S, chunk), chunk)
+
+
+def test_unit_mass_degenerate_calls():
+    # no lookup slots (k = 0): only the decay of every built unit; no queries (n_q = 0): every
+    # looked-up unit gets mass 0 and every built unit still decays; units not built stay untouched
+    rng = np.random.default_rng(21)
+    G, Hkv, D, S, chunk = 2, 2, 64, 700, 100
+    p = F.params(G * Hkv, Hkv, D, 4, 128, 32, 2, 4, "bf16")
+    q, k, v = rand_inputs(rng, G * Hkv, Hkv, S, D, "bf16")
+    L = Layer(p, 1, S, chunk=chunk)
+    qd, kd, vd = dev(q, "bf16"), dev(k, "bf16"), dev(v, "bf16")
+    for past, n in _steps(S, chunk):
+        L.step(qd, kd, vd, past, n)
+    past = S - 1  # the last step's past length had units; use the full prefix for the calls below
+    nu = O.partition(past, oparams(p)).n_units
+    assert nu > 4
+    f0 = rng.uniform(0.5, 2.0, (1, Hkv, L.max_units)).astype(np.float32)
+    freq = torch.from_numpy(f0).cuda()
+    mass = torch.full((1, Hkv, 4), 7.0, device="cuda")
+    F.infllm_unit_mass(p, L.mem.struct, None, 0, 0, past, None, 0, None, 0.25, None, freq)
+    got = host(freq)
+    assert np.allclose(got[0, :, :nu], f0[0, :, :nu] * np.float32(0.25), rtol=0, atol=0)
+    assert np.array_equal(got[0, :, nu:], f0[0, :, nu:])
+    idx = torch.tensor([[[0, 2, -1, nu - 1], [1, 3, 4, nu + 5]]], dtype=torch.int32, device="cuda")
+    F.infllm_unit_mass(p, L.mem.struct, None, 0, 0, past, idx, 4, None, 0.5, mass, freq)
+    assert np.array_equal(host(mass), np.zeros((1, Hkv, 4), dtype=np.float32))
+    got2 = host(freq)
+    assert np.allclose(got2[0, :, :nu], got[0, :, :nu] * np.float32(0.5), rtol=0, atol=0)
+    assert np.array_equal(got2[0, :, nu:], f0[0, :, nu:])
