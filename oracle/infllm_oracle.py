@@ -43,9 +43,6 @@ class Params:
     # Rotary angular frequencies theta_i (radians per position) of the D/2 dimension
     # pairs (2i, 2i+1) for the positional remap; None: positions pre-applied.
     rope_inv_freq: Optional[Tuple[float, ...]] = None
-    # With bfloat16 inputs the rotated keys R(t) k_t are held in bfloat16, like
-    # the rest of the key cache: round them once (to nearest, ties to even).
-    rope_keys_bf16: bool = False
     # Units represented by the mean of their keys (the "Mean Repr" alternative of
     # Section 4) instead of r_k representative tokens.
     mean_repr: bool = False
@@ -78,19 +75,6 @@ def rotate(x: np.ndarray, positions, inv_freq: Sequence[float]) -> np.ndarray:
     out[..., 0::2] = x[..., 0::2] * c - x[..., 1::2] * s
     out[..., 1::2] = x[..., 0::2] * s + x[..., 1::2] * c
     return out
-
-
-def round_bf16(x: np.ndarray) -> np.ndarray:
-    """Round float64 values once to bfloat16 (8 significant bits, to nearest, ties to even)."""
-    x = np.asarray(x, dtype=np.float64)
-    m, e = np.frexp(x)  # x = m * 2^e with 0.5 <= |m| < 1
-    return np.ldexp(np.round(np.ldexp(m, 8)), e - 8)
-
-
-def rotate_keys(k: np.ndarray, positions, p: Params) -> np.ndarray:
-    """Keys rotated to their own positions as the cache holds them (rounded to bf16 if so stored)."""
-    r = rotate(k, positions, p.rope_inv_freq)
-    return round_bf16(r) if p.rope_keys_bf16 else r
 
 
 def partition(past_len: int, p: Params) -> Partition:
@@ -143,7 +127,7 @@ def representative_scores(q_group: np.ndarray, k_head: np.ndarray, unit: int, p:
         # Positional remap: while token m is in the local window its queries see it
         # at the true distance j, so both sides keep their own positions.
         qw = rotate(qw, np.arange(m0 + 1, m0 + lbs + lL), p.rope_inv_freq)
-        ku = rotate_keys(ku, np.arange(m0, m0 + lbs), p)
+        ku = rotate(ku, np.arange(m0, m0 + lbs), p.rope_inv_freq)
     dots = ku @ qw.T  # dots[t, a] = k_{m0+t} . q~_{m0+1+a}
     r = np.empty(lbs)
     for t in range(lbs):
@@ -251,8 +235,8 @@ def attention_logits(q_chunk: np.ndarray, k: np.ndarray, past_len: int, sel_g: n
     kx = np.asarray(k[g, past_len: past_len + nq], dtype=np.float64)
     n_mem = pos.shape[0] - (past_len - part.local_begin)
     if remap:
-        kc[n_mem:] = rotate_keys(kc[n_mem:], pos[n_mem:], p)
-        kx = rotate_keys(kx, np.arange(past_len, past_len + nq), p)
+        kc[n_mem:] = rotate(kc[n_mem:], pos[n_mem:], p.rope_inv_freq)
+        kx = rotate(kx, np.arange(past_len, past_len + nq), p.rope_inv_freq)
     z = np.empty((G, nq, pos.shape[0] + nq))
     for hh in range(G):
         qh = np.asarray(q_chunk[g * G + hh], dtype=np.float64)

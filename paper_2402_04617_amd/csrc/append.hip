@@ -205,8 +205,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
     double* col = a.qprefix + (int64_t)bg * a.ring * D + d;
     const int slot0 = (int)(past % a.ring);
     // every load that does not depend on this launch's writes is issued first
-    // with the positional remap the stored keys of earlier tokens are read rotated
-    const T* kread = (const T*)(ROPE ? a.k_rot : a.k_store);
+    const T* kread = (const T*)a.k_store;
     double x[kThinMaxQ], ht[kThinMaxQ];
     float kt[kThinMaxQ];
 #pragma unroll
@@ -252,11 +251,9 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
           const int st = sp - a.n_local + (sp < a.n_local ? a.ring : 0);
           h = col[(int64_t)st * D];
           k = Elem<T>::load((const T*)a.k_src + (int64_t)bg * a.kv_head_stride + (t - past) * D + d);
-          if (ROPE) {
-            k = rot_lane(k, t);  // as the copy blocks store it in k_rot
-            if constexpr (sizeof(T) == 2) k = (double)bf16_to_f32(f32_to_bf16((float)k));
-          }
         }
+        // positional remap: the input key turned to its own position, unrounded
+        if (ROPE) k = rot_lane(k, t);
         double part = k * (run - h);
 #pragma unroll
         for (int o = 1; o < 16; o <<= 1) part += __shfl_xor(part, o);
@@ -282,7 +279,9 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
 
   __shared__ double wave_tot[kWaves][2][8];
   __shared__ float wave_raw[kWaves][2][8];
-  const T* kread = (const T*)(ROPE ? a.k_rot : a.k_store);  // stored keys, rotated under the remap
+  // stored keys as given (unrotated); under the remap each is turned to its own
+  // position here in float32, never through the bf16-rounded k_rot copy
+  const T* kread = (const T*)a.k_store;
   float raw_acc[8];  // unrotated query sum of this thread's positions (the chunk total feeds scoring)
 #pragma unroll
   for (int e = 0; e < 8; ++e) raw_acc[e] = 0.f;
@@ -410,6 +409,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
       const int i = i0 + s;
       float kt[8];
       raw8_to_float<T>(kr[s], kt);
+      if (ROPE && early) rotate8(kt, past + i - a.n_local, d0 / 2, a.rope);
       part[s] = 0.0;
       if (i < a.n_q) {
         const int slot = slot0 + i - (slot0 + i >= a.ring ? a.ring : 0);
@@ -470,15 +470,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
         const bool act = i < a.n_q && t >= a.n_init;
         float kt[8];
         raw8_to_float<T>(kk[s], kt);
-        // a key of this chunk comes unrotated from k_src; rotated here and rounded to
-        // the store's dtype, it equals what the copy blocks write to k_rot
-        if (ROPE && t >= past) {
-          rotate8(kt, t, d0 / 2, a.rope);
-          if constexpr (sizeof(T) == 2) {
-#pragma unroll
-            for (int e = 0; e < 8; ++e) kt[e] = bf16_to_f32(f32_to_bf16(kt[e]));
-          }
-        }
+        if (ROPE) rotate8(kt, t, d0 / 2, a.rope);  // the key at its own position, float32
         double p = 0.0;
 #pragma unroll
         for (int e = 0; e < 4; ++e)

@@ -35,8 +35,7 @@ def host(t: torch.Tensor) -> np.ndarray:
 def oparams(p: F.Params) -> O.Params:
     freqs = tuple(float(p.rope_inv_freq[i]) for i in range(p.head_dim // 2)) if p.remap else None
     return O.Params(p.n_q_heads, p.n_kv_heads, p.head_dim, p.n_init, p.n_local, p.block_size, p.n_repr,
-                    p.topk, float(p.sm_scale), rope_inv_freq=freqs, mean_repr=p.mean_repr,
-                    rope_keys_bf16=p.remap and p.dtype == F.INFLLM_BF16)
+                    p.topk, float(p.sm_scale), rope_inv_freq=freqs, mean_repr=p.mean_repr)
 
 
 class Layer:

@@ -408,21 +408,6 @@ def check_rotation_is_complex_multiplication():
     assert np.allclose(ab, O.rotate(x, 14.0, freqs), rtol=1e-12, atol=1e-12)
 
 
-def check_bf16_rounding():
-    """round_bf16 against PyTorch's float32 -> bfloat16 conversion (round to nearest even), on values
-    exactly representable in float32, including exact ties and both signs; and the bf16-stored rotated
-    keys are exactly those rounded values."""
-    rng = np.random.default_rng(39)
-    x = (rng.standard_normal(4000) * np.exp(rng.uniform(-20, 20, 4000))).astype(np.float32)
-    ties = (np.arange(1, 300, dtype=np.float32) * 2 + 1) * np.float32(2.0 ** -9)  # halfway between bf16 values
-    x = np.concatenate([x, ties, -ties])
-    ref = torch.from_numpy(x).to(torch.bfloat16).float().numpy().astype(np.float64)
-    assert np.array_equal(O.round_bf16(x.astype(np.float64)), ref)
-    p = O.Params(1, 1, 6, 0, 4, 2, 1, 1, rope_inv_freq=(0.3, 1.1, 0.07), rope_keys_bf16=True)
-    k = rng.standard_normal((5, 6))
-    assert np.array_equal(O.rotate_keys(k, np.arange(5), p), O.round_bf16(O.rotate(k, np.arange(5), p.rope_inv_freq)))
-
-
 def check_remap_zero_frequencies_is_identity():
     """All angles zero: the remap changes nothing (every rotation is the identity)."""
     rng = np.random.default_rng(32)
@@ -690,7 +675,6 @@ ALL_CHECKS = [
     check_lse_merge,
     check_hand_worked_example,
     check_rotation_is_complex_multiplication,
-    check_bf16_rounding,
     check_remap_zero_frequencies_is_identity,
     check_remap_attention_effective_positions,
     check_remap_relevance_effective_positions,

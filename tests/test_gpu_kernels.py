@@ -196,6 +196,10 @@ ATTEND_CASES = [
     ("f32", 2, 1, 64, 16, 256, 32, 4, 1000, 1, 1),
     ("f32", 4, 2, 128, 128, 512, 128, 4, 3000, 37, 2),
     ("f32", 3, 2, 64, 0, 20, 8, 50, 500, 20, 1),            # k_m larger than n_units
+    # k_m = 0 once units have been evicted (f(X, E) empty, Section 3.1): I, then a gap, then L and X
+    ("bf16", 4, 2, 128, 128, 512, 128, 0, 3000, 512, 1),
+    ("bf16", 4, 2, 128, 128, 512, 128, 0, 3000, 1, 2),     # decode
+    ("f32", 2, 1, 64, 16, 256, 32, 0, 1000, 64, 1),
 ]
 
 

@@ -20,7 +20,7 @@ def test_pin(check):
 # ------------------------------------------------------------------ mutants
 _orig = {name: getattr(O, name) for name in
          ("partition", "representative_scores", "top_indices", "unit_relevance", "attend",
-          "lse_merge", "context_positions", "select_units", "unit_start", "rotate", "mean_relevance", "round_bf16",
+          "lse_merge", "context_positions", "select_units", "unit_start", "rotate", "mean_relevance",
           "unit_mass", "frequency_update")}
 
 
@@ -132,13 +132,6 @@ def _mut_mean_skips_last_key(q, k, n_units, p):
         return np.zeros(0)
     pos = np.stack([np.arange(O.unit_start(u, p), O.unit_start(u, p) + p.block_size - 1) for u in range(n_units)])
     return O.unit_relevance(q, k, pos, p) / (p.block_size - 1)
-
-
-def _mut_round_truncates(x):
-    # round toward zero instead of to nearest even
-    x = np.asarray(x, dtype=np.float64)
-    m, e = np.frexp(x)
-    return np.ldexp(np.trunc(np.ldexp(m, 8)), e - 8)
 
 
 def _mut_attend_init_true_positions(q_chunk, k, v, past_len, sel, p):
@@ -312,7 +305,6 @@ MUTANTS = [
     ("attend", _mut_attend_init_true_positions),
     ("mean_relevance", _mut_mean_sum_not_mean),
     ("mean_relevance", _mut_mean_skips_last_key),
-    ("round_bf16", _mut_round_truncates),
 ]
 
 
