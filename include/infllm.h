@@ -143,6 +143,9 @@ infllm_status infllm_partition(const infllm_params* p, int64_t past_len, int64_t
  * for `batch` sequences and n_q current tokens (split-key partial results and
  * query sums).  Depends only on these arguments. */
 size_t infllm_workspace_bytes(const infllm_params* p, int32_t batch, int32_t n_q);
+/* The same size under the name the attention's callers may know it by; both names
+ * cover every call that takes a workspace (scoring as well as attention). */
+size_t infllm_attend_workspace_bytes(const infllm_params* p, int32_t batch, int32_t n_q);
 
 /* Append the current tokens X at positions [past_len, past_len + n_q).
  *  q: [batch][Hq] heads of n_q x D dtype rows; head h of sequence b starts at
@@ -187,7 +190,9 @@ infllm_status infllm_score_units(const infllm_params* p, const infllm_memory* m,
 /* Top-k lookup f(X, E) (Section 3.2): for each of `rows` rows of `scores`
  * ([rows][n_units] float32), the min(k, n_units) largest, ties to the lower index,
  * written ascending to idx [rows][k] int32 followed by -1 padding.  NaN scores
- * rank below every number; -0 equals +0. */
+ * rank below every number; -0 equals +0.  The selection depends on nothing but
+ * the scores and k, so it takes no params struct (rows = batch * Hkv for the
+ * scores infllm_score_units writes; k is k_m). */
 infllm_status infllm_select_topk(int32_t rows, const float* scores, int32_t n_units, int32_t k,
                                  int32_t* idx, void* stream);
 

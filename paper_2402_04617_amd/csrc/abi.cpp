@@ -442,6 +442,10 @@ size_t infllm_workspace_bytes(const infllm_params* p, int32_t batch, int32_t n_q
   return (r + 255) & ~(size_t)255;
 }
 
+size_t infllm_attend_workspace_bytes(const infllm_params* p, int32_t batch, int32_t n_q) {
+  return infllm_workspace_bytes(p, batch, n_q);
+}
+
 infllm_status infllm_append(const infllm_params* p, const infllm_memory* m, const void* q, int64_t q_head_stride,
                             const void* k, const void* v, int64_t kv_head_stride, int32_t n_q, int64_t past_len,
                             void* stream) {

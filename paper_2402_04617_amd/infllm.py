@@ -23,7 +23,7 @@ INFLLM_REPR_MEAN = 1
 STATUS = {0: "INFLLM_OK", 1: "INFLLM_E_NULL", 2: "INFLLM_E_SHAPE", 3: "INFLLM_E_RANGE",
           4: "INFLLM_E_UNSUPPORTED", 5: "INFLLM_E_WORKSPACE", 6: "INFLLM_E_LAUNCH", 7: "INFLLM_E_DEVICE"}
 
-EXPORTS = ["infllm_partition", "infllm_workspace_bytes", "infllm_append", "infllm_build_units",
+EXPORTS = ["infllm_partition", "infllm_workspace_bytes", "infllm_attend_workspace_bytes", "infllm_append", "infllm_build_units",
            "infllm_score_units", "infllm_select_topk", "infllm_chunk_attend", "infllm_attend_partial",
            "infllm_lse_merge", "infllm_step", "infllm_step_varlen", "infllm_unit_mass", "infllm_status_string"]
 
@@ -94,6 +94,8 @@ def lib() -> ctypes.CDLL:
         f.restype = ctypes.c_int
     L.infllm_workspace_bytes.argtypes = [P, i32, i32]
     L.infllm_workspace_bytes.restype = ctypes.c_size_t
+    L.infllm_attend_workspace_bytes.argtypes = [P, i32, i32]
+    L.infllm_attend_workspace_bytes.restype = ctypes.c_size_t
     L.infllm_status_string.argtypes = [ctypes.c_int]
     L.infllm_status_string.restype = ctypes.c_char_p
     _lib = L

@@ -82,6 +82,7 @@ def test_param_validation(L, kw, code):
     n0, n1, n2 = ctypes.c_int64(), ctypes.c_int32(), ctypes.c_int64()
     assert L.infllm_partition(ctypes.byref(p), 100, ctypes.byref(n0), ctypes.byref(n1), ctypes.byref(n2)) == code
     assert L.infllm_workspace_bytes(ctypes.byref(p), 1, 512) == 0
+    assert L.infllm_attend_workspace_bytes(ctypes.byref(p), 1, 512) == 0
 
 
 def test_workspace_bytes(L):
@@ -93,6 +94,8 @@ def test_workspace_bytes(L):
     # decode: room for the most key parts any batch can use, one per 256 keys of the bounded key
     # count l_I + k_m*l_bs + l_L + l_bs - 1 + 1
     wsd = L.infllm_workspace_bytes(ctypes.byref(p), 16, 1)
+    assert L.infllm_attend_workspace_bytes(ctypes.byref(p), 16, 1) == wsd
+    assert L.infllm_attend_workspace_bytes(ctypes.byref(p), 1, 512) == ws
     nv = 128 + 32 * 128 + 4096 + 127 + 1
     assert wsd >= (nv // 256) * 16 * 32 * row_bytes
 
