@@ -264,8 +264,12 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
     return;
   }
 
-  // ---- scan role
+  // ---- scan role.  The D/16 slice blocks of one (sequence, kv head) read 32-byte
+  // pieces of the same 256-byte query and key rows: they are placed on one XCD
+  // (blocks whose ids agree modulo the XCD count share one), so that its L2
+  // fetches each row from HBM once instead of once per slice.
   const int slices = D / 16;
+  if (grid.n_scan % kNumXcd == 0) blk = xcd_logical_block(blk, grid.n_scan);
   const int bg = blk / slices;
   const int b = bg / a.n_kv_heads, g = bg - b * a.n_kv_heads;
   const int64_t past = seq_past(a, b);

@@ -419,34 +419,47 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
     const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
     return fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * c2;  // c2 > 0
   };
-  // Running-max update.  Rescale only when some row's max grew by more than 2^8
-  // since the last rescale; otherwise keep the stale max (p <= 256, exact after
-  // the final normalisation).  The decision is wave-uniform, so both lane halves
-  // of a row always use the same max.
-  auto update_max = [&](float mx) {
-    if (__ballot(mx > m_run + 8.f)) {
-      const float m_new = fmaxf(m_run, mx);
-      const float alpha = (m_new == -__builtin_inff()) ? 1.f : fast_exp2(m_run - m_new);
-      l_run *= alpha;
+  // Lazy running max.  P is formed against the running max m_run without first
+  // taking the tile's own maximum; a row whose half-tile sum of P exceeds kLazy
+  // (2^16: P stays far inside the float and bf16 range) has met keys well above
+  // m_run, and only then is the tile's maximum taken and the row rescaled (a rare
+  // path; the decision is wave-uniform, and both lane halves of a row share
+  // m_run).  While a row has seen no visible key (m_run = -inf) any nonzero P
+  // takes that path, so the first visible tile sets m_run.
+  constexpr float kLazy = 65536.f;
+  auto lazy_bound = [&]() { return m_run == -__builtin_inff() ? 0.f : kLazy; };
+  auto force_max = [&](float mx) {
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = (m_new == -__builtin_inff()) ? 1.f : fast_exp2(m_run - m_new);
+    l_run *= alpha;
 #pragma unroll
-      for (int db = 0; db < DBLK; ++db)
+    for (int db = 0; db < DBLK; ++db)
 #pragma unroll
-        for (int j = 0; j < 16; ++j) oacc[db][j] *= alpha;
-      m_run = m_new;
-    }
+      for (int j = 0; j < 16; ++j) oacc[db][j] *= alpha;
+    m_run = m_new;
   };
-  // The keys [0, 32) half of P = exp2(S*c2 - m): bf16 operand pair and its row sum.
-  auto half0_p = [&](const f32x16& s0, bf16x8 (&ph)[2]) {
-    const float neg_m = (m_run == -__builtin_inff()) ? 0.f : -m_run;
+  // Two P values as a bf16 pair (one v_cvt_pk_bf16_f32), added unrounded to the
+  // two running row sums (the normaliser keeps float32 precision; rounding only
+  // the PV operand moves O by at most 2^-9 relative).
+  auto p_pair = [&](float z0, float z1, float nm, float (&acc)[2]) -> uint32_t {
+    const float e0 = fast_exp2(__builtin_fmaf(z0, c2, nm));
+    const float e1 = fast_exp2(__builtin_fmaf(z1, c2, nm));
+    acc[0] += e0;
+    acc[1] += e1;
+    bf16x2 pr;
+    pr[0] = (__bf16)e0;
+    pr[1] = (__bf16)e1;
+    return __builtin_bit_cast(uint32_t, pr);
+  };
+  // One 16-key half of P = exp2(S*c2 - m_run) as the bf16 operand pair, and its row sum.
+  auto half_p = [&](const f32x16& sh, u32x4 (&ph)[2]) {
+    const float nm = (m_run == -__builtin_inff()) ? 0.f : -m_run;
     float ps[2] = {0.f, 0.f};
 #pragma unroll
-    for (int j = 0; j < 16; ++j) {
-      const float p = fast_exp2(__builtin_fmaf(s0[j], c2, neg_m));
-      ps[j & 1] += p;
-      ph[j >> 3][j & 7] = (__bf16)p;
-    }
+    for (int w = 0; w < 8; ++w) ph[w >> 2][w & 3] = p_pair(sh[2 * w], sh[2 * w + 1], nm, ps);
     return ps[0] + ps[1];
   };
+  auto as_bf16x8 = [](const u32x4& w) { return __builtin_bit_cast(bf16x8, w); };
   // O^T += V^T P^T over the four 16-key steps (V buffer vbuf); DBLK independent
   // accumulator chains, each V^T fragment two transposed 8-byte reads.
   auto pv = [&](int vbuf, const bf16x8 (&pb)[2][2]) {
@@ -499,8 +512,10 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
   auto run_finish = [&](int tile, int64_t r) -> int64_t { return uniform64(r != -2 ? r : tile_run_start(tile)); };
   f32x16 sA[2], sB[2];
   // p0: the keys [0, 32) half of P(t), formed in the previous iteration's phase 2
-  // (or the prologue); replaced here by that half of P(t+1).
-  bf16x8 p0[2];
+  // (or the prologue), and l_pend its row sum, added to l_run once the other half
+  // of the tile has passed its lazy-max check; replaced here by that half of P(t+1).
+  u32x4 p0[2];
+  float l_pend = 0.f;
   auto iteration = [&](int t, f32x16 (&cur)[2], f32x16 (&nxt)[2], auto mask_next) {
     const int bc = (t - t_begin) % NBUF;
     const int bn = bc == NBUF - 1 ? 0 : bc + 1, bp = bc == 0 ? NBUF - 1 : bc - 1;
@@ -512,16 +527,17 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
     const int64_t run_next = run_read(t + 4);  // consumed after phase 2
 
     // Phases 1 and 2 run at raised wave priority (s_setprio 1), the barrier,
-    // address and max bookkeeping at normal priority: a wave in its MFMA phases
+    // address and bookkeeping at normal priority: a wave in its MFMA phases
     // wins the issue slots of its SIMD over a wave doing bookkeeping (measured a
     // few percent faster than uniform priority).
     __builtin_amdgcn_s_setprio(1);
-    // Phase 1: QK(t+1) on the matrix cores, half of P(t) on the vector ALUs.  Chunk s
-    // issues the K fragment reads of k-step s+1, the two MFMAs of k-step s and
-    // EPC elements of that half of P(t); scheduling fences keep that interleave.
-    const float neg_m = (m_run == -__builtin_inff()) ? 0.f : -m_run;
-    bf16x8 pb[2][2];
-    float psum[2] = {0.f, 0.f};  // two partial row sums (shorter dependency chains)
+    // Phase 1: QK(t+1) on the matrix cores, the keys [32, 64) half of P(t) on the
+    // vector ALUs.  Chunk s issues the K fragment reads of k-step s+1, the two
+    // MFMAs of k-step s and EPC elements of that half of P(t); scheduling fences
+    // keep that interleave.
+    float neg_m = (m_run == -__builtin_inff()) ? 0.f : -m_run;
+    u32x4 w1[2];
+    float ps1[2] = {0.f, 0.f};  // two partial row sums (shorter dependency chains)
     {
       const uint32_t ka = kaddr_of(bn);
       auto kfrag = [&](int kb, int s) { return kfrag_at(ka, kb, s); };
@@ -529,6 +545,7 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
       a0[0] = kfrag(0, 0);
       a1[0] = kfrag(1, 0);
       constexpr int EPC = 16 / KSTEPS;  // elements of P(t)'s keys [32, 64) half per chunk
+      static_assert(EPC % 2 == 0, "P elements are formed in bf16 pairs");
 #pragma unroll
       for (int s = 0; s < KSTEPS; ++s) {
         if (s + 1 < KSTEPS) {
@@ -547,21 +564,29 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
         if (s < NI) lds_load_run(ld_k + s * 1024, kbase, off_k[s]);
         else if (s < 2 * NI) lds_load_run(ld_v + (s - NI) * 1024, vbase, off_v[s - NI]);
 #pragma unroll
-        for (int i = 0; i < EPC; ++i) {
-          const int j = EPC * s + i;
-          const float p = fast_exp2(__builtin_fmaf(cur[1][j], c2, neg_m));
-          psum[i & 1] += p;
-          pb[1][j >> 3][j & 7] = (__bf16)p;
+        for (int i = 0; i < EPC; i += 2) {
+          const int w = (EPC * s + i) >> 1;  // bf16 pair index within the half
+          w1[w >> 2][w & 3] = p_pair(cur[1][2 * w], cur[1][2 * w + 1], neg_m, ps1);
         }
         __builtin_amdgcn_sched_barrier(0);
       }
     }
+    float psum1 = ps1[0] + ps1[1];
+    // lazy-max check of that half before it reaches the matrix cores: on the rare
+    // row that exceeds the bound, rescale to the tile's maximum and redo both halves
+    if (__ballot(psum1 > lazy_bound())) {
+      force_max(tile_max(cur));
+      l_pend = half_p(cur[0], p0);
+      psum1 = half_p(cur[1], w1);
+      neg_m = (m_run == -__builtin_inff()) ? 0.f : -m_run;
+    }
+    l_run += l_pend + psum1;
 
-    // Phase 2: PV(t) on the matrix cores; mask and row max of tile t+1 on the
-    // vector ALUs, one 16-key group (of the 32 accumulator elements) per step,
-    // and in the last two steps the keys [0, 32) half of P(t+1).
-    float mx = -__builtin_inff();
-    bf16x8 q0[2];
+    // Phase 2: PV(t) on the matrix cores; on the vector ALUs the mask of tile t+1
+    // (one 8-element group of its 32 accumulator elements per step) and, four
+    // elements per step, the keys [0, 32) half of P(t+1) against the running max
+    // (checked after the phase).
+    u32x4 q0[2];
     float ps0[2] = {0.f, 0.f};
     {
       constexpr bool MASK = decltype(mask_next)::value;
@@ -583,50 +608,38 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
       for (int j = 0; j < 4; ++j) {
 #pragma unroll
         for (int db = 0; db < DBLK; ++db) {
-          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[db], j < 2 ? p0[j & 1] : pb[1][j & 1], oacc[db], 0,
-                                                            0, 0);
+          oacc[db] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(va[db], as_bf16x8(j < 2 ? p0[j & 1] : w1[j & 1]),
+                                                            oacc[db], 0, 0, 0);
           if (j + 1 < 4) va[db] = vfrag(db, j + 1);
         }
-        if (j >= 2) {
-          // speculative P(t+1), keys [0, 32): 8 elements with the current max
-          // (redone below in the rare case the max of tile t+1 raises it)
+        if constexpr (MASK) {
+          // 8 of the 32 scores of tile t+1: elements [8j, 8j+8)
 #pragma unroll
           for (int i = 0; i < 8; ++i) {
-            const int jj = 8 * (j - 2) + i;
-            const float p = fast_exp2(__builtin_fmaf(nxt[0][jj], c2, neg_m));
-            ps0[i & 1] += p;
-            q0[jj >> 3][jj & 7] = (__bf16)p;
-          }
-        }
-        // 8 of the 32 scores of tile t+1: elements [8j, 8j+8)
-#pragma unroll
-        for (int i = 0; i < 8; ++i) {
-          const int e = 8 * j + i, kb = e >> 4, jj = e & 15;
-          if constexpr (MASK) {
+            const int e = 8 * j + i, kb = e >> 4, jj = e & 15;
             const int c = 32 * kb + 8 * (jj >> 2) + (jj & 3);
             bool vis = c <= lim;
             if (has_invalid) vis = vis && ((kv[jj >> 2][kb] >> (8 * (jj & 3))) & 0xFFu) != 0;
             nxt[kb][jj] = vis ? nxt[kb][jj] : -__builtin_inff();
           }
-          mx = fmaxf(mx, nxt[kb][jj]);
+        }
+        // P(t+1), keys [0, 32): elements [4j, 4j+4) (masked by step j/2 <= j)
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+          const int w = 2 * j + i;
+          q0[w >> 2][w & 3] = p_pair(nxt[0][2 * w], nxt[0][2 * w + 1], neg_m, ps0);
         }
         __builtin_amdgcn_sched_barrier(0);
       }
     }
-    {
-      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
-      mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * c2;  // c2 > 0
-    }
     __builtin_amdgcn_s_setprio(0);
-    l_run += psum[0] + psum[1];
     p0[0] = q0[0];
     p0[1] = q0[1];
-    float l_add = ps0[0] + ps0[1];
-    if (__ballot(mx > m_run + 8.f)) {
-      update_max(mx);
-      l_add = half0_p(nxt[0], p0);  // redo the half with the raised max
+    l_pend = ps0[0] + ps0[1];
+    if (__ballot(l_pend > lazy_bound())) {
+      force_max(tile_max(nxt));
+      l_pend = half_p(nxt[0], p0);
     }
-    l_run += l_add;
     run_v = run_k;
     run_k = run_finish(t + 4, run_next);
   };
@@ -660,8 +673,8 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
         for (int j = 0; j < 16; ++j)
           if (32 * kb + 8 * (j >> 2) + (j & 3) < lo) sA[kb][j] = -__builtin_inff();
     }
-    update_max(tile_max(sA));
-    l_run += half0_p(sA[0], p0);
+    force_max(tile_max(sA));  // the first tile sets the running max
+    l_pend = half_p(sA[0], p0);
 
     int t = t_begin;
     // next tile unmasked
@@ -686,20 +699,15 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
     }
     // drain: P and PV of the last tile (then no load is left in flight)
     publish_barrier<0>();
-    bf16x8 pb[2][2];
-    {
-      const float neg_m = (m_run == -__builtin_inff()) ? 0.f : -m_run;
-      float ps[2] = {0.f, 0.f};
-#pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const float p = fast_exp2(__builtin_fmaf(sA[1][j], c2, neg_m));
-        ps[j & 1] += p;
-        pb[1][j >> 3][j & 7] = (__bf16)p;
-      }
-      l_run += ps[0] + ps[1];
-      pb[0][0] = p0[0];
-      pb[0][1] = p0[1];
+    u32x4 w1[2];
+    float psum1 = half_p(sA[1], w1);
+    if (__ballot(psum1 > lazy_bound())) {
+      force_max(tile_max(sA));
+      l_pend = half_p(sA[0], p0);
+      psum1 = half_p(sA[1], w1);
     }
+    l_run += l_pend + psum1;
+    const bf16x8 pb[2][2] = {{as_bf16x8(p0[0]), as_bf16x8(p0[1])}, {as_bf16x8(w1[0]), as_bf16x8(w1[1])}};
     pv((t - t_begin) % NBUF, pb);
   }
 
