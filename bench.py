@@ -34,29 +34,31 @@ sys.path.insert(0, ROOT)
 PEAK_BF16_TFLOPS = 2500.0  # MI355X dense bf16 MFMA
 PEAK_HBM_GBS = 8000.0
 
-# HBM traffic of one 128K-encode attention launch, from two rocprofv3 --pmc passes (FETCH_SIZE, then
-# WRITE_SIZE; KiB per dispatch, averaged over the launches of `bench.py --legs none --steps 1 --warmup 0`),
-# each divided by what the same counter reads per KiB moved by the plain copy of `bench.py
-# --copy-calibration 1024`.  Valid only for the attention source it was taken on (sha256 below);
-# reported as null once that file changes.
-ATTN_SRC = os.path.join(ROOT, "paper_2402_04617_amd", "csrc", "attend_mfma.hip")
-ATTN_TRAFFIC = {"src_sha256": "ca0b21819ced1ced360e29015d9124ae273f0ec880f50dc0dfa4e3137856ece0",
-                "fetch_kib": 20024.35, "write_kib": 16896.0,  # per attention dispatch (768 dispatches)
-                "copy_fetch": 524300.0 / 1048576.0,  # FETCH_SIZE KiB per KiB read by the copy
-                "copy_write": 1048576.0 / 1048576.0}  # WRITE_SIZE KiB per KiB written by the copy
+# HBM traffic per launch, from two rocprofv3 --pmc passes (FETCH_SIZE, then WRITE_SIZE; KiB per
+# dispatch) over the default benchmark command, each divided by what the same counter reads per KiB
+# moved by the plain copy of `bench.py --copy-calibration 1024`.  An entry holds for the kernel
+# sources it was taken on (sha256 of each file); it is reported as null once any of them changes.
+CSRC = os.path.join(ROOT, "paper_2402_04617_amd", "csrc")
+COPY_FETCH = 524300.0 / 1048576.0  # FETCH_SIZE KiB per KiB read by the copy
+COPY_WRITE = 1048576.0 / 1048576.0  # WRITE_SIZE KiB per KiB written by the copy
+KERNEL_TRAFFIC = {
+    # key: {"src": {file: sha256}, "fetch_kib": ..., "write_kib": ...} (per launch)
+}
+
+
+def _sha(name):
+    with open(os.path.join(CSRC, name), "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def kernel_traffic_bytes(key):
+    t = KERNEL_TRAFFIC.get(key)
+    if t is None or any(_sha(f) != h for f, h in t["src"].items()):
+        return None
+    return 1024.0 * (t["fetch_kib"] / COPY_FETCH + t["write_kib"] / COPY_WRITE)
 
 
 MASS_DECAY = 0.1  # the frequency score's decay coefficient in the paper's experiments
-
-
-def attention_traffic_bytes():
-    t = ATTN_TRAFFIC
-    if t is None:
-        return None
-    with open(ATTN_SRC, "rb") as f:
-        if hashlib.sha256(f.read()).hexdigest() != t["src_sha256"]:
-            return None
-    return 1024.0 * (t["fetch_kib"] / t["copy_fetch"] + t["write_kib"] / t["copy_write"])
 
 
 def measured_peaks():
@@ -124,22 +126,23 @@ def attention_flops(wl, steps):
 
 
 def attention_bytes(wl, steps, parts):
-    """Algorithmic HBM bytes of the attention launches of a pass: each query row read once, each
-    visible context key and value read once per kv head, and the output written once per part
-    (partial rows when a launch splits the keys, the bf16 output otherwise)."""
+    """HBM bytes of the attention launches of a pass.  Algorithmic (the method's own data): each query
+    row read once, each visible context key and value read once per kv head (GQA shares them), the
+    output written once.  Split-key partials (written by the attention, read back by the merge when a
+    launch splits the keys) are implementation traffic, returned apart."""
     from paper_2402_04617_amd import infllm as F
     p = params_of(wl)
     e = 2 if wl.dtype == "bf16" else 4
     # a split-key partial row: fp16 values + lse + exponent (bf16), float32 values + lse (f32)
     part_row = 2 * wl.head_dim + 8 if wl.dtype == "bf16" else 4 * (wl.head_dim + 1)
-    total = 0
+    total = partials = 0
     for (past, n), np_ in zip(steps, parts):
         n_init, n_units, local_begin = F.infllm_partition(p, past)
         keys = n_init + min(wl.topk, n_units) * wl.block_size + (past - local_begin) + n
         rows = wl.batch * wl.n_q_heads * n
-        total += rows * wl.head_dim * e + 2 * wl.batch * wl.n_kv_heads * keys * wl.head_dim * e
-        total += np_ * rows * part_row if np_ > 1 else rows * wl.head_dim * e
-    return total
+        total += 2 * rows * wl.head_dim * e + 2 * wl.batch * wl.n_kv_heads * keys * wl.head_dim * e
+        partials += np_ * rows * part_row if np_ > 1 else 0
+    return total, partials
 
 
 def params_of(wl, remap=False, mean_repr=False):
@@ -270,6 +273,55 @@ def time_steps(torch, fn, steps, warmup):
     return t0.elapsed_time(t1) / steps
 
 
+def graph_replay_us(torch, fn, n=20, reps=5):
+    """Average duration of one call of `fn` (a library call enqueueing kernels on torch's current
+    stream): n calls captured into one HIP graph, replayed `reps` times between two HIP events.  The
+    graph removes the host's per-call cost, which exceeds the small kernels' own duration; what is
+    left is each launch plus its gap to the next.  Every call replayed here rewrites the same outputs
+    from the same inputs, so replays change no state."""
+    fn()
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        for _ in range(n):
+            fn()
+    g.replay()
+    torch.cuda.synchronize()
+    a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    a.record()
+    for _ in range(reps):
+        g.replay()
+    b.record()
+    torch.cuda.synchronize()
+    del g
+    return a.elapsed_time(b) * 1e3 / (n * reps)
+
+
+def hbm_entry(kernel, workload, us, algorithmic_bytes, traffic=None, **more):
+    """Roofline entry of an HBM-bound launch: algorithmic bytes / event-timed duration vs 8 TB/s."""
+    gbs = algorithmic_bytes / (us * 1e-6) / 1e9
+    e = {"kernel": kernel, "workload": workload, "bound": "hbm", "avg_us": us, "algorithmic_bytes": algorithmic_bytes,
+         "achieved": gbs, "peak": PEAK_HBM_GBS, "unit": "GB/s", "frac": gbs / PEAK_HBM_GBS,
+         "traffic": kernel_traffic_bytes(traffic) if traffic else None}
+    e.update(more)
+    return e
+
+
+def score_bytes(wl, n_units, n):
+    """infllm_score_units: the chunk's queries read once, each unit's key sum (float32) and score."""
+    return (wl.batch * wl.n_q_heads * n * wl.head_dim * 2
+            + wl.batch * wl.n_kv_heads * n_units * (wl.head_dim * 4 + 4))
+
+
+def append_bytes(wl, n):
+    """infllm_append of n positions: queries and the chunk's K/V read, K/V stored, the float64 running
+    sum written for each new position and read for each token leaving the window, that token's key
+    read, its partial representative scores (D/16 float64 per token) written."""
+    B, Hq, Hkv, D = wl.batch, wl.n_q_heads, wl.n_kv_heads, wl.head_dim
+    return (B * Hq * n * D * 2 + 2 * 2 * B * Hkv * n * D * 2 + 2 * B * Hkv * n * D * 8 + B * Hkv * n * D * 2
+            + B * Hkv * n * (D // 16) * 8)
+
+
 def encode_leg(name, seed, steps, warmup, torch, want_roofline=True, remap=False, inputs=None, mean_repr=False,
                mass=False, **method):
     """One encode stream of workload `name`; `method` overrides method parameters (block_size,
@@ -299,9 +351,27 @@ def encode_leg(name, seed, steps, warmup, torch, want_roofline=True, remap=False
         avg_ms, parts = st.attention_replay(plan, idx_hist)
         flops = attention_flops(wl, plan)
         tot_ms = avg_ms * len(plan)
+        ab, pb = attention_bytes(wl, plan, parts)
         res["attention"] = {"launches": len(plan), "avg_ms": avg_ms, "total_ms": tot_ms,
                             "algorithmic_flops": flops, "tflops": flops / (tot_ms / 1e3) / 1e12,
-                            "algorithmic_bytes_per_launch": attention_bytes(wl, plan, parts) / len(plan)}
+                            "algorithmic_bytes_per_launch": ab / len(plan),
+                            "split_partial_bytes_per_launch": pb / len(plan),
+                            "parts_per_launch": sorted(set(parts))}
+        # the memory-bound launches of the last chunk (the most units), replayed alone
+        past, n = plan[-1]
+        F = st.F
+        nu = F.infllm_partition(st.p, past)[1]
+        S, D = wl.seq_len, wl.head_dim
+        us = graph_replay_us(torch, lambda: F.infllm_score_units(st.p, st.mem.struct, st.ptr("q", past), S * D, n,
+                                                                 nu, st.scores, st.ws))
+        res["kernels"] = [hbm_entry("infllm_score_units (query sums + score_kernel)", f"{res['workload']} last chunk",
+                                    us, score_bytes(wl, nu, n), traffic=f"score_{name}", n_units=nu)]
+        if not mean_repr:
+            us = graph_replay_us(torch, lambda: F.infllm_append(st.p, st.mem.struct, st.ptr("q", past), S * D,
+                                                                st.ptr("k", past), st.ptr("v", past), S * D, n, past))
+            res["kernels"].append(hbm_entry("append_kernel (infllm_append: scan + copy)",
+                                            f"{res['workload']} last chunk", us, append_bytes(wl, n),
+                                            traffic=f"append_{name}"))
     return res, synth, st
 
 
@@ -322,6 +392,21 @@ def decode_leg(seed, steps, warmup, torch):
     us_tok = ms * 1e3 / len(plan)
     res = {"workload": wl.name, "decode_steps": len(plan), "batch": wl.batch, "us_per_step": us_tok,
            "tok_per_s": wl.batch * len(plan) / (ms / 1e3)}
+    # the decode attention of the last step alone (its lookup as the step wrote it), replayed
+    past, n = plan[-1]
+    F, S, D = st.F, wl.seq_len, wl.head_dim
+    idx = st.idx.clone()
+    parts = []
+    us = graph_replay_us(torch, lambda: parts.append(F.infllm_attend_partial(
+        st.p, st.mem.struct, st.ptr("q", past), S * D, n, past, idx, wl.topk, st.out, wl.chunk * D, st.lse, st.ws)))
+    ab, pb = attention_bytes(wl, [(past, n)], [parts[-1]])
+    res["kernels"] = [hbm_entry("attend_decode_kernel (infllm_attend_partial)", f"{wl.name} step {len(plan) - 1}",
+                                us, ab, traffic="attend_decode", split_partial_bytes=pb, parts=parts[-1])]
+    s_us = graph_replay_us(torch, lambda: F.infllm_score_units(st.p, st.mem.struct, st.ptr("q", past), S * D, n,
+                                                               F.infllm_partition(st.p, past)[1], st.scores, st.ws))
+    res["kernels"].append(hbm_entry("infllm_score_units (query sums + score_kernel)",
+                                    f"{wl.name} step {len(plan) - 1}", s_us,
+                                    score_bytes(wl, F.infllm_partition(st.p, past)[1], n)))
     return res, st
 
 
@@ -382,43 +467,95 @@ def decode_varlen_leg(st, steps, warmup, torch, spacing=6144):
             "us_per_step": ms * 1e3 / T, "tok_per_s": B * T / (ms / 1e3)}
 
 
-def cpu_baseline(synth, n_chunk_samples=128):
-    """The oracle on a bounded sample of the 128K encode: kv head 0 (of 8) with its 4 query heads;
-    all of that head's units are built, and every 2nd chunk is scored, looked up and attended.
-    Extrapolated linearly to all chunks and all kv heads."""
-    from oracle import infllm_oracle as O
+def _ordinal(n):
+    return f"{n}{'nd' if n == 2 else 'rd' if n == 3 else 'th'}"
+
+
+def _oracle_threads():
+    """Host cores this process may run on, and the BLAS threads the oracle's matrix products use."""
+    cores = len(os.sched_getaffinity(0))
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:  # pragma: no cover
-        threads = len(os.sched_getaffinity(0))
-    wl = synth.wl
-    G, S = wl.group, wl.seq_len
-    q = np.stack([synth.q(0, h, 0, S) for h in range(G)])[None]
-    k = synth.k(0, 0, 0, S)[None, None]
-    v = synth.v(0, 0, 0, S)[None, None]
+        blas = None
+    return cores, blas
+
+
+def _oracle_head(wl, synth, b, g, p1):
+    """The oracle over one (sequence, kv head) of a workload: inputs [0, p1) of its G query heads."""
+    from oracle import infllm_oracle as O
+    G = wl.group
+    q = np.stack([synth.q(b, g * G + h, 0, p1) for h in range(G)])[None]
+    k = synth.k(b, g, 0, p1)[None, None]
+    v = synth.v(b, g, 0, p1)[None, None]
     op = O.Params(G, 1, wl.head_dim, wl.n_init, wl.n_local, wl.block_size, wl.n_repr, wl.topk)
-    so = O.StreamOracle(q, k, v, op)
-    plan = wl.step_starts()
+    return O, O.StreamOracle(q, k, v, op), op
+
+
+def _oracle_stream(wl, synth, plan, stride, b=0):
+    """Oracle seconds for one kv head: every unit the plan builds, then every `stride`-th step of the
+    plan scored, looked up and attended.  Returns (unit seconds, step seconds, steps timed, units)."""
+    O, so, op = _oracle_head(wl, synth, b, 0, plan[-1][0] + plan[-1][1])
     last_units = O.partition(plan[-1][0], op).n_units
     t0 = time.time()
     so.group_query_sum(0, 0)
     for u in range(last_units):
         so.repr_offsets(0, 0, u)
     t_units = time.time() - t0
-    stride = max(1, len(plan) // n_chunk_samples)
-    sample = plan[stride - 1::stride]
+    sample = plan[stride - 1::stride] if stride > 1 else plan
     t0 = time.time()
     for past, n in sample:
         so.step(0, past, n)
-    t_chunks = time.time() - t0
-    t_full = wl.n_kv_heads * (t_units + t_chunks * len(plan) / len(sample))
-    return {"value": S / t_full, "unit": "ctx tok/s", "cores": threads, "kind": "oracle",
-            "sample": f"kv head 0 of {wl.n_kv_heads}: all {last_units} units built, {len(sample)} of {len(plan)} "
-                      f"chunks (every {stride}{'nd' if stride == 2 else 'rd' if stride == 3 else 'th'}) scored/selected/attended; "
-                      f"extrapolated x{len(plan) / len(sample):g} "
-                      f"over chunks and x{wl.n_kv_heads} over kv heads",
-            "sample_seconds": t_units + t_chunks}
+    return t_units, time.time() - t0, len(sample), last_units
+
+
+def cpu_baseline(synth, n_chunk_samples=64, extra=True):
+    """The oracle, unchanged, on bounded samples, timed on this host's cores.
+
+    Headline (128K encode): kv head 0 (of 8) with its 4 query heads; all of that head's units are
+    built and every 4th chunk is scored, looked up and attended; extrapolated linearly to all chunks
+    and all kv heads.  With `extra`: the 16 x 128K decode (sequence 0, kv head 0: its 991 units, then
+    every 64th of the 256 steps; per step x16 sequences x8 kv heads) and the 1M encode (kv head 0:
+    all 8,155 units, every 128th chunk; extrapolated over chunks and kv heads)."""
+    from workload import WORKLOADS, Synth
+    cores, blas = _oracle_threads()
+    wl = synth.wl
+    plan = wl.step_starts()
+    stride = max(1, len(plan) // n_chunk_samples)
+    t_units, t_steps, n_s, nu = _oracle_stream(wl, synth, plan, stride)
+    t_full = wl.n_kv_heads * (t_units + t_steps * len(plan) / n_s)
+    out = {"value": wl.seq_len / t_full, "unit": "ctx tok/s", "cores": cores, "blas_threads": blas,
+           "kind": "oracle",
+           "sample": f"kv head 0 of {wl.n_kv_heads}: all {nu} units built, {n_s} of {len(plan)} chunks (every "
+                     f"{_ordinal(stride)}) scored/selected/attended; extrapolated x{len(plan) / n_s:g} over "
+                     f"chunks and x{wl.n_kv_heads} over kv heads",
+           "sample_seconds": t_units + t_steps}
+    if not extra:
+        return out
+    # 16 x 128K decode: oracle microseconds per decode step (16 tokens)
+    wd = WORKLOADS["llama3-8b-decode-16x128k"]
+    sd = Synth(wd, synth.seed)
+    dplan = wd.step_starts()[-wd.decode_steps:]
+    t_u, t_s, n_d, nu_d = _oracle_stream(wd, sd, dplan, 64)
+    per_step = t_s / n_d * wd.batch * wd.n_kv_heads  # the units were built before the steps (prior context)
+    out["decode_16x128k"] = {"us_per_step": per_step * 1e6, "unit": "us per decode step (16 tokens)",
+                             "sample": f"sequence 0, kv head 0: its {nu_d} units built ({t_u:.1f} s, not counted: "
+                                       f"prior context), {n_d} of {len(dplan)} steps timed; x{wd.batch} sequences "
+                                       f"x{wd.n_kv_heads} kv heads",
+                             "sample_seconds": t_u + t_s}
+    # 1M encode, extrapolated from every 128th chunk
+    w1 = WORKLOADS["llama3-8b-1m"]
+    s1 = Synth(w1, synth.seed)
+    p1 = w1.step_starts()
+    t_u, t_s, n_1, nu_1 = _oracle_stream(w1, s1, p1, 128)
+    t1 = w1.n_kv_heads * (t_u + t_s * len(p1) / n_1)
+    out["encode_1m"] = {"value": w1.seq_len / t1, "unit": "ctx tok/s", "extrapolated": True,
+                        "sample": f"kv head 0 of {w1.n_kv_heads}: all {nu_1} units built, {n_1} of {len(p1)} chunks "
+                                  f"(every 128th) scored/selected/attended; extrapolated x{len(p1) / n_1:g} over "
+                                  f"chunks and x{w1.n_kv_heads} over kv heads",
+                        "sample_seconds": t_u + t_s}
+    return out
 
 
 # Memory settings of the paper's studies of them: representative tokens r_k, selected units
@@ -449,8 +586,8 @@ def main():
     ap.add_argument("--steps", type=int, default=5)
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--legs", default="1m,1m-paper,32l-1m,decode,remap,mean,mass",
-                    help="extra legs: comma list of 1m, 1m-paper, 32l-1m, decode, remap, mean, mass (or 'none')")
+    ap.add_argument("--legs", default="32k,1m,1m-paper,32l-1m,decode,remap,mean,mass",
+                    help="extra legs: comma list of 32k, 1m, 1m-paper, 32l-1m, decode, remap, mean, mass (or 'none')")
     ap.add_argument("--sweep", action="store_true",
                     help="only time the 128K stream under the paper's memory settings (r_k, k_m, l_bs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -480,6 +617,7 @@ def main():
     log(f"128K: {main_res['ms_per_step']:.2f} ms/step, {main_res['ctx_tok_per_s'] / 1e6:.2f}M ctx tok/s; "
         f"attention {main_res['attention']['tflops']:.0f} TFLOP/s")
     extra = {}
+    kernels = list(main_res.get("kernels", []))
     legs = [] if args.legs == "none" else [x.strip() for x in args.legs.split(",") if x.strip()]
     if "remap" in legs:
         # the same 128K stream with the positional remap (Llama-3 rotary frequencies), same inputs
@@ -507,10 +645,19 @@ def main():
         log(f"128K with unit mass: {rs['ms_per_step']:.2f} ms/step (+{rs['added_us_per_step']:.1f} us per chunk)")
     del st
     torch.cuda.empty_cache()
+    if "32k" in legs:
+        # the Mistral-7B-shaped 32K stream (k_m 16)
+        r2, _, st2 = encode_leg("mistral7b-32k", args.seed, args.steps, args.warmup, torch)
+        del st2
+        torch.cuda.empty_cache()
+        extra["encode_32k"] = r2
+        log(f"32K: {r2['ms_per_step']:.2f} ms/step, {r2['ctx_tok_per_s'] / 1e6:.2f}M ctx tok/s; "
+            f"attention {r2['attention']['tflops']:.0f} TFLOP/s")
     if "1m" in legs or "1m-paper" in legs or "32l-1m" in legs:
         r1, _, st1 = encode_leg("llama3-8b-1m", args.seed, max(1, min(args.steps, 2)), 1, torch)
         if "1m" in legs:
             extra["encode_1m"] = r1
+            kernels += r1.get("kernels", [])
             log(f"1M: {r1['ms_per_step']:.1f} ms/step, {r1['ctx_tok_per_s'] / 1e6:.2f}M ctx tok/s")
         if "1m-paper" in legs:
             # the paper's settings for its 1,024K run: 2048-token chunks, one representative token
@@ -534,6 +681,7 @@ def main():
     if "decode" in legs:
         rd, st_d = decode_leg(args.seed, max(1, min(args.steps, 3)), 1, torch)
         extra["decode_16x128k"] = rd
+        kernels += rd.get("kernels", [])
         log(f"decode: {rd['us_per_step']:.1f} us/step (16 seqs)")
         rv = decode_varlen_leg(st_d, max(1, min(args.steps, 3)), 1, torch)
         extra["decode_16_varlen"] = rv
@@ -561,9 +709,10 @@ def main():
                    "chunk": 512, "parallelism": "single-gpu"},
         "roofline": {"bound": "mfma", "kernel": "attend_mfma_kernel<128>", "achieved": achieved,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
-                     "traffic": attention_traffic_bytes(), "traffic_unit": "B/launch",
-                     "algorithmic_bytes": att["algorithmic_bytes_per_launch"], "avg_launch_ms": att["avg_ms"],
-                     "launches_per_step": att["launches"]},
+                     "traffic": kernel_traffic_bytes("attend_mfma_llama3-8b-128k"), "traffic_unit": "B/launch",
+                     "algorithmic_bytes": att["algorithmic_bytes_per_launch"],
+                     "split_partial_bytes": att["split_partial_bytes_per_launch"], "avg_launch_ms": att["avg_ms"],
+                     "launches_per_step": att["launches"], "kernels": kernels},
         "extra": extra,
     }
     peaks = measured_peaks()
