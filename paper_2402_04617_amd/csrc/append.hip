@@ -113,6 +113,35 @@ __device__ __forceinline__ void rotate8(V (&x)[8], int64_t pos, int pair0, const
   }
 }
 
+// Cross-lane moves of a float64 for the scan: DPP (two 32-bit halves) on the
+// vector ALU instead of LDS permutes.  Lanes whose source lies outside the
+// pattern read 0.  CTRL: row_shr:n = 0x110 + n; row_bcast:15 = 0x142.
+template <int CTRL, int ROW_MASK>
+__device__ __forceinline__ double dpp_f64(double x) {
+  const uint64_t u = (uint64_t)__double_as_longlong(x);
+  const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)u, CTRL, ROW_MASK, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(u >> 32), CTRL, ROW_MASK, 0xF, false);
+  return __longlong_as_double((long long)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo));
+}
+// Inclusive sum over lanes [32h, lane] of each 32-lane half h.
+__device__ __forceinline__ double half_wave_scan(double x) {
+  x += dpp_f64<0x111, 0xF>(x);
+  x += dpp_f64<0x112, 0xF>(x);
+  x += dpp_f64<0x114, 0xF>(x);
+  x += dpp_f64<0x118, 0xF>(x);
+  x += dpp_f64<0x142, 0xA>(x);  // rows 1 and 3 add the last lane of rows 0 and 2
+  return x;
+}
+// x of lane l plus x of lane l ^ 32, the same sum in both lanes.
+__device__ __forceinline__ double add_halves(double x) {
+  const uint64_t u = (uint64_t)__double_as_longlong(x);
+  const auto lo = __builtin_amdgcn_permlane32_swap((uint32_t)u, (uint32_t)u, false, false);
+  const auto hi = __builtin_amdgcn_permlane32_swap((uint32_t)(u >> 32), (uint32_t)(u >> 32), false, false);
+  const double a = __longlong_as_double((long long)(((uint64_t)hi[0] << 32) | lo[0]));
+  const double b = __longlong_as_double((long long)(((uint64_t)hi[1] << 32) | lo[1]));
+  return a + b;
+}
+
 // Block roles along the 1-D grid: [unit construction | query sum | scan | copy].
 struct AppendGrid {
   int n_build;          // unit-construction blocks (n_new * batch * Hkv), 0 when not fused
@@ -273,7 +302,9 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
   const int bg = blk / slices;
   const int b = bg / a.n_kv_heads, g = bg - b * a.n_kv_heads;
   const int64_t past = seq_past(a, b);
-  const int half = threadIdx.x & 1, seg = threadIdx.x >> 1;
+  // lanes [0, 32) of a wave take the slice's first 8 dims, lanes [32, 64) the other
+  // 8, for the same 32 position segments (so a segment scan is a 32-lane scan)
+  const int half = (threadIdx.x >> 5) & 1, seg = (threadIdx.x >> 6) * 32 + (threadIdx.x & 31);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int slice = blk - bg * slices;
   const int d0 = slice * 16 + half * 8;
@@ -378,16 +409,8 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
     // inclusive scan of segment totals across the 32 segments of this half in the wave
     double incl[8];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) incl[e] = tot[e];
-#pragma unroll
-    for (int o = 2; o < 64; o <<= 1) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const double y = __shfl_up(incl[e], o);
-        if (lane >= o) incl[e] += y;
-      }
-    }
-    if (lane >= 62) {
+    for (int e = 0; e < 8; ++e) incl[e] = half_wave_scan(tot[e]);
+    if ((lane & 31) == 31) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) wave_tot[wave][half][e] = incl[e];
     }
@@ -434,7 +457,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
       for (int s = 0; s < kSeg; ++s) {
         const int i = i0 + s;
         const int64_t t = past + i - a.n_local;
-        part[s] += __shfl_xor(part[s], 1);  // the two 8-dim halves of the slice
+        part[s] = add_halves(part[s]);  // the two 8-dim halves of the slice
         if (i < a.n_q && t >= a.n_init && half == 0)
           a.rpart[((int64_t)bg * slices + slice) * a.ring + (int)(t % a.ring)] = part[s];
       }
@@ -479,7 +502,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
 #pragma unroll
         for (int e = 0; e < 4; ++e)
           p += (double)kt[2 * e] * (hp[s][e].x - hq[s][e].x) + (double)kt[2 * e + 1] * (hp[s][e].y - hq[s][e].y);
-        p += __shfl_xor(p, 1);  // the two 8-dim halves of the slice
+        p = add_halves(p);  // the two 8-dim halves of the slice
         if (act && half == 0) a.rpart[((int64_t)bg * slices + slice) * a.ring + (int)(t % a.ring)] = p;
       }
     }
@@ -488,11 +511,11 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
     // plain query sum of the chunk: over the 32 segments of this half in the
     // wave, then over the waves
 #pragma unroll
-    for (int o = 2; o < 64; o <<= 1) {
+    for (int o = 1; o < 32; o <<= 1) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) raw_acc[e] += __shfl_xor(raw_acc[e], o);
     }
-    if (lane < 2) {
+    if ((lane & 31) == 0) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) wave_raw[wave][half][e] = raw_acc[e];
     }
