@@ -233,6 +233,26 @@ infllm_status infllm_lse_merge(const infllm_params* p, int32_t batch, int32_t n_
                                const void* workspace, size_t workspace_bytes, void* out,
                                int64_t out_head_stride, float* lse, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph capture,
+ * tight serving loops, harnesses that forbid hipMalloc): infllm_chunk_attend with
+ * no workspace argument.  The split-key partials go to a device array the library
+ * owns, INFLLM_NOALLOC_SCRATCH_BYTES (32 MiB) on every GPU it runs on, held from
+ * the library's load until the process ends; nothing is allocated or freed by the
+ * call.  The part count is chosen to fit that array: E_WORKSPACE when even the
+ * fewest parts the call needs do not fit (batch*Hq*n_q rows of D*2 + 8 bytes per
+ * part for bf16, (D + 1)*4 for float32; two parts whenever the positional remap
+ * attends I or a unit).  All calls on one GPU share the array and every call
+ * rewrites what it reads of it (nothing in it needs clearing), so such calls that
+ * overlap on one GPU (different streams, no ordering between them) race.
+ * E_DEVICE if the array's address cannot be looked up on the current device.
+ * Otherwise as infllm_chunk_attend, whose results it reproduces when both use the
+ * same number of key parts. */
+#define INFLLM_NOALLOC_SCRATCH_BYTES (32u << 20)
+infllm_status infllm_chunk_attend_noalloc(const infllm_params* p, const infllm_memory* m, const void* q,
+                                          int64_t q_head_stride, int32_t n_q, int64_t past_len,
+                                          const int32_t* idx, int32_t k, void* out, int64_t out_head_stride,
+                                          float* lse, void* stream);
+
 /* Attention mass of the looked-up units and the frequency score of the cache
  * policy (Section 3.2, "Cache Management", and the appendix on the cache
  * management strategy: s_b = s_b * d + sum_{j<l_X} sum_{i in b} attention score).

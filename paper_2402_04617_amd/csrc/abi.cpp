@@ -41,6 +41,33 @@ infllm_status check_device() {
   return st == 1 ? INFLLM_OK : INFLLM_E_DEVICE;
 }
 
+// Device scratch of infllm_chunk_attend_noalloc: a file-scope array that every GPU
+// the library runs on holds from module load until the process ends, in place of a
+// caller workspace.  Host code never passes the array's name (a host-side stand-in)
+// to a kernel: on first use on a device, with that device current, its device
+// address is looked up once and kept per device.
+constexpr size_t kScratchBytes = (size_t)INFLLM_NOALLOC_SCRATCH_BYTES;
+__device__ __align__(256) unsigned char scratch[kScratchBytes];
+std::atomic<void*> g_scratch_ptr[kMaxDevices];
+
+// Device address of `scratch` on the current device (nullptr on failure).
+void* scratch_device_ptr() {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) {
+    (void)hipGetLastError();
+    return nullptr;
+  }
+  void* ptr = g_scratch_ptr[dev].load(std::memory_order_acquire);
+  if (ptr == nullptr) {
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) {
+      (void)hipGetLastError();
+      return nullptr;
+    }
+    g_scratch_ptr[dev].store(ptr, std::memory_order_release);
+  }
+  return ptr;
+}
+
 bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 int esize(const infllm_params* p) { return p->dtype == INFLLM_BF16 ? 2 : 4; }
 
@@ -526,6 +553,26 @@ infllm_status infllm_chunk_attend(const infllm_params* p, const infllm_memory* m
   if ((st = launch_status(launch_attend(a, (hipStream_t)stream))) != INFLLM_OK) return st;
   if (a.parts == 1) return INFLLM_OK;
   MergeArgs ma = merge_args(p, m->batch, n_q, a.parts, workspace, out, out_head_stride, lse);
+  return launch_status(launch_merge(ma, (hipStream_t)stream));
+}
+
+infllm_status infllm_chunk_attend_noalloc(const infllm_params* p, const infllm_memory* m, const void* q,
+                                          int64_t q_head_stride, int32_t n_q, int64_t past_len, const int32_t* idx,
+                                          int32_t k, void* out, int64_t out_head_stride, float* lse, void* stream) {
+  // the scratch array's address on this device (looked up once per device), then
+  // the workspace path of infllm_chunk_attend with the array as the workspace
+  infllm_status st;
+  if ((st = check_device()) != INFLLM_OK) return st;
+  void* ws = scratch_device_ptr();
+  if (ws == nullptr) return INFLLM_E_DEVICE;
+  AttendArgs a;
+  if ((st = prepare_attend(p, m, q, q_head_stride, n_q, past_len, idx, k, out, out_head_stride, lse, ws,
+                           kScratchBytes, &a)) != INFLLM_OK)
+    return st;
+  if (n_q == 0) return INFLLM_OK;
+  if ((st = launch_status(launch_attend(a, (hipStream_t)stream))) != INFLLM_OK) return st;
+  if (a.parts == 1) return INFLLM_OK;
+  MergeArgs ma = merge_args(p, m->batch, n_q, a.parts, ws, out, out_head_stride, lse);
   return launch_status(launch_merge(ma, (hipStream_t)stream));
 }
 

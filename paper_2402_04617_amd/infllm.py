@@ -24,7 +24,8 @@ STATUS = {0: "INFLLM_OK", 1: "INFLLM_E_NULL", 2: "INFLLM_E_SHAPE", 3: "INFLLM_E_
           4: "INFLLM_E_UNSUPPORTED", 5: "INFLLM_E_WORKSPACE", 6: "INFLLM_E_LAUNCH", 7: "INFLLM_E_DEVICE"}
 
 EXPORTS = ["infllm_partition", "infllm_workspace_bytes", "infllm_attend_workspace_bytes", "infllm_append", "infllm_build_units",
-           "infllm_score_units", "infllm_select_topk", "infllm_chunk_attend", "infllm_attend_partial",
+           "infllm_score_units", "infllm_select_topk", "infllm_chunk_attend", "infllm_chunk_attend_noalloc",
+           "infllm_attend_partial",
            "infllm_lse_merge", "infllm_step", "infllm_step_varlen", "infllm_unit_mass", "infllm_status_string"]
 
 
@@ -80,6 +81,7 @@ def lib() -> ctypes.CDLL:
         "infllm_score_units": [P, M, vp, i64, i32, i32, vp, vp, sz, vp],
         "infllm_select_topk": [i32, vp, i32, i32, vp, vp],
         "infllm_chunk_attend": [P, M, vp, i64, i32, i64, vp, i32, vp, i64, vp, vp, sz, vp],
+        "infllm_chunk_attend_noalloc": [P, M, vp, i64, i32, i64, vp, i32, vp, i64, vp, vp],
         "infllm_attend_partial": [P, M, vp, i64, i32, i64, vp, i32, vp, i64, vp, vp, sz,
                                   ctypes.POINTER(i32), vp],
         "infllm_lse_merge": [P, i32, i32, i32, vp, sz, vp, i64, vp, vp],
@@ -166,6 +168,13 @@ def infllm_chunk_attend(p, m, q, q_head_stride, n_q, past_len, idx, k, out, out_
     _check("infllm_chunk_attend", lib().infllm_chunk_attend(
         ctypes.byref(p), ctypes.byref(m), _ptr(q), q_head_stride, n_q, past_len, _ptr(idx), k, _ptr(out),
         out_head_stride, _ptr(lse), _ptr(workspace), wb, _stream(stream)))
+
+
+def infllm_chunk_attend_noalloc(p, m, q, q_head_stride, n_q, past_len, idx, k, out, out_head_stride, lse=None,
+                                stream=None):
+    _check("infllm_chunk_attend_noalloc", lib().infllm_chunk_attend_noalloc(
+        ctypes.byref(p), ctypes.byref(m), _ptr(q), q_head_stride, n_q, past_len, _ptr(idx), k, _ptr(out),
+        out_head_stride, _ptr(lse), _stream(stream)))
 
 
 def infllm_attend_partial(p, m, q, q_head_stride, n_q, past_len, idx, k, out, out_head_stride, lse=None,
