@@ -332,8 +332,9 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
   }
 #pragma unroll
   for (int e = 0; e < 8; ++e) carry[e] = base[e];
-  // every thread holds the base before any slot is written (new slots never alias it: ring > n_q)
-  __syncthreads();
+  // (no barrier: the slots this launch writes, positions past .. past + n_q - 1, never
+  // alias slot past - 1 or the slots of the tokens t = p - l_L it reads, since the host
+  // checked ring >= l_L + n_q; so the base loads stay in flight with the tile's loads)
 
   constexpr int GQ = GT > 0 ? GT : 1;  // query pieces loaded up front per position
   for (int t0 = 0; t0 < a.n_q; t0 += kTile) {
@@ -347,6 +348,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
     Raw8<T> qr[kSeg][GQ];
     double2 ht[kSeg][4];
     Raw8<T> kr[kSeg];
+    int slot_t[kSeg];  // ring slot of token t = p - l_L
 #pragma unroll
     for (int s = 0; s < kSeg; ++s) {
       const int ic = min(i0 + s, a.n_q - 1);
@@ -359,6 +361,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
         const int ic = min(i0 + s, a.n_q - 1);
         const int sp = slot0 + ic - (slot0 + ic >= a.ring ? a.ring : 0);
         const int st = sp - a.n_local + (sp < a.n_local ? a.ring : 0);  // n_local < ring
+        slot_t[s] = st;
         const double2* src = (const double2*)(ring + (int64_t)st * D);
 #pragma unroll
         for (int e = 0; e < 4; ++e) ht[s][e] = src[e];
@@ -459,7 +462,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
         const int64_t t = past + i - a.n_local;
         part[s] = add_halves(part[s]);  // the two 8-dim halves of the slice
         if (i < a.n_q && t >= a.n_init && half == 0)
-          a.rpart[((int64_t)bg * slices + slice) * a.ring + (int)(t % a.ring)] = part[s];
+          a.rpart[((int64_t)bg * slices + slice) * a.ring + slot_t[s]] = part[s];
       }
     }
 #pragma unroll

@@ -118,7 +118,10 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
   const int G = a.n_q_heads / a.n_kv_heads;
   const int R = G * a.geom.n_q;
   const int n_row_tiles = (R + ROWS_WG - 1) / ROWS_WG;
-  const int L = xcd_logical_block(blockIdx.x, gridDim.x);
+  // XCD-aware order, reversed so that the workgroups dispatched first are those
+  // with the most work: the last key part (it holds the causal diagonal of X) and
+  // the last row tiles (their queries see the most of X)
+  const int L = (int)gridDim.x - 1 - xcd_logical_block(blockIdx.x, gridDim.x);
   const int rt = L % n_row_tiles;
   const int tmp = L / n_row_tiles;
   const int part = tmp % a.parts;
@@ -398,15 +401,24 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
         for (int j4 = 0; j4 < 4; ++j4)
           kv[j4][kb] = *(const uint32_t*)&sm.kvalid[kbuf][32 * kb + 8 * j4 + 4 * gsel];
     }
+    // one uniform branch for the tile, none per element
+    if (has_invalid) {
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+      for (int kb = 0; kb < 2; ++kb)
 #pragma unroll
-      for (int j = 0; j < 16; ++j) {
-        const int c = 32 * kb + 8 * (j >> 2) + (j & 3);
-        bool vis = c <= lim;
-        if (has_invalid) vis = vis && ((kv[j >> 2][kb] >> (8 * (j & 3))) & 0xFFu) != 0;
-        sacc[kb][j] = vis ? sacc[kb][j] : -__builtin_inff();
-      }
+        for (int j = 0; j < 16; ++j) {
+          const int c = 32 * kb + 8 * (j >> 2) + (j & 3);
+          const bool vis = c <= lim && ((kv[j >> 2][kb] >> (8 * (j & 3))) & 0xFFu) != 0;
+          sacc[kb][j] = vis ? sacc[kb][j] : -__builtin_inff();
+        }
+    } else {
+#pragma unroll
+      for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+        for (int j = 0; j < 16; ++j) {
+          const int c = 32 * kb + 8 * (j >> 2) + (j & 3);
+          sacc[kb][j] = c <= lim ? sacc[kb][j] : -__builtin_inff();
+        }
     }
   };
   // Row max of the tile in the exp2 domain (both lane halves combined).
@@ -613,14 +625,23 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
           if (j + 1 < 4) va[db] = vfrag(db, j + 1);
         }
         if constexpr (MASK) {
-          // 8 of the 32 scores of tile t+1: elements [8j, 8j+8)
+          // 8 of the 32 scores of tile t+1: elements [8j, 8j+8); one uniform branch
+          // per step, none per element
+          if (has_invalid) {
 #pragma unroll
-          for (int i = 0; i < 8; ++i) {
-            const int e = 8 * j + i, kb = e >> 4, jj = e & 15;
-            const int c = 32 * kb + 8 * (jj >> 2) + (jj & 3);
-            bool vis = c <= lim;
-            if (has_invalid) vis = vis && ((kv[jj >> 2][kb] >> (8 * (jj & 3))) & 0xFFu) != 0;
-            nxt[kb][jj] = vis ? nxt[kb][jj] : -__builtin_inff();
+            for (int i = 0; i < 8; ++i) {
+              const int e = 8 * j + i, kb = e >> 4, jj = e & 15;
+              const int c = 32 * kb + 8 * (jj >> 2) + (jj & 3);
+              const bool vis = c <= lim && ((kv[jj >> 2][kb] >> (8 * (jj & 3))) & 0xFFu) != 0;
+              nxt[kb][jj] = vis ? nxt[kb][jj] : -__builtin_inff();
+            }
+          } else {
+#pragma unroll
+            for (int i = 0; i < 8; ++i) {
+              const int e = 8 * j + i, kb = e >> 4, jj = e & 15;
+              const int c = 32 * kb + 8 * (jj >> 2) + (jj & 3);
+              nxt[kb][jj] = c <= lim ? nxt[kb][jj] : -__builtin_inff();
+            }
           }
         }
         // P(t+1), keys [0, 32): elements [4j, 4j+4) (masked by step j/2 <= j)
