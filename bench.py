@@ -316,10 +316,10 @@ def score_bytes(wl, n_units, n):
 def append_bytes(wl, n):
     """infllm_append of n positions: queries and the chunk's K/V read, K/V stored, the float64 running
     sum written for each new position and read for each token leaving the window, that token's key
-    read, its partial representative scores (D/16 float64 per token) written."""
+    read, its partial representative scores (D/8 float64 per token) written."""
     B, Hq, Hkv, D = wl.batch, wl.n_q_heads, wl.n_kv_heads, wl.head_dim
     return (B * Hq * n * D * 2 + 2 * 2 * B * Hkv * n * D * 2 + 2 * B * Hkv * n * D * 8 + B * Hkv * n * D * 2
-            + B * Hkv * n * (D // 16) * 8)
+            + B * Hkv * n * (D // 8) * 8)
 
 
 def encode_leg(name, seed, steps, warmup, torch, want_roofline=True, remap=False, inputs=None, mean_repr=False,

@@ -103,8 +103,8 @@ typedef struct {
  *   qprefix    [batch][Hkv][ring][D] float64 ring: slot (t mod ring) holds
  *              sum_{p <= t} sum_{h in group} q^h_p, the running sum of the group's
  *              queries.  Written and read by infllm_append.
- *   rpart      [batch][Hkv][D/16][ring] float64 ring: slot (t mod ring) of row s
- *              holds sum over dims d in [16s, 16s+16) of k_t[d] * W_t[d], where
+ *   rpart      [batch][Hkv][D/8][ring] float64 ring: slot (t mod ring) of row s
+ *              holds sum over dims d in [8s, 8s+8) of k_t[d] * W_t[d], where
  *              W_t = qprefix(t + l_L) - qprefix(t) is the window query sum of token
  *              t; summed over s it is l_L*G times the representative score r_t of
  *              Section 3.2.  Written by infllm_append once position t + l_L is

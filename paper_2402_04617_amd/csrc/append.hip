@@ -9,7 +9,7 @@
 // Pi_p = sum_{p'<=p} sum_h q^h_{p'} kept per position, W_t is one difference of
 // two ring slots, so its cost does not grow with l_L; float64 keeps the
 // difference of two large running sums exact to ~1e-16.  The scan forms it as
-// soon as position p = t + l_L arrives and stores k_t . W_t per 16-dim slice
+// soon as position p = t + l_L arrives and stores k_t . W_t per 8-dim slice
 // (rpart), which is all that unit construction reads later.
 //
 // In the whole-step path the same launch also carries the unit-construction
@@ -18,14 +18,16 @@
 // overwrite when the ring is large enough (checked on the host), so the two
 // latency-bound jobs overlap instead of running back to back.
 //
-// Scan block: one (sequence*kv head, 16-dim slice); 256 threads = 128 position
-// segments x 2 halves of 8 dims.  Each thread first issues every load of its
+// Scan block: one (sequence*kv head, 8-dim slice); 256 threads = 128 position
+// segments x 2 halves of 4 dims.  Each thread first issues every load of its
 // segment (kSeg positions: the group's query pieces, and in the streaming case
 // the running sums and keys of the tokens t = p - l_L), then sums in float64; a
-// wave-level shuffle scan and an LDS pass over the 4 waves give the segment
-// offsets, and each thread writes its kSeg ring rows.  Chunks of a few positions
-// (decoding) use thin scan blocks instead, one thread per (sequence*kv head,
-// dim).  Copy blocks likewise load all their vectors before storing any.
+// DPP scan over each 32-lane half of a wave and an LDS pass over the 4 waves give
+// the segment offsets, and each thread writes its kSeg ring rows.  (Per thread the
+// float64 work is a long dependent chain; 4 dims per thread keeps it short enough
+// that the scan ends with the copy and unit-construction blocks.)  Chunks of a few
+// positions (decoding) use thin scan blocks instead, one thread per
+// (sequence*kv head, dim).  Copy blocks load all their vectors before storing any.
 #include <cstring>
 
 #include "qsum.h"
@@ -41,38 +43,7 @@ constexpr int kSeg = 4;                        // positions per thread per tile
 constexpr int kTile = (kThreads / 2) * kSeg;   // positions per scan tile
 constexpr int kCopyPerThread = 4;              // 16-byte vectors per thread in copy blocks
 constexpr int kThinMaxQ = 8;                   // chunks this short take the one-thread-per-dim scan
-
-// Eight consecutive elements as raw 16-byte words (one for bf16, two for float32).
-template <typename T>
-struct Raw8 {
-  uint4 w[sizeof(T) / 2];
-};
-template <typename T>
-__device__ __forceinline__ Raw8<T> load_raw8(const T* p) {
-  Raw8<T> r;
-#pragma unroll
-  for (int j = 0; j < (int)(sizeof(T) / 2); ++j) r.w[j] = ((const uint4*)p)[j];
-  return r;
-}
-template <typename T>
-__device__ __forceinline__ void raw8_to_float(const Raw8<T>& r, float* out) {
-  if constexpr (sizeof(T) == 2) {
-    const uint32_t w[4] = {r.w[0].x, r.w[0].y, r.w[0].z, r.w[0].w};
-#pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      out[2 * e] = __uint_as_float(w[e] << 16);
-      out[2 * e + 1] = __uint_as_float(w[e] & 0xFFFF0000u);
-    }
-  } else {
-#pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      out[4 * j + 0] = __uint_as_float(r.w[j].x);
-      out[4 * j + 1] = __uint_as_float(r.w[j].y);
-      out[4 * j + 2] = __uint_as_float(r.w[j].z);
-      out[4 * j + 3] = __uint_as_float(r.w[j].w);
-    }
-  }
-}
+constexpr int kDPT = kRpartDims / 2;           // dimensions per scan thread (a slice's two halves)
 
 // R(pos) applied to one 16-byte vector of consecutive dimensions starting at the
 // even dimension 2*pair0 (positional remap): 4 bf16 pairs or 2 float32 pairs.
@@ -100,11 +71,47 @@ __device__ __forceinline__ uint4 rotate_vec(const uint4 w, int64_t pos, int pair
   return make_uint4(out[0], out[1], out[2], out[3]);
 }
 
-// R(pos) on 8 consecutive dimensions (4 pairs from pair0) held as float64 or float.
-template <typename V>
-__device__ __forceinline__ void rotate8(V (&x)[8], int64_t pos, int pair0, const RopeArgs& r) {
+// kDPT consecutive elements of a query or key row as raw words (kDPT*sizeof(T)
+// bytes: one 8-byte load for bf16, one 16-byte load for float32).
+template <typename T>
+struct RawD {
+  uint32_t w[kDPT * sizeof(T) / 4];
+};
+template <typename T>
+__device__ __forceinline__ RawD<T> load_rawd(const T* p) {
+  RawD<T> r;
+  if constexpr (kDPT * sizeof(T) == 8) {
+    const uint2 v = *(const uint2*)p;
+    r.w[0] = v.x;
+    r.w[1] = v.y;
+  } else {
+    static_assert(kDPT * sizeof(T) == 16, "one 8- or 16-byte piece per thread");
+    const uint4 v = *(const uint4*)p;
+    r.w[0] = v.x;
+    r.w[1] = v.y;
+    r.w[2] = v.z;
+    r.w[3] = v.w;
+  }
+  return r;
+}
+template <typename T>
+__device__ __forceinline__ void rawd_to_float(const RawD<T>& r, float* out) {
+  if constexpr (sizeof(T) == 2) {
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+    for (int e = 0; e < kDPT / 2; ++e) {
+      out[2 * e] = __uint_as_float(r.w[e] << 16);
+      out[2 * e + 1] = __uint_as_float(r.w[e] & 0xFFFF0000u);
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < kDPT; ++e) out[e] = __uint_as_float(r.w[e]);
+  }
+}
+// R(pos) on kDPT consecutive dimensions (kDPT/2 pairs from pair0), float64 or float.
+template <typename V>
+__device__ __forceinline__ void rotate_d(V (&x)[kDPT], int64_t pos, int pair0, const RopeArgs& r) {
+#pragma unroll
+  for (int j = 0; j < kDPT / 2; ++j) {
     float c, sn;
     rope_cos_sin(r, pos, pair0 + j, c, sn);
     const V x0 = x[2 * j], x1 = x[2 * j + 1];
@@ -285,58 +292,60 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
         if (ROPE) k = rot_lane(k, t);
         double part = k * (run - h);
 #pragma unroll
-        for (int o = 1; o < 16; o <<= 1) part += __shfl_xor(part, o);
-        if ((d & 15) == 0) a.rpart[((int64_t)bg * (D / 16) + d / 16) * a.ring + (int)(t % a.ring)] = part;
+        for (int o = 1; o < kRpartDims; o <<= 1) part += __shfl_xor(part, o);
+        if ((d % kRpartDims) == 0)
+          a.rpart[((int64_t)bg * (D / kRpartDims) + d / kRpartDims) * a.ring + (int)(t % a.ring)] = part;
       }
     }
     if (qbar != nullptr) qbar[(int64_t)bg * D + d] = ROPE ? raw_tot : (float)(run - base);
     return;
   }
 
-  // ---- scan role.  The D/16 slice blocks of one (sequence, kv head) read 32-byte
-  // pieces of the same 256-byte query and key rows: they are placed on one XCD
-  // (blocks whose ids agree modulo the XCD count share one), so that its L2
-  // fetches each row from HBM once instead of once per slice.
-  const int slices = D / 16;
+  // ---- scan role.  The slice blocks of one (sequence, kv head) read pieces of
+  // the same 256-byte query and key rows: they are placed on one XCD (blocks whose
+  // ids agree modulo the XCD count share one), so that its L2 fetches each row from
+  // HBM once instead of once per slice.
+  const int slices = D / kRpartDims;
   if (grid.n_scan % kNumXcd == 0) blk = xcd_logical_block(blk, grid.n_scan);
   const int bg = blk / slices;
   const int b = bg / a.n_kv_heads, g = bg - b * a.n_kv_heads;
   const int64_t past = seq_past(a, b);
-  // lanes [0, 32) of a wave take the slice's first 8 dims, lanes [32, 64) the other
-  // 8, for the same 32 position segments (so a segment scan is a 32-lane scan)
+  // lanes [0, 32) of a wave take the slice's first kDPT dims, lanes [32, 64) the
+  // other kDPT, for the same 32 position segments (a segment scan is a 32-lane scan)
   const int half = (threadIdx.x >> 5) & 1, seg = (threadIdx.x >> 6) * 32 + (threadIdx.x & 31);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int slice = blk - bg * slices;
-  const int d0 = slice * 16 + half * 8;
+  const int d0 = slice * kRpartDims + half * kDPT;
   const int G = GT > 0 ? GT : a.n_q_heads / a.n_kv_heads;
   const T* qb = (const T*)a.q + (int64_t)(b * a.n_q_heads + g * G) * a.q_head_stride + d0;
   double* ring = a.qprefix + (int64_t)bg * a.ring * D + d0;
 
-  __shared__ double wave_tot[kWaves][2][8];
-  __shared__ float wave_raw[kWaves][2][8];
+  __shared__ double wave_tot[kWaves][2][kDPT];
+  __shared__ float wave_raw[kWaves][2][kDPT];
   // stored keys as given (unrotated); under the remap each is turned to its own
   // position here in float32, never through the bf16-rounded k_rot copy
   const T* kread = (const T*)a.k_store;
-  float raw_acc[8];  // unrotated query sum of this thread's positions (the chunk total feeds scoring)
+  float raw_acc[kDPT];  // unrotated query sum of this thread's positions (the chunk total feeds scoring)
 #pragma unroll
-  for (int e = 0; e < 8; ++e) raw_acc[e] = 0.f;
+  for (int e = 0; e < kDPT; ++e) raw_acc[e] = 0.f;
   const int slot0 = (int)(past % a.ring);  // ring > n_q: slot0 + i wraps at most once
-  double base[8], carry[8];
+  double base[kDPT], carry[kDPT];
   if (past > 0) {
     const double* src = ring + (int64_t)(slot0 == 0 ? a.ring - 1 : slot0 - 1) * D;
 #pragma unroll
-    for (int e = 0; e < 8; ++e) base[e] = src[e];
+    for (int e = 0; e < kDPT; ++e) base[e] = src[e];
   } else {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) base[e] = 0.0;
+    for (int e = 0; e < kDPT; ++e) base[e] = 0.0;
   }
 #pragma unroll
-  for (int e = 0; e < 8; ++e) carry[e] = base[e];
+  for (int e = 0; e < kDPT; ++e) carry[e] = base[e];
   // (no barrier: the slots this launch writes, positions past .. past + n_q - 1, never
   // alias slot past - 1 or the slots of the tokens t = p - l_L it reads, since the host
   // checked ring >= l_L + n_q; so the base loads stay in flight with the tile's loads)
 
   constexpr int GQ = GT > 0 ? GT : 1;  // query pieces loaded up front per position
+  constexpr int NP = kDPT / 2;          // dimension pairs (double2) per thread
   for (int t0 = 0; t0 < a.n_q; t0 += kTile) {
     const int i0 = t0 + seg * kSeg;
     // When every token t = p - l_L of this tile precedes the chunk (l_L >= the
@@ -345,15 +354,15 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
     // the new running sum is written.  Loads use clamped indices (the values of
     // inactive positions are never used).
     const bool early = t0 + kTile <= a.n_local;
-    Raw8<T> qr[kSeg][GQ];
-    double2 ht[kSeg][4];
-    Raw8<T> kr[kSeg];
+    RawD<T> qr[kSeg][GQ];
+    double2 ht[kSeg][NP];
+    RawD<T> kr[kSeg];
     int slot_t[kSeg];  // ring slot of token t = p - l_L
 #pragma unroll
     for (int s = 0; s < kSeg; ++s) {
       const int ic = min(i0 + s, a.n_q - 1);
 #pragma unroll
-      for (int h = 0; h < GQ; ++h) qr[s][h] = load_raw8<T>(qb + h * a.q_head_stride + (int64_t)ic * D);
+      for (int h = 0; h < GQ; ++h) qr[s][h] = load_rawd<T>(qb + h * a.q_head_stride + (int64_t)ic * D);
     }
     if (early) {
 #pragma unroll
@@ -364,70 +373,70 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
         slot_t[s] = st;
         const double2* src = (const double2*)(ring + (int64_t)st * D);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) ht[s][e] = src[e];
+        for (int e = 0; e < NP; ++e) ht[s][e] = src[e];
         int64_t tk = past + ic - a.n_local;
         tk = tk < 0 ? 0 : tk;
-        kr[s] = load_raw8<T>(kread + ((int64_t)bg * a.capacity + tk) * D + d0);
+        kr[s] = load_rawd<T>(kread + ((int64_t)bg * a.capacity + tk) * D + d0);
       }
     }
-    double run[kSeg][8];
-    double tot[8];
+    double run[kSeg][kDPT];
+    double tot[kDPT];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) tot[e] = 0.0;
+    for (int e = 0; e < kDPT; ++e) tot[e] = 0.0;
 #pragma unroll
     for (int s = 0; s < kSeg; ++s) {
       const int i = min(i0 + s, a.n_q - 1);
       const bool valid = i0 + s < a.n_q;
-      double x[8];
+      double x[kDPT];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) x[e] = 0.0;
+      for (int e = 0; e < kDPT; ++e) x[e] = 0.0;
       if constexpr (GT > 0) {
 #pragma unroll
         for (int h = 0; h < GT; ++h) {
-          float y[8];
-          raw8_to_float<T>(qr[s][h], y);
+          float y[kDPT];
+          rawd_to_float<T>(qr[s][h], y);
 #pragma unroll
-          for (int e = 0; e < 8; ++e) x[e] += (double)y[e];
+          for (int e = 0; e < kDPT; ++e) x[e] += (double)y[e];
         }
       } else {
         for (int h = 0; h < G; ++h) {
-          float y[8];
-          raw8_to_float<T>(h == 0 ? qr[s][0] : load_raw8<T>(qb + h * a.q_head_stride + (int64_t)i * D), y);
+          float y[kDPT];
+          rawd_to_float<T>(h == 0 ? qr[s][0] : load_rawd<T>(qb + h * a.q_head_stride + (int64_t)i * D), y);
 #pragma unroll
-          for (int e = 0; e < 8; ++e) x[e] += (double)y[e];
+          for (int e = 0; e < kDPT; ++e) x[e] += (double)y[e];
         }
       }
       if (ROPE) {
         // the ring sums the queries rotated to their positions; scoring takes the plain sum
 #pragma unroll
-        for (int e = 0; e < 8; ++e) raw_acc[e] += valid ? (float)x[e] : 0.f;
-        rotate8(x, past + i, d0 / 2, a.rope);
+        for (int e = 0; e < kDPT; ++e) raw_acc[e] += valid ? (float)x[e] : 0.f;
+        rotate_d(x, past + i, d0 / 2, a.rope);
       }
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
+      for (int e = 0; e < kDPT; ++e) {
         tot[e] += valid ? x[e] : 0.0;
         run[s][e] = tot[e];
       }
     }
     // inclusive scan of segment totals across the 32 segments of this half in the wave
-    double incl[8];
+    double incl[kDPT];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) incl[e] = half_wave_scan(tot[e]);
+    for (int e = 0; e < kDPT; ++e) incl[e] = half_wave_scan(tot[e]);
     if ((lane & 31) == 31) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) wave_tot[wave][half][e] = incl[e];
+      for (int e = 0; e < kDPT; ++e) wave_tot[wave][half][e] = incl[e];
     }
     __syncthreads();
-    double off[8], tile_tot[8];
+    double off[kDPT], tile_tot[kDPT];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) {
+    for (int e = 0; e < kDPT; ++e) {
       off[e] = incl[e] - tot[e];
       tile_tot[e] = 0.0;
     }
 #pragma unroll
     for (int w = 0; w < kWaves; ++w) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
+      for (int e = 0; e < kDPT; ++e) {
         const double y = wave_tot[w][half][e];
         off[e] += (w < wave) ? y : 0.0;
         tile_tot[e] += y;
@@ -437,16 +446,15 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
 #pragma unroll
     for (int s = 0; s < kSeg; ++s) {
       const int i = i0 + s;
-      float kt[8];
-      raw8_to_float<T>(kr[s], kt);
-      if (ROPE && early) rotate8(kt, past + i - a.n_local, d0 / 2, a.rope);
+      float kt[kDPT];
+      rawd_to_float<T>(kr[s], kt);
+      if (ROPE && early) rotate_d(kt, past + i - a.n_local, d0 / 2, a.rope);
       part[s] = 0.0;
       if (i < a.n_q) {
         const int slot = slot0 + i - (slot0 + i >= a.ring ? a.ring : 0);
-        double* dst = ring + (int64_t)slot * D;
-        double2* d2 = (double2*)dst;
+        double2* d2 = (double2*)(ring + (int64_t)slot * D);
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
+        for (int e = 0; e < NP; ++e) {
           const double2 nv = make_double2(carry[2 * e] + off[2 * e] + run[s][2 * e],
                                           carry[2 * e + 1] + off[2 * e + 1] + run[s][2 * e + 1]);
           d2[e] = nv;
@@ -460,13 +468,13 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
       for (int s = 0; s < kSeg; ++s) {
         const int i = i0 + s;
         const int64_t t = past + i - a.n_local;
-        part[s] = add_halves(part[s]);  // the two 8-dim halves of the slice
+        part[s] = add_halves(part[s]);  // the two halves of the slice
         if (i < a.n_q && t >= a.n_init && half == 0)
           a.rpart[((int64_t)bg * slices + slice) * a.ring + slot_t[s]] = part[s];
       }
     }
 #pragma unroll
-    for (int e = 0; e < 8; ++e) carry[e] += tile_tot[e];
+    for (int e = 0; e < kDPT; ++e) carry[e] += tile_tot[e];
     __syncthreads();
 
     // Otherwise the partial representative scores of the tokens t = p - l_L
@@ -475,8 +483,9 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
     // checked that the ring still holds slot t).  The key of a token inside the
     // chunk comes from k_src.
     if (!early) {
-      double2 hp[kSeg][4], hq[kSeg][4];
-      Raw8<T> kk[kSeg];
+      double2 hp[kSeg][NP], hq[kSeg][NP];
+      RawD<T> kk[kSeg];
+      int st_t[kSeg];
 #pragma unroll
       for (int s = 0; s < kSeg; ++s) {
         const int ic = min(i0 + s, a.n_q - 1);
@@ -484,29 +493,30 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
         t = t < 0 ? 0 : t;
         const int sp = slot0 + ic - (slot0 + ic >= a.ring ? a.ring : 0);
         const int st = sp - a.n_local + (sp < a.n_local ? a.ring : 0);  // n_local < ring
+        st_t[s] = st;
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
+        for (int e = 0; e < NP; ++e) {
           hp[s][e] = ((const double2*)(ring + (int64_t)sp * D))[e];
           hq[s][e] = ((const double2*)(ring + (int64_t)st * D))[e];
         }
         kk[s] = t >= past
-                    ? load_raw8<T>((const T*)a.k_src + (int64_t)bg * a.kv_head_stride + (t - past) * D + d0)
-                    : load_raw8<T>(kread + ((int64_t)bg * a.capacity + t) * D + d0);
+                    ? load_rawd<T>((const T*)a.k_src + (int64_t)bg * a.kv_head_stride + (t - past) * D + d0)
+                    : load_rawd<T>(kread + ((int64_t)bg * a.capacity + t) * D + d0);
       }
 #pragma unroll
       for (int s = 0; s < kSeg; ++s) {
         const int i = i0 + s;
         const int64_t t = past + i - a.n_local;
         const bool act = i < a.n_q && t >= a.n_init;
-        float kt[8];
-        raw8_to_float<T>(kk[s], kt);
-        if (ROPE) rotate8(kt, t, d0 / 2, a.rope);  // the key at its own position, float32
+        float kt[kDPT];
+        rawd_to_float<T>(kk[s], kt);
+        if (ROPE) rotate_d(kt, t, d0 / 2, a.rope);  // the key at its own position, float32
         double p = 0.0;
 #pragma unroll
-        for (int e = 0; e < 4; ++e)
+        for (int e = 0; e < NP; ++e)
           p += (double)kt[2 * e] * (hp[s][e].x - hq[s][e].x) + (double)kt[2 * e + 1] * (hp[s][e].y - hq[s][e].y);
-        p = add_halves(p);  // the two 8-dim halves of the slice
-        if (act && half == 0) a.rpart[((int64_t)bg * slices + slice) * a.ring + (int)(t % a.ring)] = p;
+        p = add_halves(p);  // the two halves of the slice
+        if (act && half == 0) a.rpart[((int64_t)bg * slices + slice) * a.ring + st_t[s]] = p;
       }
     }
   }
@@ -516,16 +526,16 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
 #pragma unroll
     for (int o = 1; o < 32; o <<= 1) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) raw_acc[e] += __shfl_xor(raw_acc[e], o);
+      for (int e = 0; e < kDPT; ++e) raw_acc[e] += __shfl_xor(raw_acc[e], o);
     }
     if ((lane & 31) == 0) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) wave_raw[wave][half][e] = raw_acc[e];
+      for (int e = 0; e < kDPT; ++e) wave_raw[wave][half][e] = raw_acc[e];
     }
     __syncthreads();
     if (seg == 0) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
+      for (int e = 0; e < kDPT; ++e) {
         float t = 0.f;
 #pragma unroll
         for (int w = 0; w < kWaves; ++w) t += wave_raw[w][half][e];
@@ -534,7 +544,7 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
     }
   } else if (qbar != nullptr && seg == 0) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) qbar[(int64_t)bg * D + d0 + e] = (float)(carry[e] - base[e]);
+    for (int e = 0; e < kDPT; ++e) qbar[(int64_t)bg * D + d0 + e] = (float)(carry[e] - base[e]);
   }
 }
 
@@ -586,7 +596,7 @@ hipError_t launch_append(const AppendArgs& a, hipStream_t s, float* qbar, const 
   g.n_qsum = (a.mean_repr && qbar != nullptr && a.n_q > 0) ? g.qsum_parts * a.batch * a.n_kv_heads : 0;
   g.n_scan = (a.n_q <= 0 || a.mean_repr) ? 0
              : g.thin ? (a.batch * a.n_kv_heads * a.head_dim + kThreads - 1) / kThreads
-                      : a.batch * a.n_kv_heads * (a.head_dim / 16);
+                      : a.batch * a.n_kv_heads * (a.head_dim / kRpartDims);
   g.n_copy_per_head = 0;
   if (a.k_src != nullptr && a.n_q > 0) {
     const int vec_per_head = a.n_q * a.head_dim / (16 / esize);

@@ -78,6 +78,7 @@ template <int D>
 __device__ __forceinline__ int tile_off(int r, int g) { return r * D + 8 * (g ^ swz<D>(r)); }
 
 constexpr int NBUF = 3;         // K and V tile buffers
+constexpr int kMaskCost = 6;  // cost of a masked tile, in quarters of a plain tile (measured ~1.5x)
 constexpr int kRunTable = 1024;  // run starts kept in LDS for the part's tiles
 constexpr int kSelLds = 1024;    // lookup entries kept in LDS
 
@@ -150,10 +151,21 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
     rpart = part - parts_mem;
     rparts = a.parts - parts_mem;
   }
-  const int per_part = (rt1 - rt0 + rparts - 1) / rparts;
-  const int t_begin = rt0 + rpart * per_part;
-  int t_end = min(rt1, t_begin + per_part);
+  // The parts split the range by cost rather than by tile count: a tile holding
+  // current-token keys (the causal diagonal, masked) costs kMaskCost/4 of a plain
+  // tile, so the part that takes the diagonal takes fewer tiles and all parts end
+  // together.
   const int v_x0 = geo.n_virtual - geo.n_q;  // first current-token key
+  auto part_bound = [&](int pp) -> int {  // first tile of part pp of rparts
+    const int a_x = min(max(v_x0 / KB, rt0), rt1);
+    const int64_t c_plain = 4LL * (a_x - rt0);
+    const int64_t c_all = c_plain + (int64_t)kMaskCost * (rt1 - a_x);
+    const int64_t c = c_all * pp / rparts;
+    if (c <= c_plain) return rt0 + (int)((c + 3) / 4);
+    return a_x + (int)((c - c_plain + kMaskCost - 1) / kMaskCost);
+  };
+  const int t_begin = part_bound(rpart);
+  int t_end = part_bound(rpart + 1);
   {
     const int i_max = (min(R, (rt + 1) * ROWS_WG) - 1) / G;
     t_end = min(t_end, (v_x0 + i_max) / KB + 1);  // tiles past this are fully causal-masked

@@ -43,6 +43,10 @@ __host__ __device__ inline StepGeom seq_geom(const StepGeom& base, int n_local, 
   return g;
 }
 
+// Width of the dimension slices whose partial representative scores the append
+// stores (rpart holds D / kRpartDims float64 values per token).
+constexpr int kRpartDims = 8;
+
 struct AppendArgs {
   int batch, n_q_heads, n_kv_heads, head_dim, n_q, ring, n_init, n_local;
   int64_t past_len, capacity, q_head_stride, kv_head_stride;
@@ -52,7 +56,7 @@ struct AppendArgs {
   void* k_store;
   void* v_store;
   double* qprefix;
-  double* rpart;  // [B*Hkv][D/16][ring] partial representative scores
+  double* rpart;  // [B*Hkv][D/kRpartDims][ring] partial representative scores
   void* k_rot;    // positional remap: keys rotated to their own positions (same layout as k_store)
   RopeArgs rope;
   VarLen var;      // per-sequence past lengths (var.on), else past_len for all

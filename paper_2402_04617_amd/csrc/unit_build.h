@@ -4,7 +4,7 @@
 //
 // One block per (unit, sequence*kv head).  Token m of the unit has
 // l_L*G*r_m = k_m . W_m, W_m = sum_{h in group} sum_{j=1..l_L} q^h_{m+j}, which the
-// append scan already stored as D/16 float64 partial sums (rpart); here they are
+// append scan already stored as D/kRpartDims float64 partial sums (rpart); here they are
 // added in slice order (one token per thread, all loads in flight together).
 // The r_k tokens of largest r_m (ties: lower position) become R(B): each token's
 // rank under that strict order is counted against all others in LDS, split over
@@ -32,7 +32,7 @@ template <typename T, int D, int NT>
 __device__ __forceinline__ void build_one_unit(const BuildArgs& a, int unit, int unit_local, int bg,
                                                BuildSmem& sm) {
   static_assert(NT % 64 == 0 && NT >= 256 && NT <= 1024, "block size");
-  constexpr int SLICES = D / 16;
+  constexpr int SLICES = D / kRpartDims;
   const int lbs = a.block_size;
   const int tid = threadIdx.x;
   const int64_t m0 = (int64_t)a.n_init + (int64_t)unit * lbs;

@@ -273,7 +273,7 @@ def alloc_memory(p: Params, batch: int, capacity: int, max_units: int, ring: int
     # the query ring and the partial representative scores exist only for representative tokens
     ring_used = not p.mean_repr
     qprefix = torch.zeros((batch, p.n_kv_heads, ring, D), dtype=torch.float64, device=device) if ring_used else None
-    rpart = torch.zeros((batch, p.n_kv_heads, D // 16, ring), dtype=torch.float64, device=device) if ring_used else None
+    rpart = torch.zeros((batch, p.n_kv_heads, D // 8, ring), dtype=torch.float64, device=device) if ring_used else None
     k_rot = torch.zeros_like(k) if p.remap else None
     ptr = lambda t: t.data_ptr() if t is not None else None  # noqa: E731
     st = Memory(batch, capacity, k.data_ptr(), v.data_ptr(), max_units, repr_idx.data_ptr(),
