@@ -16,6 +16,7 @@ CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libinfllm.so")
 PEAKS = os.path.join(PKG, "infllm_peaks")
+TOPK_CMP = os.path.join(PKG, "infllm_topk_compare")
 
 SOURCES = ["abi.cpp", "append.hip", "build_units.hip", "score.hip", "topk.hip", "attend_mfma.hip",
            "attend.hip", "attend_decode.hip", "merge.hip", "mass.hip"]
@@ -64,6 +65,12 @@ def build(verbose: bool = False, jobs: int = 8) -> str:
     if r.returncode != 0:
         raise RuntimeError("hipcc failed on probes/peaks.hip:\n" + r.stdout + r.stderr)
     os.replace(PEAKS + ".tmp", PEAKS)
+    # radix select against a bitonic top-k on the lookup's row shapes (a separate program)
+    cmd = [hipcc, *FLAGS, os.path.join(PKG, "probes", "topk_compare.hip"), "-ldl", "-o", TOPK_CMP + ".tmp"]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("hipcc failed on probes/topk_compare.hip:\n" + r.stdout + r.stderr)
+    os.replace(TOPK_CMP + ".tmp", TOPK_CMP)
     return LIB
 
 
