@@ -42,7 +42,24 @@ CSRC = os.path.join(ROOT, "paper_2402_04617_amd", "csrc")
 COPY_FETCH = 524300.0 / 1048576.0  # FETCH_SIZE KiB per KiB read by the copy
 COPY_WRITE = 1048576.0 / 1048576.0  # WRITE_SIZE KiB per KiB written by the copy
 KERNEL_TRAFFIC = {
-    # key: {"src": {file: sha256}, "fetch_kib": ..., "write_kib": ...} (per launch)
+    # key: {"src": {file: sha256}, "fetch_kib": ..., "write_kib": ...}, per launch (per call for
+    # infllm_score_units: its two kernels), from `rocprofv3 --pmc FETCH_SIZE` and `--pmc WRITE_SIZE`
+    # runs of `bench.py --legs 1m,decode --no-cpu-baseline --steps 1 --warmup 0`, averaged over the
+    # replayed launches the bench line times
+    "attend_mfma_llama3-8b-128k": {"src": {"attend_mfma.hip": "26e9d7020cbcac1d22209ba5fb06ecab6a418e570bf13141adc744bc5703548e", "launch.h": "638c07a8c7872c15bd5db47c90b687ec8a8bfaf72a8ced41300736ca4e66f131"},
+                                   "fetch_kib": 20096.4, "write_kib": 16896.0},
+    "score_llama3-8b-128k": {"src": {"score.hip": "20aebdb59579c60b410d27bf0d8ba4dd4b01d724bb1c79e474f4aa5e8337efd9", "launch.h": "638c07a8c7872c15bd5db47c90b687ec8a8bfaf72a8ced41300736ca4e66f131"},
+                             "fetch_kib": 2074.6 + 2131.5, "write_kib": 32.0 + 31.7},
+    "append_llama3-8b-128k": {"src": {"append.hip": "fe44574fc83ade25154c0c6246e75f45770ecbba5020429ac57eca075d4f3464", "launch.h": "638c07a8c7872c15bd5db47c90b687ec8a8bfaf72a8ced41300736ca4e66f131"},
+                              "fetch_kib": 5738.5, "write_kib": 6659.0},
+    "score_llama3-8b-1m": {"src": {"score.hip": "20aebdb59579c60b410d27bf0d8ba4dd4b01d724bb1c79e474f4aa5e8337efd9", "launch.h": "638c07a8c7872c15bd5db47c90b687ec8a8bfaf72a8ced41300736ca4e66f131"},
+                           "fetch_kib": 2074.5 + 16923.5, "write_kib": 32.0 + 261.8},
+    "append_llama3-8b-1m": {"src": {"append.hip": "fe44574fc83ade25154c0c6246e75f45770ecbba5020429ac57eca075d4f3464", "launch.h": "638c07a8c7872c15bd5db47c90b687ec8a8bfaf72a8ced41300736ca4e66f131"},
+                            "fetch_kib": 5738.5, "write_kib": 6659.0},
+    "attend_decode": {"src": {"attend_decode.hip": "e9c010e0b521a9e279ded2a3f90fe08bc8e43dc66eb5d0d9b4d86bcbdbd07953", "launch.h": "638c07a8c7872c15bd5db47c90b687ec8a8bfaf72a8ced41300736ca4e66f131"},
+                      "fetch_kib": 270890.7, "write_kib": 544.1},
+    "score_decode": {"src": {"score.hip": "20aebdb59579c60b410d27bf0d8ba4dd4b01d724bb1c79e474f4aa5e8337efd9", "launch.h": "638c07a8c7872c15bd5db47c90b687ec8a8bfaf72a8ced41300736ca4e66f131"},
+                     "fetch_kib": 90.5 + 32873.1, "write_kib": 64.0 + 496.0},
 }
 
 
@@ -406,7 +423,7 @@ def decode_leg(seed, steps, warmup, torch):
                                                                F.infllm_partition(st.p, past)[1], st.scores, st.ws))
     res["kernels"].append(hbm_entry("infllm_score_units (query sums + score_kernel)",
                                     f"{wl.name} step {len(plan) - 1}", s_us,
-                                    score_bytes(wl, F.infllm_partition(st.p, past)[1], n)))
+                                    score_bytes(wl, F.infllm_partition(st.p, past)[1], n), traffic="score_decode"))
     return res, st
 
 
