@@ -33,14 +33,28 @@ __device__ __forceinline__ void qsum_block(const T* __restrict__ q, int64_t q_he
   float acc[kVec];
 #pragma unroll
   for (int e = 0; e < kVec; ++e) acc[e] = 0.f;
-#pragma unroll 4
-  for (int r = r0 + rg; r < r1; r += rgroups) {
-    const int hl = r / n_q, i = r - hl * n_q;
-    const T* row = q + (int64_t)(b * n_q_heads + g * G + hl) * q_head_stride + (int64_t)i * head_dim;
-    uint4 raw = *(const uint4*)(row + c * kVec);
-    const T* vals = (const T*)&raw;
+  // kBatch rows per thread are loaded before the first add (one memory round
+  // trip per batch); rows past the part add zeros, so each thread sums its rows
+  // in the same order whatever the batching
+  constexpr int kBatch = 8;
+  for (int r = r0 + rg; r < r1; r += kBatch * rgroups) {
+    uint4 raw[kBatch];
 #pragma unroll
-    for (int e = 0; e < kVec; ++e) acc[e] += Elem<T>::load(vals + e);
+    for (int u = 0; u < kBatch; ++u) {
+      const int rr = r + u * rgroups;
+      raw[u] = make_uint4(0u, 0u, 0u, 0u);
+      if (rr < r1) {
+        const int hl = rr / n_q, i = rr - hl * n_q;
+        const T* row = q + (int64_t)(b * n_q_heads + g * G + hl) * q_head_stride + (int64_t)i * head_dim;
+        raw[u] = *(const uint4*)(row + c * kVec);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < kBatch; ++u) {
+      const T* vals = (const T*)&raw[u];
+#pragma unroll
+      for (int e = 0; e < kVec; ++e) acc[e] += Elem<T>::load(vals + e);
+    }
   }
 #pragma unroll
   for (int e = 0; e < kVec; ++e) sm.red[rg * head_dim + c * kVec + e] = acc[e];

@@ -24,28 +24,35 @@ __global__ void __launch_bounds__(kQsumThreads) qbar_kernel(const T* __restrict_
                 sm);
 }
 
-// grid (ceil(n_units/256), batch*Hkv); one unit per thread.  Every thread
-// issues all D/4 16-byte loads of its unit's key sum first, so that they are in
-// flight while the block forms Qbar (the sum of the query-sum partials, turned
-// by R(l_L) under the positional remap: the memory keys sit at distance l_L from
-// every current token and stay unrotated).  In a variable-length batch sequence
-// b scores its own unit count (units past it are left alone) into rows of stride
-// score_stride.
+// grid (ceil(n_units/64), batch*Hkv); 64 units per block, each unit's D dims
+// split over the block's 4 waves (wave w takes 16-byte cells [w*D/16, (w+1)*D/16)),
+// so that a wave's load of one cell covers 64 consecutive units (1 KB) and a
+// chunk's few hundred units still spread over many compute units.  Every thread
+// issues its D/16 loads first, so that they are in flight while the block forms
+// Qbar (the sum of the query-sum partials, turned by R(l_L) under the positional
+// remap: the memory keys sit at distance l_L from every current token and stay
+// unrotated); the four partial dot products of a unit are added in LDS in a
+// fixed order.  In a variable-length batch sequence b scores its own unit count
+// (units past it are left alone) into rows of stride score_stride.
+constexpr int kScoreUnits = 64;
 template <int D>
 __global__ void __launch_bounds__(256) score_kernel(const ScoreArgs a, int parts) {
-  constexpr int NC = D / 4;
+  constexpr int NC = D / 4;   // 16-byte cells per unit
+  constexpr int CPW = NC / 4;  // cells per wave
   const int bg = blockIdx.y;
   const int n_units = a.var_on ? a.var_units[bg / a.n_kv_heads] : a.n_units;
-  const int u = blockIdx.x * 256 + threadIdx.x;
+  const int lane = threadIdx.x & 63, w = threadIdx.x >> 6;
+  const int u = blockIdx.x * kScoreUnits + lane;
   const bool live = u < n_units;
   // a thread past the last unit reads unit 0 (always present) and stores nothing
   const float4* ks = (const float4*)a.unit_ksum + (int64_t)bg * NC * a.max_units + (live ? u : 0);
-  float4 k4[NC];
+  float4 k4[CPW];
 #pragma unroll
-  for (int c = 0; c < NC; ++c) k4[c] = ks[(int64_t)c * a.max_units];
+  for (int c = 0; c < CPW; ++c) k4[c] = ks[(int64_t)(w * CPW + c) * a.max_units];
 
   const RopeArgs& rope = a.rope;
   __shared__ float qbar[D];
+  __shared__ float part[4][kScoreUnits];
   if (threadIdx.x < D) {
     float s = 0.f;
     for (int p = 0; p < parts; ++p) s += a.qbar_parts[((int64_t)bg * parts + p) * D + threadIdx.x];
@@ -68,19 +75,24 @@ __global__ void __launch_bounds__(256) score_kernel(const ScoreArgs a, int parts
     }
     __syncthreads();
   }
-  if (!live) return;
   float acc = 0.f;
 #pragma unroll
-  for (int c = 0; c < NC; ++c)
-    acc += qbar[4 * c] * k4[c].x + qbar[4 * c + 1] * k4[c].y + qbar[4 * c + 2] * k4[c].z + qbar[4 * c + 3] * k4[c].w;
-  a.scores[(int64_t)bg * (a.var_on ? a.score_stride : n_units) + u] = acc;
+  for (int c = 0; c < CPW; ++c) {
+    const int d = 4 * (w * CPW + c);
+    acc += qbar[d] * k4[c].x + qbar[d + 1] * k4[c].y + qbar[d + 2] * k4[c].z + qbar[d + 3] * k4[c].w;
+  }
+  part[w][lane] = acc;
+  __syncthreads();
+  if (w == 0 && live)
+    a.scores[(int64_t)bg * (a.var_on ? a.score_stride : n_units) + u] =
+        ((part[0][lane] + part[1][lane]) + part[2][lane]) + part[3][lane];
 }
 
 }  // namespace
 
 int score_qbar_parts(int G, int n_q) {
   int rows = G * n_q;
-  int parts = (rows + 255) / 256;
+  int parts = (rows + 127) / 128;  // 128 rows per block: one batch of loads per thread
   return parts < 1 ? 1 : (parts > kMaxQbarParts ? kMaxQbarParts : parts);
 }
 
@@ -100,7 +112,7 @@ hipError_t launch_score(const ScoreArgs& a, hipStream_t s) {
 
 hipError_t launch_score_given_qbar(const ScoreArgs& a, int parts, hipStream_t s) {
   if (a.n_units == 0) return hipSuccess;
-  dim3 g2((a.n_units + 255) / 256, a.batch * a.n_kv_heads);  // n_units: the largest count of the batch
+  dim3 g2((a.n_units + kScoreUnits - 1) / kScoreUnits, a.batch * a.n_kv_heads);  // n_units: the largest of the batch
   if (a.head_dim == 128) hipLaunchKernelGGL(score_kernel<128>, g2, dim3(256), 0, s, a, parts);
   else hipLaunchKernelGGL(score_kernel<64>, g2, dim3(256), 0, s, a, parts);
   return hipGetLastError();
