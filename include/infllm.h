@@ -99,7 +99,9 @@ typedef struct {
  *              representative tokens R(B), ascending.  Written by infllm_build_units.
  *   unit_ksum  [batch][Hkv][D/4][max_units][4] float32: per unit, the sum of its
  *              representative keys, sum_{j in R(B)} k_j, stored four dimensions per
- *              16-byte cell, unit-contiguous (the layout unit scoring streams).
+ *              16-byte cell, unit-contiguous (the layout unit scoring streams; with
+ *              max_units a multiple of 8 and a 128-byte aligned base every row
+ *              starts on a cache line, which scoring reads 64 units at a time).
  *   qprefix    [batch][Hkv][ring][D] float64 ring: slot (t mod ring) holds
  *              sum_{p <= t} sum_{h in group} q^h_p, the running sum of the group's
  *              queries.  Written and read by infllm_append.
