@@ -31,7 +31,8 @@ def rand_inputs(rng, Hq, Hkv, S, D, dtype, qk_std=None, B=1):
 # ------------------------------------------------------------------ a5: top-k
 @pytest.mark.parametrize("n,k", [(0, 4), (1, 4), (5, 5), (7, 3), (100, 32), (987, 32), (8155, 32),
                                  (9000, 64), (300, 1), (50, 0), (4096, 100), (600, 256), (16384, 32),
-                                 (20000, 32), (2000, 300), (3000, 64), (700, 65)])
+                                 (20000, 32), (2000, 300), (3000, 64), (700, 65),
+                                 (2000, 1100), (1100, 1100), (5000, 1024)])  # k above the 512 threads
 def test_select_topk_bit_exact(n, k):
     rng = np.random.default_rng(n * 131 + k)
     rows = 8
@@ -250,6 +251,23 @@ def test_chunk_attend(case):
 def test_chunk_attend_single_part_and_invalid_entries(case):
     _attend_case(case, workspace=False)
     _attend_case(case, invalid_entry=True)
+
+
+# A lookup of more units than the attention keeps in LDS (its first 1,024 entries;
+# later ones are read from global memory) and, as one part, more key tiles than its
+# run-start table holds (1,024 per part): 1,100 units of 64 keys.
+LARGE_LOOKUP = ("bf16", 4, 1, 128, 16, 256, 64, 1100, 71000, 64, 1)
+
+
+@pytest.mark.parametrize("mode", ["one-part", "parts", "skipped-entry", "one-token"])
+def test_chunk_attend_large_lookup(mode):
+    if mode == "one-token":
+        # n_q = 1 with more than 1,024 units selected: the matrix-core kernel, not the decode kernel
+        _attend_case(LARGE_LOOKUP[:9] + (1, 1))
+    elif mode == "skipped-entry":
+        _attend_case(LARGE_LOOKUP, invalid_entry=True)
+    else:
+        _attend_case(LARGE_LOOKUP, workspace=mode == "parts")
 
 
 def test_attend_partial_plus_merge_equals_chunk_attend():
