@@ -201,6 +201,8 @@ ATTEND_CASES = [
     ("bf16", 4, 2, 128, 128, 512, 128, 0, 3000, 512, 1),
     ("bf16", 4, 2, 128, 128, 512, 128, 0, 3000, 1, 2),     # decode
     ("f32", 2, 1, 64, 16, 256, 32, 0, 1000, 64, 1),
+    # decode at the decode kernel's largest lookup (1,024 units staged in LDS)
+    ("bf16", 4, 1, 128, 16, 256, 16, 1024, 17000, 1, 1),
 ]
 
 

@@ -119,5 +119,10 @@ def test_varlen_chunks_bf16():
     _run("bf16", 4, 2, 128, 128, 1024, 128, 8, [0, 1024, 2560], n_q=512, n_steps=2)
 
 
+def test_varlen_decode_max_batch():
+    # the largest batch a variable-length step takes: 64 sequences, 50 to 1,499 tokens deep
+    _run("bf16", 2, 1, 64, 8, 64, 16, 3, [50 + 23 * i for i in range(64)], n_q=1, n_steps=2)
+
+
 def test_varlen_decode_f32():
     _run("f32", 2, 1, 64, 16, 256, 32, 4, [200, 640, 1100], n_q=1, n_steps=3)
