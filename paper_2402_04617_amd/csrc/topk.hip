@@ -6,7 +6,9 @@
 // key > T and the lowest-indexed keys == T, writing survivors with a block-wide
 // ballot scan so the output is ascending by construction.  Deterministic.
 // Rows of up to kThreads*kMaxPer keys keep their keys in registers for all
-// passes (radix_select_reg); longer rows re-read them from memory.
+// passes (radix_select_reg); longer rows re-read them from memory.  Rows of
+// several keys per thread first narrow the keys to the candidates at or above
+// the selection threshold of the per-thread maxima (filtered_select).
 #include "launch.h"
 
 namespace infllm {
@@ -15,6 +17,7 @@ namespace {
 constexpr int kThreads = 512;
 constexpr int kWaves = kThreads / 64;
 constexpr int kMaxPer = 16;  // most keys per thread held in registers
+constexpr int kCountMax = 128;  // most filter candidates ranked by counting
 
 __device__ __forceinline__ uint32_t order_key(float x) {
   if (x != x) return 0u;        // NaN below everything
@@ -142,32 +145,35 @@ __device__ __forceinline__ void tiled_scan(const bool (&pred)[PER], int (&rank)[
   __syncthreads();  // cnt may be written again by the next scan
 }
 
-// Common path: the same radix select with the row's keys held in registers
-// (thread t: keys t, t + kThreads, ...; read once), the histogram of a pass
-// built with one atomic per wave where the wave's live digits agree (typical of
-// the leading digits), double-buffered histograms (two barriers per pass), and
-// a final pass whose index-order ranks come from one tiled ballot scan (two
-// when only some keys equal to T are kept).  The passes stop early once every
-// key sharing the resolved prefix is kept.
-template <int PER>
-__device__ void radix_select_reg(const float* __restrict__ s, int n, int k_eff, int32_t* __restrict__ out) {
+// Threshold of the radix select over keys held PER per thread (thread t: keys
+// t, t + kThreads, ...; live[j] marks the ones taking part): the histogram of a
+// pass is built with one atomic per wave where the wave's live digits agree
+// (typical of the leading digits), histograms are double-buffered (two barriers
+// per pass), and the passes stop early once every key sharing the resolved
+// prefix is kept.  On return thr is the k_eff-th largest live key and
+// `remaining` the number of live keys equal to it to keep (lowest indices
+// first) -- or, with ge_all set, thr is that prefix with its low bits zero and
+// exactly k_eff live keys are >= thr.  Either way at least k_eff live keys are
+// >= thr.  With MAXP < 4 the passes stop after MAXP digits: thr is then only
+// such a lower bound (the resolved prefix, low bits zero; ge_all is false).
+// Requires 0 < k_eff <= the live count.
+template <int PER, int MAXP = 4, typename Live>
+__device__ void radix_threshold(const uint32_t (&key)[PER], Live live_in, int k_eff, uint32_t& thr,
+                                int& remaining_out, bool& ge_all) {
   __shared__ uint32_t hist[2][256];
   __shared__ uint32_t sh_digit, sh_remaining, sh_eq_total;
   const int t = threadIdx.x, lane = t & 63;
-  uint32_t key[PER];
-#pragma unroll
-  for (int j = 0; j < PER; ++j) key[j] = order_key(s[min(t + j * kThreads, n - 1)]);
   for (int j = t; j < 256; j += kThreads) hist[0][j] = 0;
   __syncthreads();
   uint32_t prefix = 0, mask = 0;
   int remaining = k_eff;
   uint32_t eq_total = 0;
-  for (int pass = 0; pass < 4; ++pass) {
+  for (int pass = 0; pass < MAXP; ++pass) {
     const int shift = 24 - 8 * pass;
     uint32_t* h = hist[pass & 1];
 #pragma unroll
     for (int j = 0; j < PER; ++j) {
-      const bool live = t + j * kThreads < n && (key[j] & mask) == prefix;
+      const bool live = live_in(j) && (key[j] & mask) == prefix;
       const uint32_t d = (key[j] >> shift) & 255u;
       const unsigned long long lm = __ballot(live);
       if (lm == 0) continue;
@@ -209,28 +215,147 @@ __device__ void radix_select_reg(const float* __restrict__ s, int n, int k_eff, 
     // threshold that keeps exactly k_eff keys, so the remaining passes are skipped.
     if ((uint32_t)remaining == eq_total) break;
   }
-  const uint32_t thr = prefix;
-  // Final pass: ranks in index order (tile j = indices [j*kThreads, (j+1)*kThreads))
-  // from per-(tile, wave) ballot counts, one barrier per scan.
+  // the shared words are read again by the next call
+  __syncthreads();
+  thr = prefix;
+  remaining_out = remaining;
+  ge_all = (uint32_t)remaining == eq_total;
+}
+
+// The selection given a threshold: keep the live keys above thr and the first
+// `remaining` equal to it in element order (element j of thread t is the
+// (j * kThreads + t)-th; ranks from per-(tile, wave) ballot counts), and write
+// the pos-th kept element's index ix(j) to out[pos] -- ascending when ix is.
+template <int PER, typename Live, typename Index>
+__device__ void write_selection(const uint32_t (&key)[PER], Live live, Index ix, uint32_t thr, int remaining,
+                                bool ge_all, int k_eff, int32_t* __restrict__ out) {
   bool keep[PER];
-  if ((uint32_t)remaining == eq_total) {
+  if (ge_all) {
 #pragma unroll
-    for (int j = 0; j < PER; ++j) keep[j] = t + j * kThreads < n && key[j] >= thr;
+    for (int j = 0; j < PER; ++j) keep[j] = live(j) && key[j] >= thr;
   } else {
     bool eq[PER];
 #pragma unroll
-    for (int j = 0; j < PER; ++j) eq[j] = t + j * kThreads < n && key[j] == thr;
+    for (int j = 0; j < PER; ++j) eq[j] = live(j) && key[j] == thr;
     int eq_rank[PER], tot;
     tiled_scan<PER>(eq, eq_rank, &tot);
 #pragma unroll
-    for (int j = 0; j < PER; ++j)
-      keep[j] = t + j * kThreads < n && (key[j] > thr || (eq[j] && eq_rank[j] < remaining));
+    for (int j = 0; j < PER; ++j) keep[j] = live(j) && (key[j] > thr || (eq[j] && eq_rank[j] < remaining));
   }
   int pos[PER], tot;
   tiled_scan<PER>(keep, pos, &tot);
 #pragma unroll
   for (int j = 0; j < PER; ++j)
-    if (keep[j] && pos[j] < k_eff) out[pos[j]] = t + j * kThreads;
+    if (keep[j] && pos[j] < k_eff) out[pos[j]] = ix(j);
+}
+
+// Long rows (several keys per thread, k_eff <= kThreads): a cheap filter first.
+// Let m be a key with at least k_eff per-thread maxima >= m (the 16-bit prefix
+// two radix passes over the maxima resolve): those k_eff maxima are distinct
+// keys >= m, so the row's k_eff-th largest key T is >= m, and every key the
+// selection keeps (the keys > T and the lowest-indexed keys == T) is among the
+// candidates >= m.  The candidates are compacted in index order and the
+// selection is run on them, one per thread: few candidates rank themselves by
+// counting (rank = candidates with a larger key, or an equal key at a lower
+// index; kept iff rank < k_eff), more run the radix select.  Either way the
+// result is the one the full select gives.  Returns false (workgroup-uniform)
+// when more than kThreads candidates remain, e.g. on massive ties; the caller
+// then selects over all keys.
+template <int PER>
+__device__ bool filtered_select(const uint32_t (&key)[PER], int n, int k_eff, int32_t* __restrict__ out) {
+  __shared__ uint32_t ckey[kThreads];
+  __shared__ int32_t cidx[kThreads];
+  const int t = threadIdx.x;
+  auto valid = [&](int j) { return t + j * kThreads < n; };
+  uint32_t mx[1] = {0u};
+#pragma unroll
+  for (int j = 0; j < PER; ++j)
+    if (valid(j)) mx[0] = max(mx[0], key[j]);
+  uint32_t m;
+  int rem;
+  bool ge;
+  radix_threshold<1, 2>(mx, [&](int) { return t < n; }, k_eff, m, rem, ge);  // thread t holds key t
+  // Compaction in element order: per-(tile, wave) candidate counts, their
+  // exclusive prefix in element order (tile-major), then each candidate's slot
+  // from its wave's ballot.  The predicate is recomputed rather than kept.
+  __shared__ int cbase[PER * kWaves + 1];
+  const int lane = t & 63, wave = t >> 6;
+  auto cand = [&](int j) { return valid(j) && key[j] >= m; };
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const unsigned long long b = __ballot(cand(j));
+    if (lane == 0) cbase[j * kWaves + wave] = __popcll(b);
+  }
+  __syncthreads();
+  if (t < 64) {
+    // lane l takes entries 2l and 2l+1 (PER * kWaves <= 128)
+    constexpr int NE = PER * kWaves;
+    const int c0 = 2 * t < NE ? cbase[2 * t] : 0, c1 = 2 * t + 1 < NE ? cbase[2 * t + 1] : 0;
+    int inc = c0 + c1;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+      const int x = __shfl_up(inc, o);
+      inc += t >= o ? x : 0;
+    }
+    if (2 * t < NE) cbase[2 * t] = inc - c0 - c1;
+    if (2 * t + 1 < NE) cbase[2 * t + 1] = inc - c1;
+    if (t == 63) cbase[NE] = inc;
+  }
+  __syncthreads();
+  const int n_cand = cbase[PER * kWaves];
+  if (n_cand > kThreads) return false;
+  const unsigned long long below = (1ull << lane) - 1ull;
+#pragma unroll
+  for (int j = 0; j < PER; ++j) {
+    const bool c = cand(j);
+    const unsigned long long b = __ballot(c);
+    if (c) {
+      const int r = cbase[j * kWaves + wave] + __popcll(b & below);
+      ckey[r] = key[j];
+      cidx[r] = t + j * kThreads;
+    }
+  }
+  __syncthreads();
+  const bool live = t < n_cand;
+  const uint32_t ck[1] = {live ? ckey[t] : 0u};
+  const int ci = live ? cidx[t] : 0;
+  if (n_cand <= kCountMax) {
+    int rank = 0;
+    for (int c = 0; c < n_cand; ++c) {
+      const uint32_t kc = ckey[c];  // same address across the wave: one broadcast read
+      rank += (kc > ck[0] || (kc == ck[0] && c < t)) ? 1 : 0;
+    }
+    __shared__ int wave_tot[kWaves];
+    int tot;
+    const bool keep = live && rank < k_eff;
+    const int pos = block_scan(keep, wave_tot, &tot);
+    if (keep) out[pos] = ci;
+    return true;
+  }
+  uint32_t thr;
+  radix_threshold<1>(ck, [&](int) { return live; }, k_eff, thr, rem, ge);
+  write_selection<1>(ck, [&](int) { return live; }, [&](int) { return ci; }, thr, rem, ge, k_eff, out);
+  return true;
+}
+
+// Common path: the radix select with the row's keys held in registers (thread
+// t: keys t, t + kThreads, ...; read once); rows of 4+ keys per thread try the
+// filter above first.
+template <int PER>
+__device__ void radix_select_reg(const float* __restrict__ s, int n, int k_eff, int32_t* __restrict__ out) {
+  const int t = threadIdx.x;
+  uint32_t key[PER];
+#pragma unroll
+  for (int j = 0; j < PER; ++j) key[j] = order_key(s[min(t + j * kThreads, n - 1)]);
+  if constexpr (PER >= 4) {
+    if (k_eff <= kThreads && filtered_select<PER>(key, n, k_eff, out)) return;
+  }
+  auto valid = [&](int j) { return t + j * kThreads < n; };
+  uint32_t thr;
+  int rem;
+  bool ge;
+  radix_threshold<PER>(key, valid, k_eff, thr, rem, ge);
+  write_selection<PER>(key, valid, [&](int j) { return t + j * kThreads; }, thr, rem, ge, k_eff, out);
 }
 
 // PER: keys per thread of the common path (0: radix select only).
