@@ -289,6 +289,9 @@ infllm_status infllm_unit_mass(const infllm_params* p, const infllm_memory* m, c
  *   3. relevance of every unit: scores [batch][Hkv][n_units(past_len)] float32;
  *   4. lookup of the k_m best: idx [batch][Hkv][k_m] int32 (as infllm_select_topk);
  *   5. attention (as infllm_chunk_attend) into out / lse.
+ * With bf16 chunks (the matrix-core attention) and at most 1,024 units, stages 4
+ * and 5 share one launch: the attention selects the units from the scores itself
+ * and writes idx as stage 4 would (same entries, order and padding).
  * units_built is the number of units built by earlier steps (0 for the first
  * step); afterwards n_units(past_len) units are built.  Every stage is validated
  * before the first is enqueued. */

@@ -676,9 +676,20 @@ infllm_status infllm_step(const infllm_params* p, const infllm_memory* m, const 
       return st;
     }
   }
-  // with no units yet this still writes the -1 padding of idx
-  if (p->topk > 0 && (st = launch_status(launch_select_topk(rows, scores, part.n_units, p->topk, idx, s))) != INFLLM_OK)
+  // The matrix-core attention selects the units itself (one launch fewer on the
+  // step's critical path) when the score rows are short enough for its prologue;
+  // otherwise the selection kernel runs first.  With no units yet the selection
+  // kernel still writes the -1 padding of idx.
+  const bool select_in_attend = p->topk > 0 && part.n_units > 0 && part.n_units <= kFusedSelectMax &&
+                                attend_uses_mfma(at);
+  if (select_in_attend) {
+    at.sel_scores = scores;
+    at.sel_stride = part.n_units;
+    at.idx_out = idx;
+  } else if (p->topk > 0 &&
+             (st = launch_status(launch_select_topk(rows, scores, part.n_units, p->topk, idx, s))) != INFLLM_OK) {
     return st;
+  }
   if (n_q == 0) return INFLLM_OK;
   if ((st = launch_status(launch_attend(at, s))) != INFLLM_OK) return st;
   if (at.parts == 1) return INFLLM_OK;

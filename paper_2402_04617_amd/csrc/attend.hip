@@ -178,6 +178,11 @@ int attend_max_parts(bool bf16, int G, int n_q, int64_t max_virtual) {
   return bf16 ? 8 : 16;
 }
 
+bool attend_uses_mfma(const AttendArgs& a) {
+  const int G = a.n_q_heads / a.n_kv_heads;
+  return a.geom.n_q > 0 && a.bf16 && !decode_eligible(a.bf16, a.geom.n_q, G, a.geom.n_sel);
+}
+
 hipError_t launch_attend(const AttendArgs& a, hipStream_t s) {
   if (a.geom.n_q == 0) return hipSuccess;
   const int G = a.n_q_heads / a.n_kv_heads;

@@ -20,6 +20,7 @@
 //                  transpose read (ds_read_b64_tr_b16), in the key order the
 //                  accumulator layout gives P^T.
 #include "launch.h"
+#include "topk_select.h"
 
 namespace infllm {
 namespace {
@@ -79,6 +80,7 @@ __device__ __forceinline__ int tile_off(int r, int g) { return r * D + 8 * (g ^ 
 
 constexpr int NBUF = 3;         // K and V tile buffers
 constexpr int kMaskCost = 6;  // cost of a masked tile, in quarters of a plain tile (measured ~1.5x)
+constexpr int kSelTiles4 = 5;  // the in-prologue unit selection, in quarters of a plain tile
 constexpr int kRunTable = 1024;  // run starts kept in LDS for the part's tiles
 constexpr int kSelLds = 1024;    // lookup entries kept in LDS
 
@@ -105,7 +107,9 @@ __device__ __forceinline__ void publish_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-template <int D>
+// SEL: the workgroups select the lookup themselves from a.sel_scores (a kernel
+// of its own, so that the plain kernel's code is unaffected).
+template <int D, bool SEL>
 __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a) {
   constexpr int CH = D / 8;                   // 16-byte granules per row
   constexpr int KSTEPS = D / 16;              // MFMA k-steps over the head dim
@@ -158,11 +162,28 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
   const int v_x0 = geo.n_virtual - geo.n_q;  // first current-token key
   auto part_bound = [&](int pp) -> int {  // first tile of part pp of rparts
     const int a_x = min(max(v_x0 / KB, rt0), rt1);
-    const int64_t c_plain = 4LL * (a_x - rt0);
-    const int64_t c_all = c_plain + (int64_t)kMaskCost * (rt1 - a_x);
+    if constexpr (!SEL) {
+      const int64_t c_plain = 4LL * (a_x - rt0);
+      const int64_t c_all = c_plain + (int64_t)kMaskCost * (rt1 - a_x);
+      const int64_t c = c_all * pp / rparts;
+      if (c <= c_plain) return rt0 + (int)((c + 3) / 4);
+      return a_x + (int)((c - c_plain + kMaskCost - 1) / kMaskCost);
+    }
+    // The parts that read unit keys also select the units (see below), about
+    // kSelTiles tiles of work each.  The tiles up to the end of the units are
+    // charged that work spread over them, for the share of the parts expected to
+    // fall there (costs in 1/64 of a plain tile).
+    const int u_end = (geo.n_init + geo.n_sel * geo.block_size + KB - 1) / KB;
+    const int s_end = min(max(u_end, rt0), a_x);
+    constexpr int64_t kPlain = 64, kMask = 16 * kMaskCost;
+    const int64_t kSel = kPlain + (kPlain * kSelTiles4 * rparts) / (4 * max(1, rt1 - rt0));
+    const int64_t c_sel = kSel * (s_end - rt0);
+    const int64_t c_plain = c_sel + kPlain * (a_x - s_end);
+    const int64_t c_all = c_plain + kMask * (rt1 - a_x);
     const int64_t c = c_all * pp / rparts;
-    if (c <= c_plain) return rt0 + (int)((c + 3) / 4);
-    return a_x + (int)((c - c_plain + kMaskCost - 1) / kMaskCost);
+    if (c <= c_sel) return rt0 + (int)((c + kSel - 1) / kSel);
+    if (c <= c_plain) return s_end + (int)((c - c_sel + kPlain - 1) / kPlain);
+    return a_x + (int)((c - c_plain + kMask - 1) / kMask);
   };
   const int t_begin = part_bound(rpart);
   int t_end = part_bound(rpart + 1);
@@ -192,10 +213,31 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
   // the check for skipped (out-of-range) entries, which send every tile through
   // the per-key gather path and the validity mask.
   bool bad = false;
-  for (int u = tid; u < geo.n_sel; u += 64 * NWAVE) {
-    const int x = idx_row[u];
-    if (u < kSelLds) sm.sidx[u] = x;
-    bad |= (x < 0 || x >= geo.n_units);
+  if constexpr (!SEL) {
+    for (int u = tid; u < geo.n_sel; u += 64 * NWAVE) {
+      const int x = idx_row[u];
+      if (u < kSelLds) sm.sidx[u] = x;
+      bad |= (x < 0 || x >= geo.n_units);
+    }
+  }
+  // Lookup inside the attention: a workgroup selects the units itself when a
+  // tile it reads (its own, the run-start table's and the loads issued ahead:
+  // [t_begin, t_end + 4)) holds unit keys; the workgroup of row tile 0 and part
+  // 0 always does, and writes the row out.  Every entry is then valid.  The
+  // score row is loaded here, its latency overlapping the Q loads below.
+  static_assert(tk::kThreads == 64 * NWAVE && 2 * tk::kThreads >= kFusedSelectMax, "select layout");
+  const bool sel_writer = SEL && rt == 0 && part == 0;
+  bool sel_here = sel_writer;
+  if constexpr (SEL) {
+    const int u_t0 = geo.n_init / KB, u_t1 = (geo.n_init + geo.n_sel * geo.block_size + KB - 1) / KB;
+    sel_here |= t_begin < u_t1 && t_end + 4 > u_t0;
+  }
+  const bool sel_all = geo.n_sel == 0 || geo.n_sel == geo.n_units;  // every unit (or none) is looked up
+  uint32_t skey[2] = {0u, 0u};
+  if (SEL && sel_here && !sel_all) {
+    const float* srow = a.sel_scores + (int64_t)bg * a.sel_stride;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) skey[j] = tk::order_key(srow[min(tid + j * tk::kThreads, geo.n_units - 1)]);
   }
   // Q rows of this wave as the B operand (8 bf16 per lane per k-step).
   bf16x8 qreg[KSTEPS];
@@ -221,6 +263,24 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
         }
       }
       qreg[s] = __builtin_bit_cast(bf16x8, raw);
+    }
+  }
+  if (SEL && sel_here) {
+    if (sel_all) {
+      for (int u = tid; u < geo.n_sel; u += 64 * NWAVE) sm.sidx[u] = u;
+    } else {
+      auto valid = [&](int j) { return tid + j * tk::kThreads < geo.n_units; };
+      uint32_t thr;
+      int rem;
+      bool ge;
+      tk::radix_threshold<2>(skey, valid, geo.n_sel, thr, rem, ge);
+      tk::write_selection<2>(skey, valid, [&](int j) { return tid + j * tk::kThreads; }, thr, rem, ge, geo.n_sel,
+                             sm.sidx);
+    }
+    __syncthreads();
+    if (sel_writer) {
+      int32_t* orow = a.idx_out + (int64_t)bg * geo.idx_stride;
+      for (int u = tid; u < geo.idx_stride; u += 64 * NWAVE) orow[u] = u < geo.n_sel ? sm.sidx[u] : -1;
     }
   }
   const bool has_invalid = __syncthreads_or(bad) != 0;
@@ -835,10 +895,15 @@ hipError_t launch_attend_mfma(const AttendArgs& a, hipStream_t s) {
   const int R = G * a.geom.n_q;
   const int n_row_tiles = (R + ROWS_WG - 1) / ROWS_WG;
   const int blocks = n_row_tiles * a.parts * a.batch * a.n_kv_heads;
-  if (a.head_dim == 128)
-    hipLaunchKernelGGL(attend_mfma_kernel<128>, dim3(blocks), dim3(64 * NWAVE), 0, s, a);
-  else
-    hipLaunchKernelGGL(attend_mfma_kernel<64>, dim3(blocks), dim3(64 * NWAVE), 0, s, a);
+  const dim3 grid(blocks), block(64 * NWAVE);
+  const bool sel = a.sel_scores != nullptr;
+  if (a.head_dim == 128) {
+    if (sel) hipLaunchKernelGGL((attend_mfma_kernel<128, true>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((attend_mfma_kernel<128, false>), grid, block, 0, s, a);
+  } else {
+    if (sel) hipLaunchKernelGGL((attend_mfma_kernel<64, true>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((attend_mfma_kernel<64, false>), grid, block, 0, s, a);
+  }
   return hipGetLastError();
 }
 

@@ -136,6 +136,8 @@ constexpr int kDecodeMinKeysPerWg = 256;
 // the matrix-core kernel.
 constexpr int kDecodeMaxSel = 1024;
 
+constexpr int kFusedSelectMax = 1024;  // most units the attention selects itself
+
 struct AttendArgs {
   int batch, n_q_heads, n_kv_heads, head_dim;
   int64_t capacity, q_head_stride, out_head_stride;
@@ -159,6 +161,14 @@ struct AttendArgs {
   VarLen var;
   int n_local;
   const int32_t* idx;
+  // Lookup inside the attention (sel_scores non-null; matrix-core kernel, one
+  // step geometry, n_units <= kFusedSelectMax): a workgroup whose tiles hold unit
+  // keys selects its kv head's n_sel units from the score row itself, with the
+  // select of infllm_select_topk, instead of reading idx; the workgroup of row
+  // tile 0 and part 0 also writes the row to idx_out (the -1 padding included).
+  const float* sel_scores;  // [batch * n_kv_heads][sel_stride]
+  int64_t sel_stride;
+  int32_t* idx_out;         // [batch * n_kv_heads][geom.idx_stride]
   void* out;     // final output (one part)
   float* lse;    // nullable
   // Split-key partials (parts > 1), see the layout in common.h: float32 rows for
@@ -192,6 +202,8 @@ __host__ __device__ inline SeqStep seq_step(const AttendArgs& a, int b) {
 int attend_choose_parts(bool bf16, int batch, int n_q_heads, int n_kv_heads, int n_q, int n_sel, int n_virtual,
                         int max_parts);
 hipError_t launch_attend(const AttendArgs& a, hipStream_t s);
+// Whether launch_attend runs the matrix-core kernel for these arguments.
+bool attend_uses_mfma(const AttendArgs& a);
 
 struct MergeArgs {
   int rows, head_dim, parts, n_q, n_q_heads;

@@ -113,6 +113,30 @@ def test_stream_no_lookup(remap):
     run_and_check(wl, 4, {0, 9, 10, 33, n - 1}, q, k, v, remap=remap)
 
 
+@pytest.mark.parametrize("block_size", [128, 32], ids=["128-token-units", "32-token-units"])
+def test_stream_tied_unit_scores(block_size):
+    """Chunks whose queries are all zero give every unit the score 0 (Q-bar = 0): the lookup is then
+    one full tie and takes the k_m lowest-indexed units, the tie rule of the memory lookup.  At these
+    shapes the matrix-core attention selects the units itself in its prologue; 32-token units put
+    more than 512 units in a row (two keys per thread of the select).  The middle zero chunk is
+    checked against the oracle like any step, the last one also exactly: idx = 0 .. k_m - 1."""
+    import dataclasses
+    wl = dataclasses.replace(WORKLOADS["mistral7b-32k"], block_size=block_size)
+    s = Synth(wl, 6)
+    q, k, v = s.full("q"), s.full("k"), s.full("v")
+    steps = wl.step_starts()
+    n = len(steps)
+    zero = {n // 2, n - 1}
+    for si in zero:
+        past, ln = steps[si]
+        q[:, :, past:past + ln] = 0.0
+    L = run_and_check(wl, 6, zero | {n // 2 + 1}, q, k, v)
+    nu = O.partition(steps[-1][0], oparams(L.p)).n_units
+    assert nu > wl.topk and (block_size == 128 or nu > 512), nu
+    idx = host(L.idx).reshape(wl.batch, wl.n_kv_heads, -1)[:, :, : wl.topk]
+    assert (idx == np.arange(wl.topk)).all(), idx
+
+
 def test_stream_paper_1m_settings():
     """The paper's settings for its 1,024K run (2048-token chunks, one representative token) on the
     Mistral-7B shape: append scans of four tiles, single-part attention over 8,192 rows per kv head."""
