@@ -790,7 +790,13 @@ infllm_status infllm_step_varlen(const infllm_params* p, const infllm_memory* m,
       return st;
     }
   }
-  if (p->topk > 0) {
+  // As in infllm_step: the attention selects each sequence's units itself when
+  // every score row is short enough (a sequence without units gets -1 padding).
+  if (p->topk > 0 && n_units_max > 0 && n_units_max <= kFusedSelectMax && attend_uses_mfma(at)) {
+    at.sel_scores = scores;
+    at.sel_stride = m->max_units;
+    at.idx_out = idx;
+  } else if (p->topk > 0) {
     TopkRows tr;
     tr.rows_per_seq = p->n_kv_heads;
     for (int b = 0; b < B; ++b) tr.row_n[b] = n_units[b];
