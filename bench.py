@@ -48,18 +48,18 @@ KERNEL_TRAFFIC = {
     # replayed launches the bench line times
     "attend_mfma_llama3-8b-128k": {"src": {"attend_mfma.hip": "74f1b2cf417eb9b43ce14ef740bbe8b5c249c77bc9ea3bb94850e23d95e2af75", "launch.h": "08e9e4cfaedca2f172e4ed01c1a20223a892130f475105e4b1039fd79660af94"},
                                    "fetch_kib": 20091.3, "write_kib": 16896.0},
-    "score_llama3-8b-128k": {"src": {"score.hip": "2ca2d6a79da7f4cf9826056be879736c84296102c76a518d0900e245645c4806", "launch.h": "08e9e4cfaedca2f172e4ed01c1a20223a892130f475105e4b1039fd79660af94"},
-                             "fetch_kib": 2086.6 + 2276.0, "write_kib": 64.0 + 34.3},
+    "score_llama3-8b-128k": {"src": {"score.hip": "b863ba9bf6e01b4901383469e615c02c7ae9b482693bef88e3f29735e4666a13", "launch.h": "08e9e4cfaedca2f172e4ed01c1a20223a892130f475105e4b1039fd79660af94"},
+                             "fetch_kib": 2086.6 + 2281.5, "write_kib": 64.0 + 34.3},
     "append_llama3-8b-128k": {"src": {"append.hip": "fe44574fc83ade25154c0c6246e75f45770ecbba5020429ac57eca075d4f3464", "launch.h": "08e9e4cfaedca2f172e4ed01c1a20223a892130f475105e4b1039fd79660af94"},
                               "fetch_kib": 5738.3, "write_kib": 6659.0},
-    "score_llama3-8b-1m": {"src": {"score.hip": "2ca2d6a79da7f4cf9826056be879736c84296102c76a518d0900e245645c4806", "launch.h": "08e9e4cfaedca2f172e4ed01c1a20223a892130f475105e4b1039fd79660af94"},
-                           "fetch_kib": 2086.5 + 16612.6, "write_kib": 64.0 + 282.8},
+    "score_llama3-8b-1m": {"src": {"score.hip": "b863ba9bf6e01b4901383469e615c02c7ae9b482693bef88e3f29735e4666a13", "launch.h": "08e9e4cfaedca2f172e4ed01c1a20223a892130f475105e4b1039fd79660af94"},
+                           "fetch_kib": 2086.5 + 16617.6, "write_kib": 64.0 + 282.8},
     "append_llama3-8b-1m": {"src": {"append.hip": "fe44574fc83ade25154c0c6246e75f45770ecbba5020429ac57eca075d4f3464", "launch.h": "08e9e4cfaedca2f172e4ed01c1a20223a892130f475105e4b1039fd79660af94"},
                             "fetch_kib": 5738.0, "write_kib": 6659.0},
     "attend_decode": {"src": {"attend_decode.hip": "e9c010e0b521a9e279ded2a3f90fe08bc8e43dc66eb5d0d9b4d86bcbdbd07953", "launch.h": "08e9e4cfaedca2f172e4ed01c1a20223a892130f475105e4b1039fd79660af94"},
                       "fetch_kib": 270890.8, "write_kib": 544.0},
-    "score_decode": {"src": {"score.hip": "2ca2d6a79da7f4cf9826056be879736c84296102c76a518d0900e245645c4806", "launch.h": "08e9e4cfaedca2f172e4ed01c1a20223a892130f475105e4b1039fd79660af94"},
-                     "fetch_kib": 102.5 + 32276.0, "write_kib": 64.0 + 496.0},
+    "score_decode": {"src": {"score.hip": "b863ba9bf6e01b4901383469e615c02c7ae9b482693bef88e3f29735e4666a13", "launch.h": "08e9e4cfaedca2f172e4ed01c1a20223a892130f475105e4b1039fd79660af94"},
+                     "fetch_kib": 102.5 + 32281.5, "write_kib": 64.0 + 496.0},
 }
 
 

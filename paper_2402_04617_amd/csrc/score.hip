@@ -54,8 +54,20 @@ __global__ void __launch_bounds__(256) score_kernel(const ScoreArgs a, int parts
   __shared__ float qbar[D];
   __shared__ float part[4][kScoreUnits];
   if (threadIdx.x < D) {
+    // every part's load issued before the first add (a loop that waits for each
+    // load in turn would also wait behind the key-sum loads above)
+    const float* qp = a.qbar_parts + (int64_t)bg * parts * D + threadIdx.x;
     float s = 0.f;
-    for (int p = 0; p < parts; ++p) s += a.qbar_parts[((int64_t)bg * parts + p) * D + threadIdx.x];
+    if (parts == 1) {
+      s = *qp;
+    } else {
+      float v[kMaxQbarParts];
+#pragma unroll
+      for (int p = 0; p < kMaxQbarParts; ++p) v[p] = p < parts ? qp[p * D] : 0.f;
+#pragma unroll
+      for (int p = 0; p < kMaxQbarParts; ++p)
+        if (p < parts) s += v[p];
+    }
     qbar[threadIdx.x] = s;
   }
   __syncthreads();
