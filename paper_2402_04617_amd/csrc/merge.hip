@@ -18,7 +18,11 @@ __global__ void __launch_bounds__(256) merge_kernel(MergeArgs a) {
   constexpr int DPT = HALF ? 8 : 4;  // dims per thread
   const int tpr = a.head_dim / DPT;
   const int rows_per_wg = 256 / tpr;
-  const int row = blockIdx.x * rows_per_wg + threadIdx.x / tpr;
+  // Workgroups in the attention's XCD order (reversed, consecutive ids on one
+  // XCD): where a kv head's parts were written by the workgroups of one XCD, the
+  // rows of that kv head are merged on the same XCD and read its L2.
+  const int wg = (int)gridDim.x - 1 - xcd_logical_block(blockIdx.x, gridDim.x);
+  const int row = wg * rows_per_wg + threadIdx.x / tpr;
   const int c = threadIdx.x % tpr;
   if (row >= a.rows) return;
   float M = -__builtin_inff(), tot = 0.f;
