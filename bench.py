@@ -262,9 +262,10 @@ class Stream:
         return built
 
     def attention_replay(self, steps, idx_hist):
-        """The attention kernels alone, the same launches as in the step (lookups recorded from a real
-        pass), issued back to back on the launching stream between two HIP events: returns the average
-        launch duration (ms) and the number of key parts of each launch."""
+        """The attention kernels alone, in the step's launch configuration on the lookups recorded from a
+        real pass (the plain kernel: in the step the same launches also select the units in their
+        prologue), issued back to back on the launching stream between two HIP events: returns the
+        average launch duration (ms) and the number of key parts of each launch."""
         F, torch, wl, S, D = self.F, self.torch, self.wl, self.wl.seq_len, self.wl.head_dim
         parts_seen = []
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -726,7 +727,7 @@ def main():
         "config": {"workload": "llama3-8b-128k", "seq_len": 131072, "batch": 1, "q_heads": 32, "kv_heads": 8,
                    "head_dim": 128, "n_init": 128, "n_local": 4096, "block_size": 128, "n_repr": 4, "topk": 32,
                    "chunk": 512, "parallelism": "single-gpu"},
-        "roofline": {"bound": "mfma", "kernel": "attend_mfma_kernel<128>", "achieved": achieved,
+        "roofline": {"bound": "mfma", "kernel": "attend_mfma_kernel<128, false>", "achieved": achieved,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
                      "traffic": kernel_traffic_bytes("attend_mfma_llama3-8b-128k"), "traffic_unit": "B/launch",
                      "algorithmic_bytes": att["algorithmic_bytes_per_launch"],
