@@ -205,12 +205,15 @@ class Stream:
 
     def step(self, past, n, units_built):
         wl, S, D = self.wl, self.wl.seq_len, self.wl.head_dim
-        self.F.infllm_step(self.p, self.mem.struct, self.ptr("q", past), S * D, self.ptr("k", past),
-                           self.ptr("v", past), S * D, n, past, units_built, self.scores, self.idx, self.out,
-                           wl.chunk * D, self.lse, self.ws)
         if self.mass is not None:
-            self.F.infllm_unit_mass(self.p, self.mem.struct, self.ptr("q", past), S * D, n, past, self.idx, wl.topk,
-                                    self.lse, MASS_DECAY, self.mass, self.freq)
+            # the step with the looked-up units' attention mass and the frequency score update
+            self.F.infllm_step_mass(self.p, self.mem.struct, self.ptr("q", past), S * D, self.ptr("k", past),
+                                    self.ptr("v", past), S * D, n, past, units_built, self.scores, self.idx,
+                                    self.out, wl.chunk * D, self.lse, MASS_DECAY, self.mass, self.freq, self.ws)
+        else:
+            self.F.infllm_step(self.p, self.mem.struct, self.ptr("q", past), S * D, self.ptr("k", past),
+                               self.ptr("v", past), S * D, n, past, units_built, self.scores, self.idx, self.out,
+                               wl.chunk * D, self.lse, self.ws)
         return self.F.infllm_partition(self.p, past)[1]
 
     def run(self, steps, built=0, on_step=None):
@@ -661,6 +664,7 @@ def main():
         del st_s
         rs["added_us_per_step"] = (rs["ms_per_step"] - main_res["ms_per_step"]) * 1e3 / len(st.wl.step_starts())
         rs["decay"] = MASS_DECAY
+        rs["entry"] = "infllm_step_mass"
         extra["encode_128k_unit_mass"] = rs
         log(f"128K with unit mass: {rs['ms_per_step']:.2f} ms/step (+{rs['added_us_per_step']:.1f} us per chunk)")
     del st

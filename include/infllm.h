@@ -300,6 +300,24 @@ infllm_status infllm_step(const infllm_params* p, const infllm_memory* m, const 
                           int32_t units_built, float* scores, int32_t* idx, void* out, int64_t out_head_stride,
                           float* lse, void* workspace, size_t workspace_bytes, void* stream);
 
+/* infllm_step followed by the attention mass of its lookup and the frequency
+ * score update (Section 3.2, "Cache Management"; the appendix on the cache
+ * management strategy): mass [batch][Hkv][k_m] and freq [batch][Hkv][max_units]
+ * (nullable) as infllm_unit_mass writes them for this step's q, idx and lse, with
+ * the same decay and the same argument rules (lse is required when n_q, k_m > 0).
+ * Where the matrix-core attention also selects the units (bf16 chunks, at most
+ * 1,024 units) and l_I and l_bs are multiples of 64, the attention writes each
+ * looked-up 64-key tile's per-row sum of P and its running maximum into the end
+ * of the workspace, and one small launch after the merge forms the masses from
+ * them and the merged lse (no second pass over the keys); otherwise the step is
+ * followed by the unit-mass kernel.  The two agree to float32 rounding.
+ * infllm_workspace_bytes covers the partials. */
+infllm_status infllm_step_mass(const infllm_params* p, const infllm_memory* m, const void* q,
+                               int64_t q_head_stride, const void* k, const void* v, int64_t kv_head_stride,
+                               int32_t n_q, int64_t past_len, int32_t units_built, float* scores, int32_t* idx,
+                               void* out, int64_t out_head_stride, float* lse, float decay, float* mass, float* freq,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
 /* One step of a batch whose sequences have different past lengths (a serving
  * batch: each sequence decodes, or encodes a chunk, at its own position).
  * Sequence b appends its n_q tokens at [past_lens[b], past_lens[b] + n_q) and

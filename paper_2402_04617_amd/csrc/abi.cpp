@@ -458,6 +458,15 @@ infllm_status infllm_partition(const infllm_params* p, int64_t past_len, int64_t
   return INFLLM_OK;
 }
 
+// Bytes of the per-tile unit-mass partials infllm_step_mass keeps at the end of
+// the workspace (0 where the attention cannot write them: units not made of
+// whole 64-key tiles).
+static size_t mass_part_bytes(const infllm_params* p, int32_t batch, int32_t n_q) {
+  if (p->topk <= 0 || p->block_size % 64 != 0 || p->n_init % 64 != 0 || n_q <= 0) return 0;
+  const int G = p->n_q_heads / p->n_kv_heads;
+  return (size_t)batch * p->n_kv_heads * p->topk * (p->block_size / 64) * (size_t)G * n_q * sizeof(float2);
+}
+
 size_t infllm_workspace_bytes(const infllm_params* p, int32_t batch, int32_t n_q) {
   if (check_params(p) != INFLLM_OK || batch < 1 || n_q < 0) return 0;
   const int G = p->n_q_heads / p->n_kv_heads;
@@ -466,7 +475,8 @@ size_t infllm_workspace_bytes(const infllm_params* p, int32_t batch, int32_t n_q
   size_t a = attend_ws_bytes(p, batch, n_q, parts);
   size_t b = qbar_ws_bytes(p, batch, n_q);
   size_t r = a > b ? a : b;
-  return (r + 255) & ~(size_t)255;
+  r = (r + 255) & ~(size_t)255;
+  return r + ((mass_part_bytes(p, batch, n_q) + 255) & ~(size_t)255);
 }
 
 size_t infllm_attend_workspace_bytes(const infllm_params* p, int32_t batch, int32_t n_q) {
@@ -576,10 +586,14 @@ infllm_status infllm_chunk_attend_noalloc(const infllm_params* p, const infllm_m
   return launch_status(launch_merge(ma, (hipStream_t)stream));
 }
 
-infllm_status infllm_unit_mass(const infllm_params* p, const infllm_memory* m, const void* q,
-                               int64_t q_head_stride, int32_t n_q, int64_t past_len, const int32_t* idx, int32_t k,
-                               const float* lse, float decay, float* mass, float* freq, void* stream) {
+// Validation and arguments of the unit-mass launch (infllm_unit_mass, and the
+// fallback of infllm_step_mass).  *skip: nothing to launch.
+static infllm_status prep_unit_mass(const infllm_params* p, const infllm_memory* m, const void* q,
+                                    int64_t q_head_stride, int32_t n_q, int64_t past_len, const int32_t* idx,
+                                    int32_t k, const float* lse, float decay, float* mass, float* freq, MassArgs* a,
+                                    bool* skip) {
   infllm_status st;
+  *skip = false;
   if ((st = check_params(p)) != INFLLM_OK) return st;
   if ((st = check_store(p, m)) != INFLLM_OK) return st;
   if (n_q < 0 || past_len < 0 || k < 0) return INFLLM_E_SHAPE;
@@ -597,39 +611,59 @@ infllm_status infllm_unit_mass(const infllm_params* p, const infllm_memory* m, c
       if ((st = check_rows(p, q, q_head_stride, n_q)) != INFLLM_OK) return st;
     }
   }
-  if (k == 0 && (freq == nullptr || part.n_units == 0)) return INFLLM_OK;
+  if (k == 0 && (freq == nullptr || part.n_units == 0)) {
+    *skip = true;
+    return INFLLM_OK;
+  }
+  std::memset(a, 0, sizeof(*a));
+  a->rows = m->batch * p->n_kv_heads;
+  a->n_q_heads = p->n_q_heads;
+  a->n_kv_heads = p->n_kv_heads;
+  a->head_dim = p->head_dim;
+  a->n_q = n_q;
+  a->k = k;
+  a->n_units = part.n_units;
+  a->max_units = m->max_units;
+  a->block_size = p->block_size;
+  a->n_init = p->n_init;
+  a->capacity = m->capacity;
+  a->q_head_stride = q_head_stride;
+  a->sm_scale = p->sm_scale;
+  a->decay = decay;
+  a->q = q;
+  a->k_store = m->k;
+  a->idx = idx;
+  a->lse = lse;
+  a->mass = mass;
+  a->freq = part.n_units > 0 ? freq : nullptr;
+  a->rope = rope_args(p);
+  a->bf16 = p->dtype == INFLLM_BF16;
+  return INFLLM_OK;
+}
+
+infllm_status infllm_unit_mass(const infllm_params* p, const infllm_memory* m, const void* q,
+                               int64_t q_head_stride, int32_t n_q, int64_t past_len, const int32_t* idx, int32_t k,
+                               const float* lse, float decay, float* mass, float* freq, void* stream) {
   MassArgs a;
-  std::memset(&a, 0, sizeof(a));
-  a.rows = m->batch * p->n_kv_heads;
-  a.n_q_heads = p->n_q_heads;
-  a.n_kv_heads = p->n_kv_heads;
-  a.head_dim = p->head_dim;
-  a.n_q = n_q;
-  a.k = k;
-  a.n_units = part.n_units;
-  a.max_units = m->max_units;
-  a.block_size = p->block_size;
-  a.n_init = p->n_init;
-  a.capacity = m->capacity;
-  a.q_head_stride = q_head_stride;
-  a.sm_scale = p->sm_scale;
-  a.decay = decay;
-  a.q = q;
-  a.k_store = m->k;
-  a.idx = idx;
-  a.lse = lse;
-  a.mass = mass;
-  a.freq = part.n_units > 0 ? freq : nullptr;
-  a.rope = rope_args(p);
-  a.bf16 = p->dtype == INFLLM_BF16;
+  bool skip;
+  infllm_status st = prep_unit_mass(p, m, q, q_head_stride, n_q, past_len, idx, k, lse, decay, mass, freq, &a,
+                                    &skip);
+  if (st != INFLLM_OK || skip) return st;
   if ((st = check_device()) != INFLLM_OK) return st;
   return launch_status(launch_unit_mass(a, (hipStream_t)stream));
 }
 
-infllm_status infllm_step(const infllm_params* p, const infllm_memory* m, const void* q, int64_t q_head_stride,
-                          const void* k, const void* v, int64_t kv_head_stride, int32_t n_q, int64_t past_len,
-                          int32_t units_built, float* scores, int32_t* idx, void* out, int64_t out_head_stride,
-                          float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+struct MassRequest {
+  float decay;
+  float* mass;
+  float* freq;
+};
+
+static infllm_status step_impl(const infllm_params* p, const infllm_memory* m, const void* q,
+                               int64_t q_head_stride, const void* k, const void* v, int64_t kv_head_stride,
+                               int32_t n_q, int64_t past_len, int32_t units_built, float* scores, int32_t* idx,
+                               void* out, int64_t out_head_stride, float* lse, void* workspace,
+                               size_t workspace_bytes, void* stream, const MassRequest* mr) {
   infllm_status st;
   if ((st = check_params(p)) != INFLLM_OK) return st;
   if (m == nullptr) return INFLLM_E_NULL;
@@ -640,6 +674,22 @@ infllm_status infllm_step(const infllm_params* p, const infllm_memory* m, const 
   AppendArgs aa;
   ScoreArgs sa;
   AttendArgs at;
+  MassArgs mass_args;
+  bool mass_skip = true;
+  char* mass_area = nullptr;
+  if (mr != nullptr) {
+    // the unit mass of this step's lookup, validated like infllm_unit_mass
+    if ((st = prep_unit_mass(p, m, q, q_head_stride, n_q, past_len, idx, p->topk, lse, mr->decay, mr->mass, mr->freq,
+                             &mass_args, &mass_skip)) != INFLLM_OK)
+      return st;
+    // the attention's per-tile partials at the end of the workspace, when it has room
+    const size_t mb = mass_part_bytes(p, m->batch, n_q);
+    if (mb > 0 && workspace != nullptr && workspace_bytes >= mb + 256) {
+      const size_t off = (workspace_bytes - mb) & ~(size_t)255;
+      mass_area = (char*)workspace + off;
+      workspace_bytes = off;
+    }
+  }
   if ((st = prep_build(p, m, units_built, part.n_units - units_built, past_len, nullptr, &ba)) != INFLLM_OK) return st;
   if ((st = prep_append(p, m, q, q_head_stride, k, v, kv_head_stride, n_q, past_len, &aa)) != INFLLM_OK) return st;
   if ((st = prep_score(p, m, q, q_head_stride, n_q, part.n_units, scores, workspace, workspace_bytes, &sa)) !=
@@ -690,11 +740,60 @@ infllm_status infllm_step(const infllm_params* p, const infllm_memory* m, const 
              (st = launch_status(launch_select_topk(rows, scores, part.n_units, p->topk, idx, s))) != INFLLM_OK) {
     return st;
   }
-  if (n_q == 0) return INFLLM_OK;
-  if ((st = launch_status(launch_attend(at, s))) != INFLLM_OK) return st;
-  if (at.parts == 1) return INFLLM_OK;
-  MergeArgs ma = merge_args(p, m->batch, n_q, at.parts, workspace, out, out_head_stride, lse);
-  return launch_status(launch_merge(ma, s));
+  // With the unit mass asked for and the lookup inside the attention, the
+  // attention also writes each unit tile's per-row sums of P; one small launch
+  // after the merge turns them into the masses (else the unit-mass kernel).
+  const bool mass_in_attend = mr != nullptr && !mass_skip && select_in_attend && mass_area != nullptr;
+  if (mass_in_attend) {
+    at.mass_part = (float2*)mass_area;
+    at.mass_tiles = p->topk * (p->block_size / 64);
+  }
+  if (n_q > 0) {
+    if ((st = launch_status(launch_attend(at, s))) != INFLLM_OK) return st;
+    if (at.parts > 1) {
+      MergeArgs ma = merge_args(p, m->batch, n_q, at.parts, workspace, out, out_head_stride, lse);
+      if ((st = launch_status(launch_merge(ma, s))) != INFLLM_OK) return st;
+    }
+  }
+  if (mr == nullptr || mass_skip) return INFLLM_OK;
+  if (!mass_in_attend) return launch_status(launch_unit_mass(mass_args, s));
+  MassPartsArgs mp;
+  std::memset(&mp, 0, sizeof(mp));
+  mp.rows = rows;
+  mp.n_q_heads = p->n_q_heads;
+  mp.n_kv_heads = p->n_kv_heads;
+  mp.n_q = n_q;
+  mp.k = p->topk;
+  mp.n_sel = at.geom.n_sel;
+  mp.n_units = part.n_units;
+  mp.max_units = m->max_units;
+  mp.tiles_per_unit = p->block_size / 64;
+  mp.mass_tiles = at.mass_tiles;
+  mp.decay = mr->decay;
+  mp.mass_part = at.mass_part;
+  mp.idx = idx;
+  mp.lse = lse;
+  mp.mass = mr->mass;
+  mp.freq = mass_args.freq;
+  return launch_status(launch_unit_mass_parts(mp, s));
+}
+
+infllm_status infllm_step(const infllm_params* p, const infllm_memory* m, const void* q, int64_t q_head_stride,
+                          const void* k, const void* v, int64_t kv_head_stride, int32_t n_q, int64_t past_len,
+                          int32_t units_built, float* scores, int32_t* idx, void* out, int64_t out_head_stride,
+                          float* lse, void* workspace, size_t workspace_bytes, void* stream) {
+  return step_impl(p, m, q, q_head_stride, k, v, kv_head_stride, n_q, past_len, units_built, scores, idx, out,
+                   out_head_stride, lse, workspace, workspace_bytes, stream, nullptr);
+}
+
+infllm_status infllm_step_mass(const infllm_params* p, const infllm_memory* m, const void* q,
+                               int64_t q_head_stride, const void* k, const void* v, int64_t kv_head_stride,
+                               int32_t n_q, int64_t past_len, int32_t units_built, float* scores, int32_t* idx,
+                               void* out, int64_t out_head_stride, float* lse, float decay, float* mass, float* freq,
+                               void* workspace, size_t workspace_bytes, void* stream) {
+  const MassRequest mr = {decay, mass, freq};
+  return step_impl(p, m, q, q_head_stride, k, v, kv_head_stride, n_q, past_len, units_built, scores, idx, out,
+                   out_head_stride, lse, workspace, workspace_bytes, stream, &mr);
 }
 
 infllm_status infllm_step_varlen(const infllm_params* p, const infllm_memory* m, const void* q,

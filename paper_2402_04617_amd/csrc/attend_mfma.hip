@@ -108,8 +108,12 @@ __device__ __forceinline__ void publish_barrier() {
 }
 
 // SEL: the workgroups select the lookup themselves from a.sel_scores (a kernel
-// of its own, so that the plain kernel's code is unaffected).
-template <int D, bool SEL>
+// of its own, so that the plain kernel's code is unaffected).  MASS (with SEL):
+// for every tile of the looked-up units the kernel also stores, per query row,
+// the tile's sum of P = exp2(S*c2 - m) and the running max m it was formed
+// against, from which the attention mass of each unit follows once the final
+// lse is known (mass_parts_kernel).
+template <int D, bool SEL, bool MASS>
 __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a) {
   constexpr int CH = D / 8;                   // 16-byte granules per row
   constexpr int KSTEPS = D / 16;              // MFMA k-steps over the head dim
@@ -522,6 +526,21 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
       for (int j = 0; j < 16; ++j) oacc[db][j] *= alpha;
     m_run = m_new;
   };
+  // Tile t's contribution to the unit masses (MASS): for a tile of the looked-up
+  // units (whole tiles: l_I and l_bs are multiples of the tile), the row's sum of
+  // P over the tile's 64 keys (this lane's half plus the other lane half's) and
+  // the running max it was formed against.  Later rescales of l_run leave the
+  // stored pair valid: it carries its own max.
+  auto mass_tile = [&](int t, float half_sum) {
+    const int ut = t - geo.n_init / KB;  // tile index within the units
+    const int n_ut = geo.n_sel * (geo.block_size / KB);
+    if (ut < 0 || ut >= n_ut) return;
+    const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(half_sum), __float_as_uint(half_sum), false,
+                                                      false);
+    const float tsum = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+    if (row_ok && gsel == 0)
+      a.mass_part[((int64_t)bg * a.mass_tiles + ut) * R + row] = make_float2(tsum, m_run);
+  };
   // Two P values as a bf16 pair (one v_cvt_pk_bf16_f32), added unrounded to the
   // two running row sums (the normaliser keeps float32 precision; rounding only
   // the PV operand moves O by at most 2^-9 relative).
@@ -665,6 +684,7 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
       neg_m = (m_run == -__builtin_inff()) ? 0.f : -m_run;
     }
     l_run += l_pend + psum1;
+    if constexpr (MASS) mass_tile(t, l_pend + psum1);
 
     // Phase 2: PV(t) on the matrix cores; on the vector ALUs the mask of tile t+1
     // (one 8-element group of its 32 accumulator elements per step) and, four
@@ -800,6 +820,7 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
       psum1 = half_p(sA[1], w1);
     }
     l_run += l_pend + psum1;
+    if constexpr (MASS) mass_tile(t, l_pend + psum1);
     const bf16x8 pb[2][2] = {{as_bf16x8(p0[0]), as_bf16x8(p0[1])}, {as_bf16x8(w1[0]), as_bf16x8(w1[1])}};
     pv((t - t_begin) % NBUF, pb);
   }
@@ -896,13 +917,15 @@ hipError_t launch_attend_mfma(const AttendArgs& a, hipStream_t s) {
   const int n_row_tiles = (R + ROWS_WG - 1) / ROWS_WG;
   const int blocks = n_row_tiles * a.parts * a.batch * a.n_kv_heads;
   const dim3 grid(blocks), block(64 * NWAVE);
-  const bool sel = a.sel_scores != nullptr;
+  const bool sel = a.sel_scores != nullptr, mass = sel && a.mass_part != nullptr;
   if (a.head_dim == 128) {
-    if (sel) hipLaunchKernelGGL((attend_mfma_kernel<128, true>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((attend_mfma_kernel<128, false>), grid, block, 0, s, a);
+    if (mass) hipLaunchKernelGGL((attend_mfma_kernel<128, true, true>), grid, block, 0, s, a);
+    else if (sel) hipLaunchKernelGGL((attend_mfma_kernel<128, true, false>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((attend_mfma_kernel<128, false, false>), grid, block, 0, s, a);
   } else {
-    if (sel) hipLaunchKernelGGL((attend_mfma_kernel<64, true>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((attend_mfma_kernel<64, false>), grid, block, 0, s, a);
+    if (mass) hipLaunchKernelGGL((attend_mfma_kernel<64, true, true>), grid, block, 0, s, a);
+    else if (sel) hipLaunchKernelGGL((attend_mfma_kernel<64, true, false>), grid, block, 0, s, a);
+    else hipLaunchKernelGGL((attend_mfma_kernel<64, false, false>), grid, block, 0, s, a);
   }
   return hipGetLastError();
 }

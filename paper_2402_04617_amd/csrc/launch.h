@@ -169,6 +169,13 @@ struct AttendArgs {
   const float* sel_scores;  // [batch * n_kv_heads][sel_stride]
   int64_t sel_stride;
   int32_t* idx_out;         // [batch * n_kv_heads][geom.idx_stride]
+  // Per-tile unit-mass partials (with sel_scores; null: off): for tile u of the
+  // looked-up units (u < n_sel * l_bs / 64; l_I and l_bs multiples of 64) and
+  // attention row r (query-major, r = i * G + h) of kv row bg:
+  // mass_part[(bg * mass_tiles + u) * G * n_q + r] = (sum of P over the tile, m)
+  // with P = exp2(z * log2(e) - m), z the logit.
+  float2* mass_part;
+  int mass_tiles;  // tiles per kv row in mass_part (k * l_bs / 64)
   void* out;     // final output (one part)
   float* lse;    // nullable
   // Split-key partials (parts > 1), see the layout in common.h: float32 rows for
@@ -236,5 +243,23 @@ struct MassArgs {
   bool bf16;
 };
 hipError_t launch_unit_mass(const MassArgs& a, hipStream_t s);
+
+// Unit masses from the attention's per-tile partials (AttendArgs::mass_part):
+// for slot j < n_sel of kv row bg, mass = sum over the unit's tiles and the
+// G * n_q rows of P_sum * exp2(m - lse * log2(e)), lse the step's merged
+// natural-log normaliser; slots past n_sel get 0.  The frequency scores as in
+// launch_unit_mass.
+struct MassPartsArgs {
+  int rows;  // batch * n_kv_heads
+  int n_q_heads, n_kv_heads, n_q, k, n_sel, n_units, max_units;
+  int tiles_per_unit, mass_tiles;
+  float decay;
+  const float2* mass_part;
+  const int32_t* idx;  // [rows][k]
+  const float* lse;    // [batch][Hq][n_q]
+  float* mass;         // [rows][k]
+  float* freq;         // [rows][max_units] or null
+};
+hipError_t launch_unit_mass_parts(const MassPartsArgs& a, hipStream_t s);
 
 }  // namespace infllm

@@ -27,7 +27,8 @@ constexpr int kMassThreads = 1024;
 constexpr int kMassWaves = kMassThreads / 64;
 constexpr int kMassMaxBlock = 256;  // largest l_bs
 
-// Sum of a float over the workgroup (every thread gets it).
+// Sum of a float over a workgroup of NW waves (every thread gets it).
+template <int NW = kMassWaves>
 __device__ __forceinline__ float block_sum(float x, float* red) {
   x = wave_sum(x);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -35,8 +36,58 @@ __device__ __forceinline__ float block_sum(float x, float* red) {
   __syncthreads();
   float t = 0.f;
 #pragma unroll
-  for (int w = 0; w < kMassWaves; ++w) t += red[w];
+  for (int w = 0; w < NW; ++w) t += red[w];
   return t;
+}
+
+// Decay of the frequency scores of the units that row's lookup idx_row did not
+// take (the looked-up ones are updated by their slot's workgroup, so every score
+// is written by exactly one thread).
+// Scores are read BATCH per thread at a time, every load before the first store;
+// the looked-up units are marked in an LDS bitmap first (one lookup per unit
+// instead of a scan of the row's k entries).
+constexpr int kDecayBitmapWords = 2048;  // units 0 .. 65,535
+template <int BATCH>
+__device__ void decay_unselected(const int32_t* idx_row, int k, float* f, int n_units, float decay, int* sel) {
+  __shared__ uint32_t bits[kDecayBitmapWords];
+  const int step = blockDim.x;
+  const bool bitmap = n_units <= 32 * kDecayBitmapWords;
+  // the first batch of scores is in flight while the lookup row is marked
+  float fv[BATCH];
+#pragma unroll
+  for (int i = 0; i < BATCH; ++i) {
+    const int u = threadIdx.x + i * step;
+    fv[i] = f[min(u, n_units - 1)];
+  }
+  if (bitmap) {
+    for (int w = threadIdx.x; w < (n_units + 31) / 32; w += step) bits[w] = 0u;
+    __syncthreads();
+    for (int j = threadIdx.x; j < k; j += step) {
+      const int u = idx_row[j];
+      if (u >= 0 && u < n_units) atomicOr(&bits[u >> 5], 1u << (u & 31));
+    }
+  } else {
+    for (int j = threadIdx.x; j < k; j += step) sel[j] = idx_row[j];
+  }
+  __syncthreads();
+  for (int u0 = threadIdx.x; u0 < n_units; u0 += step * BATCH) {
+    if (u0 != (int)threadIdx.x) {
+#pragma unroll
+      for (int i = 0; i < BATCH; ++i) fv[i] = f[min(u0 + i * step, n_units - 1)];
+    }
+#pragma unroll
+    for (int i = 0; i < BATCH; ++i) {
+      const int u = u0 + i * step;
+      if (u >= n_units) continue;
+      bool looked_up = false;
+      if (bitmap) {
+        looked_up = ((bits[u >> 5] >> (u & 31)) & 1u) != 0u;
+      } else {
+        for (int j = 0; j < k; ++j) looked_up |= sel[j] == u;
+      }
+      if (!looked_up) f[u] = fv[i] * decay;
+    }
+  }
 }
 
 // Mass of one looked-up unit, bf16 inputs (D = 64 or 128).
@@ -215,7 +266,73 @@ __global__ void __launch_bounds__(kMassThreads) mass_kernel(MassArgs a) {
   else unit_mass_f32<D>(a, bg, slot, unit, red);
 }
 
+// Unit masses from the attention's per-tile partials: one workgroup per (kv row,
+// lookup slot) sums P_sum * exp2(m - lse2) over the unit's tiles and the rows in
+// a fixed order; extra workgroups decay the units not looked up.
+constexpr int kPartsThreads = 256;
+constexpr int kPartsRows = 8;                              // rows per thread per load batch
+constexpr int kMaxTilesPerUnit = kMassMaxBlock / 64;  // 64-key tiles of the longest unit
+__global__ void __launch_bounds__(kPartsThreads) mass_parts_kernel(MassPartsArgs a) {
+  __shared__ float red[kPartsThreads / 64];
+  __shared__ int sel[kMassMaxK];
+  const int n_slot_blocks = a.rows * a.k;
+  if ((int)blockIdx.x >= n_slot_blocks) {
+    const int bg = blockIdx.x - n_slot_blocks;
+    decay_unselected<4>(a.idx + (int64_t)bg * a.k, a.k, a.freq + (int64_t)bg * a.max_units, a.n_units, a.decay, sel);
+    return;
+  }
+  const int bg = blockIdx.x / a.k, slot = blockIdx.x - bg * a.k;
+  if (slot >= a.n_sel) {
+    if (threadIdx.x == 0) a.mass[(int64_t)bg * a.k + slot] = 0.f;
+    return;
+  }
+  const int b = bg / a.n_kv_heads, g = bg - b * a.n_kv_heads;
+  const int G = a.n_q_heads / a.n_kv_heads, R = G * a.n_q;
+  const float* lse_g = a.lse + (int64_t)(b * a.n_q_heads + g * G) * a.n_q;  // head hh at lse_g + hh * n_q
+  // Each thread takes kPartsRows rows per batch; all of a batch's loads (the rows'
+  // lse and their partials in every tile of the unit) are issued before the first
+  // use, so a batch costs one memory round trip.
+  const float2* mp = a.mass_part + ((int64_t)bg * a.mass_tiles + (int64_t)slot * a.tiles_per_unit) * R;
+  float acc = 0.f;
+  // (indices past the row count or the unit's tiles are clamped, so that every
+  // load is unconditional, and their terms dropped after)
+  for (int base = 0; base < R; base += kPartsThreads * kPartsRows) {
+    float lr[kPartsRows];
+    float2 e[kMaxTilesPerUnit][kPartsRows];
+#pragma unroll
+    for (int j = 0; j < kPartsRows; ++j) {
+      const int r = min(base + j * kPartsThreads + (int)threadIdx.x, R - 1);
+      const int i = r / G, hh = r - i * G;  // attention rows are query-major
+      lr[j] = lse_g[(int64_t)hh * a.n_q + i];
+#pragma unroll
+      for (int t = 0; t < kMaxTilesPerUnit; ++t) e[t][j] = mp[(int64_t)min(t, a.tiles_per_unit - 1) * R + r];
+    }
+#pragma unroll
+    for (int t = 0; t < kMaxTilesPerUnit; ++t)
+#pragma unroll
+      for (int j = 0; j < kPartsRows; ++j) {
+        const float term = e[t][j].x * __builtin_amdgcn_exp2f(e[t][j].y - lr[j] * 1.4426950408889634f);
+        acc += (t < a.tiles_per_unit && base + j * kPartsThreads + (int)threadIdx.x < R) ? term : 0.f;
+      }
+  }
+  const float tot = block_sum<kPartsThreads / 64>(acc, red);
+  if (threadIdx.x == 0) {
+    a.mass[(int64_t)bg * a.k + slot] = tot;
+    if (a.freq != nullptr) {
+      float* f = a.freq + (int64_t)bg * a.max_units + a.idx[(int64_t)bg * a.k + slot];
+      *f = *f * a.decay + tot;
+    }
+  }
+}
+
 }  // namespace
+
+hipError_t launch_unit_mass_parts(const MassPartsArgs& a, hipStream_t s) {
+  const int blocks = a.rows * a.k + (a.freq != nullptr ? a.rows : 0);
+  if (blocks == 0) return hipSuccess;
+  hipLaunchKernelGGL(mass_parts_kernel, dim3(blocks), dim3(kPartsThreads), 0, s, a);
+  return hipGetLastError();
+}
 
 hipError_t launch_unit_mass(const MassArgs& a, hipStream_t s) {
   const int blocks = a.rows * a.k + (a.freq != nullptr ? a.rows : 0);

@@ -26,7 +26,8 @@ STATUS = {0: "INFLLM_OK", 1: "INFLLM_E_NULL", 2: "INFLLM_E_SHAPE", 3: "INFLLM_E_
 EXPORTS = ["infllm_partition", "infllm_workspace_bytes", "infllm_attend_workspace_bytes", "infllm_append", "infllm_build_units",
            "infllm_score_units", "infllm_select_topk", "infllm_chunk_attend", "infllm_chunk_attend_noalloc",
            "infllm_attend_partial",
-           "infllm_lse_merge", "infllm_step", "infllm_step_varlen", "infllm_unit_mass", "infllm_status_string"]
+           "infllm_lse_merge", "infllm_step", "infllm_step_mass", "infllm_step_varlen", "infllm_unit_mass",
+           "infllm_status_string"]
 
 
 class InfllmError(RuntimeError):
@@ -86,6 +87,8 @@ def lib() -> ctypes.CDLL:
                                   ctypes.POINTER(i32), vp],
         "infllm_lse_merge": [P, i32, i32, i32, vp, sz, vp, i64, vp, vp],
         "infllm_step": [P, M, vp, i64, vp, vp, i64, i32, i64, i32, vp, vp, vp, i64, vp, vp, sz, vp],
+        "infllm_step_mass": [P, M, vp, i64, vp, vp, i64, i32, i64, i32, vp, vp, vp, i64, vp, ctypes.c_float, vp, vp,
+                             vp, sz, vp],
         "infllm_step_varlen": [P, M, vp, i64, vp, vp, i64, i32, ctypes.POINTER(i64), ctypes.POINTER(i32), vp, vp,
                                vp, i64, vp, vp, sz, vp],
         "infllm_unit_mass": [P, M, vp, i64, i32, i64, vp, i32, vp, ctypes.c_float, vp, vp, vp],
@@ -203,6 +206,16 @@ def infllm_step(p, m, q, q_head_stride, k, v, kv_head_stride, n_q, past_len, uni
         ctypes.byref(p), ctypes.byref(m), _ptr(q), q_head_stride, _ptr(k), _ptr(v), kv_head_stride, n_q, past_len,
         units_built, _ptr(scores), _ptr(idx), _ptr(out), out_head_stride, _ptr(lse), _ptr(workspace), wb,
         _stream(stream)))
+
+
+def infllm_step_mass(p, m, q, q_head_stride, k, v, kv_head_stride, n_q, past_len, units_built, scores, idx, out,
+                     out_head_stride, lse, decay, mass, freq=None, workspace=None, workspace_bytes=None, stream=None):
+    wb = (0 if workspace is None else workspace.numel() * workspace.element_size()) \
+        if workspace_bytes is None else workspace_bytes
+    _check("infllm_step_mass", lib().infllm_step_mass(
+        ctypes.byref(p), ctypes.byref(m), _ptr(q), q_head_stride, _ptr(k), _ptr(v), kv_head_stride, n_q, past_len,
+        units_built, _ptr(scores), _ptr(idx), _ptr(out), out_head_stride, _ptr(lse), float(decay), _ptr(mass),
+        _ptr(freq), _ptr(workspace), wb, _stream(stream)))
 
 
 def infllm_unit_mass(p, m, q, q_head_stride, n_q, past_len, idx, k, lse, decay, mass, freq=None, stream=None):

@@ -70,6 +70,16 @@ class Layer:
                       self.chunk * D, self.lse, self.ws)
         self.units_built = O.partition(past, oparams(self.p)).n_units
 
+    def step_mass(self, q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, past: int, n: int, decay: float,
+                  mass: torch.Tensor, freq: Optional[torch.Tensor]) -> None:
+        """The same step through infllm_step_mass: also the unit masses and frequency scores."""
+        S, D = q.shape[2], q.shape[3]
+        off = past * D * self.esize
+        F.infllm_step_mass(self.p, self.mem.struct, q.data_ptr() + off, S * D, k.data_ptr() + off,
+                           v.data_ptr() + off, S * D, n, past, self.units_built, self.scores, self.idx, self.out,
+                           self.chunk * D, self.lse, decay, mass, freq, self.ws)
+        self.units_built = O.partition(past, oparams(self.p)).n_units
+
     def capture(self, n: int, n_units: int) -> Dict[str, np.ndarray]:
         torch.cuda.synchronize()
         B, Hq, Hkv = self.batch, self.p.n_q_heads, self.p.n_kv_heads

@@ -32,7 +32,7 @@ def _rel_tol(p):
     return 2e-2 if p.remap else 2e-3
 
 
-def _run(p, dtype, q, k, v, steps, chunk):
+def _run(p, dtype, q, k, v, steps, chunk, in_step=False):
     op = oparams(p)
     B, G, Hkv = q.shape[0], p.n_q_heads // p.n_kv_heads, p.n_kv_heads
     L = Layer(p, B, q.shape[2], chunk=chunk)
@@ -47,10 +47,13 @@ def _run(p, dtype, q, k, v, steps, chunk):
     rel = _rel_tol(p)
     n_checked = 0
     for si, (past, n) in enumerate(steps):
-        L.step(qd, kd, vd, past, n)
-        F.infllm_unit_mass(p, L.mem.struct, qd.data_ptr() + past * D * esz, S * D, n, past, L.idx, p.topk,
-                           L.lse, DECAY, mass, freq)
-        log(f"[mass] step={si} past={past} n={n}")
+        if in_step:
+            L.step_mass(qd, kd, vd, past, n, DECAY, mass, freq)
+        else:
+            L.step(qd, kd, vd, past, n)
+            F.infllm_unit_mass(p, L.mem.struct, qd.data_ptr() + past * D * esz, S * D, n, past, L.idx, p.topk,
+                               L.lse, DECAY, mass, freq)
+        log(f"[mass] step={si} past={past} n={n} in_step={in_step}")
         nu = O.partition(past, op).n_units
         got = L.capture(n, nu)
         gm, gf = host(mass), host(freq)
@@ -99,6 +102,59 @@ def test_unit_mass_stream(case):
     p = F.params(G * Hkv, Hkv, D, n_init, n_local, lbs, nrep, topk, dtype, rope_inv_freq=freqs)
     q, k, v = rand_inputs(rng, G * Hkv, Hkv, S, D, dtype)
     _run(p, dtype, q, k, v, _steps(S, chunk), chunk)
+
+
+# infllm_step_mass: the first three shapes have l_I and l_bs multiples of 64 (the attention writes
+# the per-tile partials while it runs, the masses follow from the merged lse); the last one takes
+# the unit-mass kernel after the step.
+STEP_CASES = [
+    ("bf16", 8, 1, 128, 64, 512, 64, 4, 8, 2600, 256, False),
+    ("bf16", 2, 1, 64, 0, 256, 256, 2, 3, 1800, 300, False),
+    ("bf16", 4, 2, 128, 128, 512, 128, 4, 6, 3000, 256, True),
+    ("bf16", 4, 2, 128, 5, 300, 24, 4, 7, 1500, 128, False),
+]
+
+
+@pytest.mark.parametrize("case", STEP_CASES)
+def test_unit_mass_in_step(case):
+    dtype, G, Hkv, D, n_init, n_local, lbs, nrep, topk, S, chunk, remap = case
+    rng = np.random.default_rng(sum(case[1:11]) + 1)
+    freqs = F.rope_frequencies(D, 10000.0) if remap else None
+    p = F.params(G * Hkv, Hkv, D, n_init, n_local, lbs, nrep, topk, dtype, rope_inv_freq=freqs)
+    q, k, v = rand_inputs(rng, G * Hkv, Hkv, S, D, dtype)
+    _run(p, dtype, q, k, v, _steps(S, chunk), chunk, in_step=True)
+
+
+def test_unit_mass_in_step_matches_separate_call():
+    """infllm_step_mass against infllm_step + infllm_unit_mass on the same stream (Llama-3 layer shape,
+    512-token chunks, k_m 32): the same lookup, output and lse bit for bit (the attention's arithmetic
+    is unchanged by the partial sums it also writes), masses and frequency scores to float32 rounding
+    of the two summation orders."""
+    rng = np.random.default_rng(77)
+    G, Hkv, D, S, chunk = 4, 2, 128, 4096 + 128 + 40 * 128 + 3 * 512, 512
+    p = F.params(G * Hkv, Hkv, D, 128, 4096, 128, 4, 32, "bf16")
+    q, k, v = rand_inputs(rng, G * Hkv, Hkv, S, D, "bf16")
+    La, Lb = Layer(p, 1, S, chunk=chunk), Layer(p, 1, S, chunk=chunk)
+    qd, kd, vd = dev(q, "bf16"), dev(k, "bf16"), dev(v, "bf16")
+    ma, mb = (torch.zeros((1, Hkv, 32), device="cuda") for _ in range(2))
+    fa, fb = (torch.zeros((1, Hkv, La.max_units), device="cuda") for _ in range(2))
+    n_cmp = 0
+    for past, n in _steps(S, chunk):
+        La.step(qd, kd, vd, past, n)
+        F.infllm_unit_mass(p, La.mem.struct, qd.data_ptr() + past * D * 2, S * D, n, past, La.idx, 32, La.lse,
+                           DECAY, ma, fa)
+        Lb.step_mass(qd, kd, vd, past, n, DECAY, mb, fb)
+        nu = O.partition(past, oparams(p)).n_units
+        log(f"[mass] in-step vs separate past={past} units={nu}")
+        a, b = La.capture(n, nu), Lb.capture(n, nu)
+        assert np.array_equal(a["idx"], b["idx"]) and np.array_equal(a["out"], b["out"])
+        assert np.array_equal(a["lse"], b["lse"])
+        gma, gmb = host(ma), host(mb)
+        assert np.all(np.abs(gma - gmb) <= 2e-5 * np.abs(gma) + 1e-5), np.abs(gma - gmb).max()
+        gfa, gfb = host(fa), host(fb)
+        assert np.all(np.abs(gfa - gfb) <= 2e-5 * np.abs(gfa) + 1e-5)
+        n_cmp += int(nu > 0)
+    assert n_cmp >= 3
 
 
 def test_unit_mass_decode():
