@@ -141,9 +141,11 @@ typedef struct {
 infllm_status infllm_partition(const infllm_params* p, int64_t past_len, int64_t* n_init,
                                int32_t* n_units, int64_t* local_begin);
 
-/* Bytes of device workspace that infllm_score_units and infllm_chunk_attend need
- * for `batch` sequences and n_q current tokens (split-key partial results and
- * query sums).  Depends only on these arguments. */
+/* Bytes of device workspace that infllm_score_units, infllm_chunk_attend and the
+ * step calls need for `batch` sequences and n_q current tokens (split-key
+ * partial results and query sums, plus the per-tile unit-mass partials that
+ * infllm_step_mass keeps at the end of its workspace).  Depends only on these
+ * arguments. */
 size_t infllm_workspace_bytes(const infllm_params* p, int32_t batch, int32_t n_q);
 /* The same size under the name the attention's callers may know it by; both names
  * cover every call that takes a workspace (scoring as well as attention). */
