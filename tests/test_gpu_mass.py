@@ -125,6 +125,17 @@ def test_unit_mass_in_step(case):
     _run(p, dtype, q, k, v, _steps(S, chunk), chunk, in_step=True)
 
 
+def test_unit_mass_in_step_mean_repr():
+    # the Mean Repr units (scored by the mean of their keys): the same attention tiles, so the
+    # same partials; 128-token units after a 64-token I, the lookup larger than the unit count
+    # in the first steps (every unit looked up) and smaller later
+    rng = np.random.default_rng(31)
+    G, Hkv, D, S, chunk = 4, 2, 128, 2900, 256
+    p = F.params(G * Hkv, Hkv, D, 64, 512, 128, 4, 6, "bf16", repr_mode="mean")
+    q, k, v = rand_inputs(rng, G * Hkv, Hkv, S, D, "bf16")
+    _run(p, "bf16", q, k, v, _steps(S, chunk), chunk, in_step=True)
+
+
 def test_unit_mass_in_step_matches_separate_call():
     """infllm_step_mass against infllm_step + infllm_unit_mass on the same stream (Llama-3 layer shape,
     512-token chunks, k_m 32): the same lookup, output and lse bit for bit (the attention's arithmetic
