@@ -731,7 +731,7 @@ def main():
         "config": {"workload": "llama3-8b-128k", "seq_len": 131072, "batch": 1, "q_heads": 32, "kv_heads": 8,
                    "head_dim": 128, "n_init": 128, "n_local": 4096, "block_size": 128, "n_repr": 4, "topk": 32,
                    "chunk": 512, "parallelism": "single-gpu"},
-        "roofline": {"bound": "mfma", "kernel": "attend_mfma_kernel<128, false>", "achieved": achieved,
+        "roofline": {"bound": "mfma", "kernel": "attend_mfma_kernel<128, 0, false>", "achieved": achieved,
                      "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": achieved / PEAK_BF16_TFLOPS,
                      "traffic": kernel_traffic_bytes("attend_mfma_llama3-8b-128k"), "traffic_unit": "B/launch",
                      "algorithmic_bytes": att["algorithmic_bytes_per_launch"],

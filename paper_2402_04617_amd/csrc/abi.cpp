@@ -730,11 +730,12 @@ static infllm_status step_impl(const infllm_params* p, const infllm_memory* m, c
   // step's critical path) when the score rows are short enough for its prologue;
   // otherwise the selection kernel runs first.  With no units yet the selection
   // kernel still writes the -1 padding of idx.
-  const bool select_in_attend = p->topk > 0 && part.n_units > 0 && part.n_units <= kFusedSelectMax &&
-                                attend_uses_mfma(at);
+  const bool select_in_attend = p->topk > 0 && p->topk <= kFusedSelectMaxK && part.n_units > 0 &&
+                                part.n_units <= kFusedSelectMax && attend_uses_mfma(at);
   if (select_in_attend) {
     at.sel_scores = scores;
     at.sel_stride = part.n_units;
+    at.sel_units = part.n_units;
     at.idx_out = idx;
   } else if (p->topk > 0 &&
              (st = launch_status(launch_select_topk(rows, scores, part.n_units, p->topk, idx, s))) != INFLLM_OK) {
@@ -891,9 +892,11 @@ infllm_status infllm_step_varlen(const infllm_params* p, const infllm_memory* m,
   }
   // As in infllm_step: the attention selects each sequence's units itself when
   // every score row is short enough (a sequence without units gets -1 padding).
-  if (p->topk > 0 && n_units_max > 0 && n_units_max <= kFusedSelectMax && attend_uses_mfma(at)) {
+  if (p->topk > 0 && p->topk <= kFusedSelectMaxK && n_units_max > 0 && n_units_max <= kFusedSelectMax &&
+      attend_uses_mfma(at)) {
     at.sel_scores = scores;
     at.sel_stride = m->max_units;
+    at.sel_units = n_units_max;
     at.idx_out = idx;
   } else if (p->topk > 0) {
     TopkRows tr;

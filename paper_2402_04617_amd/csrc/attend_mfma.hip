@@ -81,8 +81,10 @@ __device__ __forceinline__ int tile_off(int r, int g) { return r * D + 8 * (g ^ 
 constexpr int NBUF = 3;         // K and V tile buffers
 constexpr int kMaskCost = 6;  // cost of a masked tile, in quarters of a plain tile (measured ~1.5x)
 constexpr int kSelTiles4 = 5;  // the in-prologue unit selection, in quarters of a plain tile
+constexpr int kSelTiles4Long = 16;  // the same for rows of more than kFusedSelectShort units
 constexpr int kRunTable = 1024;  // run starts kept in LDS for the part's tiles
 constexpr int kSelLds = 1024;    // lookup entries kept in LDS
+static_assert(kFusedSelectMaxK <= kSelLds, "a selected lookup row fits in LDS");
 
 template <int D>
 struct Smem {
@@ -107,13 +109,15 @@ __device__ __forceinline__ void publish_barrier() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "workgroup", "local");
 }
 
-// SEL: the workgroups select the lookup themselves from a.sel_scores (a kernel
-// of its own, so that the plain kernel's code is unaffected).  MASS (with SEL):
+// SEL > 0: the workgroups select the lookup themselves from a.sel_scores, SEL
+// keys of a score row per thread (2: rows of at most kFusedSelectShort units;
+// 16: longer rows, filtered first) -- kernels of their own, so that the plain
+// kernel's code is unaffected.  MASS (with SEL):
 // for every tile of the looked-up units the kernel also stores, per query row,
 // the tile's sum of P = exp2(S*c2 - m) and the running max m it was formed
 // against, from which the attention mass of each unit follows once the final
 // lse is known (mass_parts_kernel).
-template <int D, bool SEL, bool MASS>
+template <int D, int SEL, bool MASS>
 __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a) {
   constexpr int CH = D / 8;                   // 16-byte granules per row
   constexpr int KSTEPS = D / 16;              // MFMA k-steps over the head dim
@@ -180,7 +184,8 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
     const int u_end = (geo.n_init + geo.n_sel * geo.block_size + KB - 1) / KB;
     const int s_end = min(max(u_end, rt0), a_x);
     constexpr int64_t kPlain = 64, kMask = 16 * kMaskCost;
-    const int64_t kSel = kPlain + (kPlain * kSelTiles4 * rparts) / (4 * max(1, rt1 - rt0));
+    constexpr int64_t kSel4 = SEL > 2 ? kSelTiles4Long : kSelTiles4;
+    const int64_t kSel = kPlain + (kPlain * kSel4 * rparts) / (4 * max(1, rt1 - rt0));
     const int64_t c_sel = kSel * (s_end - rt0);
     const int64_t c_plain = c_sel + kPlain * (a_x - s_end);
     const int64_t c_all = c_plain + kMask * (rt1 - a_x);
@@ -229,19 +234,23 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
   // [t_begin, t_end + 4)) holds unit keys; the workgroup of row tile 0 and part
   // 0 always does, and writes the row out.  Every entry is then valid.  The
   // score row is loaded here, its latency overlapping the Q loads below.
-  static_assert(tk::kThreads == 64 * NWAVE && 2 * tk::kThreads >= kFusedSelectMax, "select layout");
-  const bool sel_writer = SEL && rt == 0 && part == 0;
+  static_assert(SEL == 0 || SEL == 2 || SEL == tk::kMaxPer, "select keys per thread");
+  static_assert(tk::kThreads == 64 * NWAVE && 2 * tk::kThreads >= kFusedSelectShort &&
+                    tk::kMaxPer * tk::kThreads >= kFusedSelectMax,
+                "select layout");
+  const bool sel_writer = SEL > 0 && rt == 0 && part == 0;
   bool sel_here = sel_writer;
   if constexpr (SEL) {
     const int u_t0 = geo.n_init / KB, u_t1 = (geo.n_init + geo.n_sel * geo.block_size + KB - 1) / KB;
     sel_here |= t_begin < u_t1 && t_end + 4 > u_t0;
   }
   const bool sel_all = geo.n_sel == 0 || geo.n_sel == geo.n_units;  // every unit (or none) is looked up
-  uint32_t skey[2] = {0u, 0u};
-  if (SEL && sel_here && !sel_all) {
+  constexpr int SK = SEL > 0 ? SEL : 1;
+  uint32_t skey[SK] = {};
+  if (SEL > 0 && sel_here && !sel_all) {
     const float* srow = a.sel_scores + (int64_t)bg * a.sel_stride;
 #pragma unroll
-    for (int j = 0; j < 2; ++j) skey[j] = tk::order_key(srow[min(tid + j * tk::kThreads, geo.n_units - 1)]);
+    for (int j = 0; j < SK; ++j) skey[j] = tk::order_key(srow[min(tid + j * tk::kThreads, geo.n_units - 1)]);
   }
   // Q rows of this wave as the B operand (8 bf16 per lane per k-step).
   bf16x8 qreg[KSTEPS];
@@ -269,17 +278,23 @@ __global__ void __launch_bounds__(64 * NWAVE, 1) attend_mfma_kernel(AttendArgs a
       qreg[s] = __builtin_bit_cast(bf16x8, raw);
     }
   }
-  if (SEL && sel_here) {
+  if (SEL > 0 && sel_here) {
     if (sel_all) {
       for (int u = tid; u < geo.n_sel; u += 64 * NWAVE) sm.sidx[u] = u;
     } else {
       auto valid = [&](int j) { return tid + j * tk::kThreads < geo.n_units; };
+      auto index = [&](int j) { return tid + j * tk::kThreads; };
       uint32_t thr;
       int rem;
       bool ge;
-      tk::radix_threshold<2>(skey, valid, geo.n_sel, thr, rem, ge);
-      tk::write_selection<2>(skey, valid, [&](int j) { return tid + j * tk::kThreads; }, thr, rem, ge, geo.n_sel,
-                             sm.sidx);
+      // long rows: the filter first (it declines, uniformly, when the bound it
+      // finds leaves more than a thread's worth of candidates)
+      bool done = false;
+      if constexpr (SEL > 2) done = geo.n_sel <= tk::kThreads && tk::filtered_select<SK>(skey, geo.n_units, geo.n_sel, sm.sidx);
+      if (!done) {
+        tk::radix_threshold<SK>(skey, valid, geo.n_sel, thr, rem, ge);
+        tk::write_selection<SK>(skey, valid, index, thr, rem, ge, geo.n_sel, sm.sidx);
+      }
     }
     __syncthreads();
     if (sel_writer) {
@@ -918,15 +933,19 @@ hipError_t launch_attend_mfma(const AttendArgs& a, hipStream_t s) {
   const int blocks = n_row_tiles * a.parts * a.batch * a.n_kv_heads;
   const dim3 grid(blocks), block(64 * NWAVE);
   const bool sel = a.sel_scores != nullptr, mass = sel && a.mass_part != nullptr;
-  if (a.head_dim == 128) {
-    if (mass) hipLaunchKernelGGL((attend_mfma_kernel<128, true, true>), grid, block, 0, s, a);
-    else if (sel) hipLaunchKernelGGL((attend_mfma_kernel<128, true, false>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((attend_mfma_kernel<128, false, false>), grid, block, 0, s, a);
-  } else {
-    if (mass) hipLaunchKernelGGL((attend_mfma_kernel<64, true, true>), grid, block, 0, s, a);
-    else if (sel) hipLaunchKernelGGL((attend_mfma_kernel<64, true, false>), grid, block, 0, s, a);
-    else hipLaunchKernelGGL((attend_mfma_kernel<64, false, false>), grid, block, 0, s, a);
-  }
+  if (sel && (a.sel_units < 1 || a.sel_units > kFusedSelectMax)) return hipErrorInvalidValue;
+  const bool long_rows = sel && a.sel_units > kFusedSelectShort;
+#define INFLLM_ATTEND_MFMA(DD)                                                                         \
+  do {                                                                                                 \
+    if (mass && long_rows) hipLaunchKernelGGL((attend_mfma_kernel<DD, 16, true>), grid, block, 0, s, a); \
+    else if (mass) hipLaunchKernelGGL((attend_mfma_kernel<DD, 2, true>), grid, block, 0, s, a);          \
+    else if (long_rows) hipLaunchKernelGGL((attend_mfma_kernel<DD, 16, false>), grid, block, 0, s, a);   \
+    else if (sel) hipLaunchKernelGGL((attend_mfma_kernel<DD, 2, false>), grid, block, 0, s, a);          \
+    else hipLaunchKernelGGL((attend_mfma_kernel<DD, 0, false>), grid, block, 0, s, a);                   \
+  } while (0)
+  if (a.head_dim == 128) INFLLM_ATTEND_MFMA(128);
+  else INFLLM_ATTEND_MFMA(64);
+#undef INFLLM_ATTEND_MFMA
   return hipGetLastError();
 }
 

@@ -136,7 +136,13 @@ constexpr int kDecodeMinKeysPerWg = 256;
 // the matrix-core kernel.
 constexpr int kDecodeMaxSel = 1024;
 
-constexpr int kFusedSelectMax = 1024;  // most units the attention selects itself
+// Score rows the matrix-core attention selects from itself: rows of at most
+// kFusedSelectShort units hold two keys per thread, longer rows up to
+// kFusedSelectMax sixteen (filtered first); at most kFusedSelectMaxK units are
+// looked up.
+constexpr int kFusedSelectShort = 1024;
+constexpr int kFusedSelectMax = 8192;
+constexpr int kFusedSelectMaxK = 1024;
 
 struct AttendArgs {
   int batch, n_q_heads, n_kv_heads, head_dim;
@@ -161,13 +167,14 @@ struct AttendArgs {
   VarLen var;
   int n_local;
   const int32_t* idx;
-  // Lookup inside the attention (sel_scores non-null; matrix-core kernel, one
-  // step geometry, n_units <= kFusedSelectMax): a workgroup whose tiles hold unit
+  // Lookup inside the attention (sel_scores non-null; matrix-core kernel,
+  // n_units <= kFusedSelectMax, n_sel <= kFusedSelectMaxK): a workgroup whose tiles hold unit
   // keys selects its kv head's n_sel units from the score row itself, with the
   // select of infllm_select_topk, instead of reading idx; the workgroup of row
   // tile 0 and part 0 also writes the row to idx_out (the -1 padding included).
   const float* sel_scores;  // [batch * n_kv_heads][sel_stride]
   int64_t sel_stride;
+  int sel_units;            // most units in any score row (picks the select's keys per thread)
   int32_t* idx_out;         // [batch * n_kv_heads][geom.idx_stride]
   // Per-tile unit-mass partials (with sel_scores; null: off): for tile u of the
   // looked-up units (u < n_sel * l_bs / 64; l_I and l_bs multiples of 64) and

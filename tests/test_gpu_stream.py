@@ -113,13 +113,15 @@ def test_stream_no_lookup(remap):
     run_and_check(wl, 4, {0, 9, 10, 33, n - 1}, q, k, v, remap=remap)
 
 
-@pytest.mark.parametrize("block_size", [128, 32], ids=["128-token-units", "32-token-units"])
+@pytest.mark.parametrize("block_size", [128, 32, 16], ids=["128-token-units", "32-token-units", "16-token-units"])
 def test_stream_tied_unit_scores(block_size):
     """Chunks whose queries are all zero give every unit the score 0 (Q-bar = 0): the lookup is then
     one full tie and takes the k_m lowest-indexed units, the tie rule of the memory lookup.  At these
     shapes the matrix-core attention selects the units itself in its prologue; 32-token units put
-    more than 512 units in a row (two keys per thread of the select).  The middle zero chunk is
-    checked against the oracle like any step, the last one also exactly: idx = 0 .. k_m - 1."""
+    more than 512 units in a row (two keys per thread of the select), 16-token units more than
+    1,024 (sixteen keys per thread, where the tie defeats the filter and the full radix select
+    runs).  The middle zero chunk is checked against the oracle like any step, the last one also
+    exactly: idx = 0 .. k_m - 1."""
     import dataclasses
     wl = dataclasses.replace(WORKLOADS["mistral7b-32k"], block_size=block_size)
     s = Synth(wl, 6)
@@ -132,9 +134,25 @@ def test_stream_tied_unit_scores(block_size):
         q[:, :, past:past + ln] = 0.0
     L = run_and_check(wl, 6, zero | {n // 2 + 1}, q, k, v)
     nu = O.partition(steps[-1][0], oparams(L.p)).n_units
-    assert nu > wl.topk and (block_size == 128 or nu > 512), nu
+    assert nu > wl.topk and (block_size == 128 or nu > 512) and (block_size != 16 or nu > 1024), nu
     idx = host(L.idx).reshape(wl.batch, wl.n_kv_heads, -1)[:, :, : wl.topk]
     assert (idx == np.arange(wl.topk)).all(), idx
+
+
+def test_stream_long_score_rows():
+    """Units of 16 tokens put up to 1,752 units in a score row, more than the attention's
+    two-keys-per-thread select holds: its prologue then loads sixteen keys per thread and filters
+    them first (per-thread maxima bound the k_m-th score).  Steps past 1,024 units are checked
+    against the oracle, selections exactly where the score gap allows."""
+    import dataclasses
+    wl = dataclasses.replace(WORKLOADS["mistral7b-32k"], block_size=16)
+    op = oparams(wl_params(wl))
+    steps = wl.step_starts()
+    long_rows = [si for si, (past, _) in enumerate(steps) if O.partition(past, op).n_units > 1024]
+    assert len(long_rows) >= 3, long_rows
+    s = Synth(wl, 7)
+    q, k, v = s.full("q"), s.full("k"), s.full("v")
+    run_and_check(wl, 7, {long_rows[0], long_rows[len(long_rows) // 2], long_rows[-1]}, q, k, v)
 
 
 def test_stream_paper_1m_settings():
