@@ -119,6 +119,13 @@ def test_varlen_chunks_bf16():
     _run("bf16", 4, 2, 128, 128, 1024, 128, 8, [0, 1024, 2560], n_q=512, n_steps=2)
 
 
+def test_varlen_chunks_long_rows_bf16():
+    # 16-token units: the deepest sequence's score rows pass 1,024 units (1,178 and more), so the
+    # attention selects with sixteen keys per thread, for a batch that also holds a sequence with
+    # a short row (490 units) and one with no units yet
+    _run("bf16", 4, 2, 128, 128, 1024, 16, 8, [0, 9000, 20000], n_q=512, n_steps=2)
+
+
 def test_varlen_decode_max_batch():
     # the largest batch a variable-length step takes: 64 sequences, 50 to 1,499 tokens deep
     _run("bf16", 2, 1, 64, 8, 64, 16, 3, [50 + 23 * i for i in range(64)], n_q=1, n_steps=2)
