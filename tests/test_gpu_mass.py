@@ -125,6 +125,17 @@ def test_unit_mass_in_step(case):
     _run(p, dtype, q, k, v, _steps(S, chunk), chunk, in_step=True)
 
 
+def test_unit_mass_in_step_long_rows():
+    # 64-token units past 65,920 prior tokens: the score rows hold more than 1,024 units (1,035 and
+    # 1,051 at the last two steps), where the attention selects with sixteen keys per thread; it
+    # writes the same per-tile partials
+    p = F.params(2, 1, 64, 64, 256, 64, 2, 4, "bf16")
+    S, chunk = 68000, 1024
+    assert O.partition(S - chunk, oparams(p)).n_units > 1024
+    q, k, v = rand_inputs(np.random.default_rng(1234), 2, 1, S, 64, "bf16")
+    _run(p, "bf16", q, k, v, _steps(S, chunk), chunk, in_step=True)
+
+
 def test_unit_mass_in_step_mean_repr():
     # the Mean Repr units (scored by the mean of their keys): the same attention tiles, so the
     # same partials; 128-token units after a 64-token I, the lookup larger than the unit count
