@@ -291,9 +291,10 @@ infllm_status infllm_unit_mass(const infllm_params* p, const infllm_memory* m, c
  *   3. relevance of every unit: scores [batch][Hkv][n_units(past_len)] float32;
  *   4. lookup of the k_m best: idx [batch][Hkv][k_m] int32 (as infllm_select_topk);
  *   5. attention (as infllm_chunk_attend) into out / lse.
- * With bf16 chunks (the matrix-core attention) and at most 1,024 units, stages 4
- * and 5 share one launch: the attention selects the units from the scores itself
- * and writes idx as stage 4 would (same entries, order and padding).
+ * With bf16 chunks (the matrix-core attention), at most 8,192 units and k_m at
+ * most 1,024, stages 4 and 5 share one launch: the attention selects the units
+ * from the scores itself and writes idx as stage 4 would (same entries, order
+ * and padding).
  * units_built is the number of units built by earlier steps (0 for the first
  * step); afterwards n_units(past_len) units are built.  Every stage is validated
  * before the first is enqueued. */
@@ -308,9 +309,10 @@ infllm_status infllm_step(const infllm_params* p, const infllm_memory* m, const 
  * (nullable) as infllm_unit_mass writes them for this step's q, idx and lse, with
  * the same decay and the same argument rules (lse is required when n_q, k_m > 0).
  * Where the matrix-core attention also selects the units (bf16 chunks, at most
- * 1,024 units) and l_I and l_bs are multiples of 64, the attention writes each
- * looked-up 64-key tile's per-row sum of P and its running maximum into the end
- * of the workspace, and one small launch after the merge forms the masses from
+ * 8,192 units, k_m at most 1,024) and l_I and l_bs are multiples of 64, the
+ * attention writes each looked-up 64-key tile's per-row sum of P and its running
+ * maximum into the end of the workspace, and one small launch after the merge
+ * forms the masses from
  * them and the merged lse (no second pass over the keys); otherwise the step is
  * followed by the unit-mass kernel.  The two agree to float32 rounding.
  * infllm_workspace_bytes covers the partials. */
