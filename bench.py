@@ -47,15 +47,15 @@ KERNEL_TRAFFIC = {
     # runs of `bench.py --legs 1m,decode --no-cpu-baseline --steps 1 --warmup 0`, averaged over the
     # replayed launches the bench line times
     "attend_mfma_llama3-8b-128k": {"src": {"attend_mfma.hip": "8e6f615f1b8b0f3845348431fc7e85216df7b7ee1dd5f879cd23492c919980f7", "launch.h": "773b89a4b862e0906d83400bc662d292d0f41bae789623c3fb8b00f10acda697"},
-                                   "fetch_kib": 20093.9, "write_kib": 16896.0},
+                                   "fetch_kib": 20095.6, "write_kib": 16896.0},
     "score_llama3-8b-128k": {"src": {"score.hip": "b863ba9bf6e01b4901383469e615c02c7ae9b482693bef88e3f29735e4666a13", "launch.h": "773b89a4b862e0906d83400bc662d292d0f41bae789623c3fb8b00f10acda697"},
                              "fetch_kib": 2086.6 + 2281.5, "write_kib": 64.0 + 34.3},
-    "append_llama3-8b-128k": {"src": {"append.hip": "fe44574fc83ade25154c0c6246e75f45770ecbba5020429ac57eca075d4f3464", "launch.h": "773b89a4b862e0906d83400bc662d292d0f41bae789623c3fb8b00f10acda697"},
-                              "fetch_kib": 5738.2, "write_kib": 6659.3},
+    "append_llama3-8b-128k": {"src": {"append.hip": "d09c349a86c28dba43f0fcae0b6c8675a8486c7e054e0404c7a79a8b140f5002", "launch.h": "773b89a4b862e0906d83400bc662d292d0f41bae789623c3fb8b00f10acda697"},
+                              "fetch_kib": 5717.6, "write_kib": 6659.0},
     "score_llama3-8b-1m": {"src": {"score.hip": "b863ba9bf6e01b4901383469e615c02c7ae9b482693bef88e3f29735e4666a13", "launch.h": "773b89a4b862e0906d83400bc662d292d0f41bae789623c3fb8b00f10acda697"},
                            "fetch_kib": 2086.5 + 16617.6, "write_kib": 64.0 + 282.8},
-    "append_llama3-8b-1m": {"src": {"append.hip": "fe44574fc83ade25154c0c6246e75f45770ecbba5020429ac57eca075d4f3464", "launch.h": "773b89a4b862e0906d83400bc662d292d0f41bae789623c3fb8b00f10acda697"},
-                            "fetch_kib": 5738.0, "write_kib": 6659.0},
+    "append_llama3-8b-1m": {"src": {"append.hip": "d09c349a86c28dba43f0fcae0b6c8675a8486c7e054e0404c7a79a8b140f5002", "launch.h": "773b89a4b862e0906d83400bc662d292d0f41bae789623c3fb8b00f10acda697"},
+                            "fetch_kib": 5717.6, "write_kib": 6659.0},
     "attend_decode": {"src": {"attend_decode.hip": "e9c010e0b521a9e279ded2a3f90fe08bc8e43dc66eb5d0d9b4d86bcbdbd07953", "launch.h": "773b89a4b862e0906d83400bc662d292d0f41bae789623c3fb8b00f10acda697"},
                       "fetch_kib": 270891.2, "write_kib": 544.1},
     "score_decode": {"src": {"score.hip": "b863ba9bf6e01b4901383469e615c02c7ae9b482693bef88e3f29735e4666a13", "launch.h": "773b89a4b862e0906d83400bc662d292d0f41bae789623c3fb8b00f10acda697"},

@@ -18,11 +18,11 @@
 // overwrite when the ring is large enough (checked on the host), so the two
 // latency-bound jobs overlap instead of running back to back.
 //
-// Scan block: one (sequence*kv head, 8-dim slice); 256 threads = 128 position
+// Scan block: one (sequence*kv head, 8-dim slice); 512 threads = 256 position
 // segments x 2 halves of 4 dims.  Each thread first issues every load of its
 // segment (kSeg positions: the group's query pieces, and in the streaming case
 // the running sums and keys of the tokens t = p - l_L), then sums in float64; a
-// DPP scan over each 32-lane half of a wave and an LDS pass over the 4 waves give
+// DPP scan over each 32-lane half of a wave and an LDS pass over the 8 waves give
 // the segment offsets, and each thread writes its kSeg ring rows.  (Per thread the
 // float64 work is a long dependent chain; 4 dims per thread keeps it short enough
 // that the scan ends with the copy and unit-construction blocks.)  Chunks of a few
@@ -36,10 +36,10 @@
 namespace infllm {
 namespace {
 
-constexpr int kThreads = 256;                  // threads of every block of the launch (one wave per SIMD:
+constexpr int kThreads = 512;                  // threads of every block of the launch (two waves per SIMD;
                                                // a scan thread keeps a whole segment's loads in flight)
 constexpr int kWaves = kThreads / 64;
-constexpr int kSeg = 4;                        // positions per thread per tile
+constexpr int kSeg = 2;                        // positions per thread per tile: a 512-position chunk is one tile
 constexpr int kTile = (kThreads / 2) * kSeg;   // positions per scan tile
 constexpr int kCopyPerThread = 4;              // 16-byte vectors per thread in copy blocks
 constexpr int kThinMaxQ = 8;                   // chunks this short take the one-thread-per-dim scan
@@ -178,8 +178,8 @@ __global__ void __launch_bounds__(kThreads) append_kernel(AppendArgs a, BuildArg
   if (blk < grid.n_qsum) {
     // ---- query-sum role (Mean Repr, which has no scan): the chunk's group-query
     // partial sums that unit scoring consumes
-    __shared__ QsumSmem<T> qsm;
-    qsum_block<T>((const T*)a.q, a.q_head_stride, a.n_q_heads, a.n_kv_heads, D, a.n_q, blk % grid.qsum_parts,
+    __shared__ QsumSmem<T, kThreads> qsm;
+    qsum_block<T, kThreads>((const T*)a.q, a.q_head_stride, a.n_q_heads, a.n_kv_heads, D, a.n_q, blk % grid.qsum_parts,
                   grid.qsum_parts, blk / grid.qsum_parts, qbar, qsm);
     return;
   }

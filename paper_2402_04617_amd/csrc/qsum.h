@@ -8,17 +8,18 @@
 
 namespace infllm {
 
-constexpr int kQsumThreads = 256;
+constexpr int kQsumThreads = 256;  // threads of the scoring kernels' query-sum blocks
 
-template <typename T>
+// NT: the block's thread count (all of them take part).
+template <typename T, int NT = kQsumThreads>
 struct QsumSmem {
-  float red[kQsumThreads * (16 / sizeof(T))];
+  float red[NT * (16 / sizeof(T))];
 };
 
-template <typename T>
+template <typename T, int NT = kQsumThreads>
 __device__ __forceinline__ void qsum_block(const T* __restrict__ q, int64_t q_head_stride, int n_q_heads,
                                            int n_kv_heads, int head_dim, int n_q, int part, int parts, int bg,
-                                           float* __restrict__ qbar_parts, QsumSmem<T>& sm) {
+                                           float* __restrict__ qbar_parts, QsumSmem<T, NT>& sm) {
   constexpr int kVec = 16 / sizeof(T);
   const int b = bg / n_kv_heads, g = bg - b * n_kv_heads;
   const int G = n_q_heads / n_kv_heads;
@@ -26,7 +27,7 @@ __device__ __forceinline__ void qsum_block(const T* __restrict__ q, int64_t q_he
   const int per = (rows + parts - 1) / parts;
   const int r0 = min(rows, part * per), r1 = min(rows, r0 + per);
   const int lanes_per_row = head_dim / kVec;
-  const int rgroups = kQsumThreads / lanes_per_row;
+  const int rgroups = NT / lanes_per_row;
   const int c = threadIdx.x % lanes_per_row;
   const int rg = threadIdx.x / lanes_per_row;
 
@@ -59,7 +60,7 @@ __device__ __forceinline__ void qsum_block(const T* __restrict__ q, int64_t q_he
 #pragma unroll
   for (int e = 0; e < kVec; ++e) sm.red[rg * head_dim + c * kVec + e] = acc[e];
   __syncthreads();
-  for (int d = threadIdx.x; d < head_dim; d += kQsumThreads) {
+  for (int d = threadIdx.x; d < head_dim; d += NT) {
     float s = 0.f;
     for (int j = 0; j < rgroups; ++j) s += sm.red[j * head_dim + d];
     qbar_parts[((int64_t)bg * parts + part) * head_dim + d] = s;
