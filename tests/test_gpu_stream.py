@@ -139,13 +139,15 @@ def test_stream_tied_unit_scores(block_size):
     assert (idx == np.arange(wl.topk)).all(), idx
 
 
-def test_stream_long_score_rows():
+@pytest.mark.parametrize("topk", [16, 600], ids=["k16", "k600"])
+def test_stream_long_score_rows(topk):
     """Units of 16 tokens put up to 1,752 units in a score row, more than the attention's
     two-keys-per-thread select holds: its prologue then loads sixteen keys per thread and filters
-    them first (per-thread maxima bound the k_m-th score).  Steps past 1,024 units are checked
-    against the oracle, selections exactly where the score gap allows."""
+    them first (per-thread maxima bound the k_m-th score); a lookup of more than 512 units skips the
+    filter and runs the radix select on all keys.  Steps past 1,024 units are checked against the
+    oracle, selections exactly where the score gap allows."""
     import dataclasses
-    wl = dataclasses.replace(WORKLOADS["mistral7b-32k"], block_size=16)
+    wl = dataclasses.replace(WORKLOADS["mistral7b-32k"], block_size=16, topk=topk)
     op = oparams(wl_params(wl))
     steps = wl.step_starts()
     long_rows = [si for si, (past, _) in enumerate(steps) if O.partition(past, op).n_units > 1024]
