@@ -50,8 +50,9 @@ __device__ __forceinline__ int block_scan(bool pred, int* wave_tot, int* total) 
   return off + pre;
 }
 
-// Radix-select path (see above); s, out: this row.
-__device__ void radix_select(const float* __restrict__ s, int n, int k_eff, int32_t* __restrict__ out,
+// Radix-select path (see above); s, out: this row.  (Unused by the attention
+// kernels that include this header.)
+[[maybe_unused]] __device__ void radix_select(const float* __restrict__ s, int n, int k_eff, int32_t* __restrict__ out,
                              int* wave_tot) {
   __shared__ uint32_t hist[256];
   __shared__ uint32_t sh_digit, sh_remaining;
