@@ -139,13 +139,14 @@ def test_stream_tied_unit_scores(block_size):
     assert (idx == np.arange(wl.topk)).all(), idx
 
 
-@pytest.mark.parametrize("topk", [16, 600], ids=["k16", "k600"])
-def test_stream_long_score_rows(topk):
+@pytest.mark.parametrize("topk,remap", [(16, False), (600, False), (16, True)], ids=["k16", "k600", "k16-remap"])
+def test_stream_long_score_rows(topk, remap):
     """Units of 16 tokens put up to 1,752 units in a score row, more than the attention's
     two-keys-per-thread select holds: its prologue then loads sixteen keys per thread and filters
     them first (per-thread maxima bound the k_m-th score); a lookup of more than 512 units skips the
-    filter and runs the radix select on all keys.  Steps past 1,024 units are checked against the
-    oracle, selections exactly where the score gap allows."""
+    filter and runs the radix select on all keys; under the positional remap the memory parts (I and
+    the units) select.  Steps past 1,024 units are checked against the oracle, selections exactly
+    where the score gap allows."""
     import dataclasses
     wl = dataclasses.replace(WORKLOADS["mistral7b-32k"], block_size=16, topk=topk)
     op = oparams(wl_params(wl))
@@ -154,7 +155,7 @@ def test_stream_long_score_rows(topk):
     assert len(long_rows) >= 3, long_rows
     s = Synth(wl, 7)
     q, k, v = s.full("q"), s.full("k"), s.full("v")
-    run_and_check(wl, 7, {long_rows[0], long_rows[len(long_rows) // 2], long_rows[-1]}, q, k, v)
+    run_and_check(wl, 7, {long_rows[0], long_rows[len(long_rows) // 2], long_rows[-1]}, q, k, v, remap=remap)
 
 
 def test_stream_paper_1m_settings():
